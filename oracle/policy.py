@@ -1,0 +1,347 @@
+"""TEST INFRASTRUCTURE — CPU oracle of SAECache's eviction hot path.
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import
+this module.  It shares no code with the HIP path and is deliberately plain:
+full sorts, Python dicts and literal loops over the paper's rules.
+
+One `OracleCache` object is one cache instance.  Its state follows the paper:
+
+* a pool of KV blocks, each routed to a queue (Sec. 3.1, queue routing) with a
+  token type tau(b) (Sec. 3.1: the type of the block's median token);
+* the block index of the prefix cache: content hash -> block (strict prefix
+  matching, Sec. 2.1);
+* ``recently_evicted``: content hash -> (tau, queue) of recent victims
+  (Algorithm 1, Add);
+* ``token_stats[tau].{evicted, miss_after_evict}`` (Algorithm 3) and
+  ``queue_hits[q]`` / ``queue_evictions[q]`` (Algorithm 2);
+* the learned parameters w_tau, alpha_q, mu_q, sigma_q, gamma.
+
+Readings of points where the paper is silent (each listed in the design doc):
+
+* A block is evictable iff it is valid, a leaf (no cached child) and
+  unreferenced: tail-first eviction (Sec. 2.1 figure b) of free blocks.
+* One eviction *decision* takes k victims from a snapshot: parameters and
+  ``now`` are fixed, and a parent that becomes a leaf is eligible only at the
+  next decision.  On a snapshot, k successive Evict() calls of Algorithm 1
+  equal "stage 1 from the evict-first queue by (num_tokens, id), then stage 2
+  by (P, id) over the other queues" (checked by `evict_sequential_literal`).
+  Ties are broken by block id.
+* ``recently_evicted`` keeps the victims of decision d while fewer than W
+  evictions happened after d (W = ghost window).  An entry is consumed by
+  the first Add() of its hash (counted once) and then forgotten.
+* The learners run once per decision in which floor(evictions / K) grew
+  (Algorithm 1's "every K evictions").  lambda = 0.99 decays a counter x to
+  floor(99 x / 100) exactly.
+"""
+import math
+
+import numpy as np
+
+from . import _native
+
+EVICT_FIRST, STRUCTURAL, LOGNORMAL, RECENCY = 0, 1, 2, 3
+N_TYPES = 5  # system, user, tool, response, cot — the order of Algorithm 3
+F32 = np.float32
+
+
+def block_type(counts):
+    """tau(b) from per-block token-type counts [n, 5] (Sec. 3.1: the type of the
+    median token).  Tokens are ranked by type in the order of Algorithm 3; the
+    median is the lower median, rank floor((n-1)/2); tau is the type holding it."""
+    counts = np.asarray(counts, np.int64)
+    n = counts.sum(axis=1)
+    m = (n - 1) // 2
+    cum = np.cumsum(counts, axis=1)
+    tau = np.zeros(len(counts), np.int32)
+    for i in range(len(counts)):
+        for t in range(N_TYPES):
+            if cum[i, t] > m[i]:
+                tau[i] = t
+                break
+    return tau
+
+
+def clamp(x, lo, hi):
+    return min(max(x, F32(lo)), F32(hi))
+
+
+class Params:
+    """Learned parameters and learner settings (Sec. 3.1, App. B)."""
+
+    def __init__(self, n_queues, w=1.0, alpha=1.0, mu=0.0, sigma=1.0, gamma=1.0,
+                 eta=0.01, T=1.0, beta=0.1, K=32, learn_w=True, learn_alpha=True):
+        def vec(v, n):
+            a = np.zeros(n, F32)
+            a[:] = np.resize(np.asarray(v, F32), n)
+            return a
+        self.w = vec(w, N_TYPES)
+        self.alpha = vec(alpha, n_queues)
+        self.mu = vec(mu, n_queues)
+        self.sigma = vec(sigma, n_queues)
+        self.gamma = F32(gamma)
+        self.eta = F32(eta)
+        self.T = F32(T)
+        self.beta = F32(beta)
+        self.K = int(K)
+        self.learn_w = bool(learn_w)
+        self.learn_alpha = bool(learn_alpha)
+
+
+class OracleCache:
+    def __init__(self, n_blocks, kinds, params, ghost_window=None):
+        N = int(n_blocks)
+        self.N = N
+        self.kind = [int(k) for k in kinds]
+        self.Q = len(self.kind)
+        assert sum(k == EVICT_FIRST for k in self.kind) <= 1
+        self.prm = params
+        self.W = N if ghost_window is None else int(ghost_window)
+        self.la = np.zeros(N, np.int32)
+        self.queue = np.zeros(N, np.int32)
+        self.tau = np.zeros(N, np.int32)
+        self.ntok = np.full(N, 16, np.int32)
+        self.ob = np.zeros(N, np.int32)
+        self.omax = np.zeros(N, np.int32)
+        self.valid = np.zeros(N, bool)
+        self.ref_count = np.zeros(N, np.int32)
+        self.child_count = np.zeros(N, np.int32)
+        self.parent = np.full(N, -1, np.int32)
+        self.hash = np.zeros(N, np.uint64)
+        self.access_count = np.zeros(N, np.int32)
+        self.index = {}
+        self.ghost = {}
+        self.evicted = [0] * N_TYPES
+        self.missed = [0] * N_TYPES
+        self.hits = [0] * self.Q
+        self.evictions = [0] * self.Q
+        self.ev_count = 0
+        self.pending = False
+        self.n_updates = 0
+
+    # ------------------------------------------------------------------ state
+    def bind(self, last_access, queue, tau, ntok, ob, omax, valid, ref_count,
+             parent, hashes, access_count=None):
+        """Set the whole pool; child counts follow from the parent links and the
+        index holds every valid block (vLLM's prefix cache)."""
+        self.la[:] = last_access
+        self.queue[:] = queue
+        self.tau[:] = tau
+        self.ntok[:] = ntok
+        self.ob[:] = ob
+        self.omax[:] = omax
+        self.valid[:] = np.asarray(valid, bool)
+        self.ref_count[:] = ref_count
+        self.parent[:] = parent
+        self.hash[:] = hashes
+        self.access_count[:] = 0 if access_count is None else access_count
+        self.child_count[:] = 0
+        for b in range(self.N):
+            p = int(self.parent[b])
+            if self.valid[b] and p >= 0:
+                self.child_count[p] += 1
+        self.index = {int(self.hash[b]): b for b in np.nonzero(self.valid)[0].tolist()}
+
+    def evictable(self):
+        return self.valid & (self.child_count == 0) & (self.ref_count == 0)
+
+    def ghost_live(self, entry):
+        return self.ev_count - entry[2] < self.W
+
+    # ---------------------------------------------------------- Eq. 1-3 keys
+    def keys(self, now):
+        p = self.prm
+        return _native.score_blocks(now, self.la, self.queue, self.tau, self.ntok, self.ob,
+                                    self.omax, self.kind, p.alpha, p.mu, p.sigma, p.w, p.gamma)
+
+    # ------------------------------------------------- selection and decision
+    def select_per_queue(self, now, k):
+        """For every queue, the min(k, |evictable in q|) evictable blocks with the
+        smallest (key, id), in that order."""
+        key, p = self.keys(now)
+        ev = self.evictable()
+        lists = []
+        for q in range(self.Q):
+            ids = np.nonzero(ev & (self.queue == q))[0]
+            order = np.lexsort((ids, key[ids]))
+            lists.append(ids[order[:k]].astype(np.int32))
+        return lists, key, p
+
+    def decide(self, lists, key, k):
+        """Algorithm 1 applied k times to one snapshot: stage 1 drains the
+        evict-first queue by (num_tokens, id); stage 2 takes the rest by
+        (P, id) over all other queues."""
+        stage1 = np.zeros(0, np.int32)
+        others = []
+        for q in range(self.Q):
+            if self.kind[q] == EVICT_FIRST:
+                stage1 = lists[q][:k]
+            else:
+                others.append(lists[q])
+        rest = k - len(stage1)
+        cand = np.concatenate(others) if others else np.zeros(0, np.int32)
+        order = np.lexsort((cand, key[cand]))
+        stage2 = cand[order[:rest]]
+        return np.concatenate([stage1, stage2]).astype(np.int32)
+
+    def evict_sequential_literal(self, now, k):
+        """Algorithm 1's Evict() called k times on one snapshot, written as the
+        paper states it (strict '<' scan), blocks visited in id order."""
+        key, _ = self.keys(now)
+        P = key.view(np.float32)
+        ev = self.evictable().copy()
+        out = []
+        for _ in range(k):
+            ef = [q for q in range(self.Q) if self.kind[q] == EVICT_FIRST]
+            victim = None
+            if ef:
+                best = None
+                for b in range(self.N):
+                    if ev[b] and self.queue[b] == ef[0]:
+                        if best is None or self.ntok[b] < best:
+                            best, victim = self.ntok[b], b
+            if victim is None:
+                best = math.inf
+                for b in range(self.N):
+                    if ev[b] and self.kind[self.queue[b]] != EVICT_FIRST:
+                        if victim is None or P[b] < best:
+                            best, victim = P[b], b
+            if victim is None:
+                break
+            out.append(victim)
+            ev[victim] = False
+        return np.array(out, np.int32)
+
+    def score_select(self, now, k, commit=False):
+        lists, key, p = self.select_per_queue(now, k)
+        decision = self.decide(lists, key, k)
+        if commit:
+            self.commit(decision)
+        return lists, key, decision
+
+    def commit(self, decision):
+        """Remove the victims: index erase, recently_evicted insert (Algorithm 1),
+        token_stats[tau].evicted++ (Algorithm 3), queue_evictions[q]++
+        (Algorithm 2), and the parent becomes a leaf when its last child goes."""
+        n = len(decision)
+        before = self.ev_count
+        stamp = before + n
+        for b in decision.tolist():
+            assert self.valid[b] and self.child_count[b] == 0 and self.ref_count[b] == 0
+            self.valid[b] = False
+            h = int(self.hash[b])
+            del self.index[h]
+            self.ghost[h] = (int(self.tau[b]), int(self.queue[b]), stamp)
+            self.evicted[self.tau[b]] += 1
+            self.evictions[self.queue[b]] += 1
+            par = int(self.parent[b])
+            if par >= 0:
+                self.child_count[par] -= 1
+        self.ev_count = stamp
+        K = self.prm.K
+        if K > 0 and stamp // K > before // K:
+            self.pending = True
+
+    # ------------------------------------------------------------ prefix match
+    def prefix_match(self, hashes, lens, now, touch=True, stats=True):
+        """Strict prefix matching (Sec. 2.1): match_len = number of leading
+        hashes found in the index.  All requests see the same snapshot; touches
+        (last_access = now, access_count += 1 per request hit) apply afterwards.
+        With stats, every hit block counts for queue_hits[queue(b)]."""
+        hashes = np.asarray(hashes, np.uint64)
+        n = len(lens)
+        mlen = np.zeros(n, np.int32)
+        matched = np.full(hashes.shape, -1, np.int32)
+        touched = []
+        for r in range(n):
+            m = 0
+            while m < lens[r]:
+                b = self.index.get(int(hashes[r, m]))
+                if b is None:
+                    break
+                matched[r, m] = b
+                m += 1
+            mlen[r] = m
+            for j in range(m):
+                b = matched[r, j]
+                if stats:
+                    self.hits[self.queue[b]] += 1
+                if touch:
+                    touched.append(b)
+        for b in touched:
+            self.la[b] = now
+            self.access_count[b] += 1
+        return mlen, matched
+
+    # ---------------------------------------------------------------- Add()
+    def insert(self, ids, hashes, parent, last_access, queue, tau, ntok, ob, omax):
+        """Algorithm 1 Add() for a batch of new blocks placed in free slots.
+        A hash still in recently_evicted counts one miss after eviction for the
+        type recorded at eviction, and leaves recently_evicted."""
+        for i, b in enumerate(np.asarray(ids).tolist()):
+            assert not self.valid[b]
+            h = int(hashes[i])
+            assert h not in self.index
+            self.valid[b] = True
+            self.hash[b] = h
+            self.parent[b] = parent[i]
+            self.la[b] = last_access[i]
+            self.queue[b] = queue[i]
+            self.tau[b] = tau[i]
+            self.ntok[b] = ntok[i]
+            self.ob[b] = ob[i]
+            self.omax[b] = omax[i]
+            self.child_count[b] = 0
+            self.ref_count[b] = 0
+            self.access_count[b] = 0
+            self.index[h] = b
+            g = self.ghost.pop(h, None)
+            if g is not None and self.ghost_live(g):
+                self.missed[g[0]] += 1
+        for i in range(len(ids)):
+            if parent[i] >= 0:
+                self.child_count[parent[i]] += 1
+
+    def ref(self, ids, delta):
+        np.add.at(self.ref_count, np.asarray(ids, np.int64), int(delta))
+
+    # ------------------------------------------------------------- learners
+    def token_weights(self):
+        """Algorithm 3 in fp32; counters decay by lambda = 99/100 (floored)."""
+        p = self.prm
+        for t in range(N_TYPES):
+            ev, mi = self.evicted[t], self.missed[t]
+            if ev > 10:
+                rate = F32(mi) / F32(ev)
+                p.w[t] = clamp(p.w[t] * (F32(1.0) + p.eta * rate), 0.1, 5.0)
+            self.evicted[t] = (99 * ev) // 100
+            self.missed[t] = (99 * mi) // 100
+
+    def queue_weights(self):
+        """Algorithm 2 in fp32 over every queue except the evict-first one."""
+        p = self.prm
+        for q in range(self.Q):
+            if self.kind[q] == EVICT_FIRST:
+                continue
+            h, e = self.hits[q], self.evictions[q]
+            if e > 5:
+                eff = F32(h) / F32(e)
+                target = F32(1.0) + eff / p.T
+                p.alpha[q] = clamp(p.alpha[q] + p.beta * (target - p.alpha[q]), 0.1, 3.0)
+            self.hits[q] = 0
+            self.evictions[q] = 0
+
+    def feedback(self, force=False):
+        if not (self.pending or force):
+            return False
+        if self.prm.learn_w:
+            self.token_weights()
+        if self.prm.learn_alpha:
+            self.queue_weights()
+        self.pending = False
+        self.n_updates += 1
+        return True
+
+    def counters(self):
+        return dict(evicted=list(self.evicted), missed=list(self.missed),
+                    hits=list(self.hits), evictions=list(self.evictions),
+                    ev_count=self.ev_count, pending=self.pending)
