@@ -1,0 +1,309 @@
+/*
+ * sae.h — C ABI of the MI355X (gfx950) hot path of SAECache's semantic-aware
+ * eviction for LLM prefix (KV-block) caches.
+ *
+ * Paper: "Not All Tokens Are Worth Caching: Learning Semantic-Aware Eviction
+ * for LLM Prefix Caches" (arXiv 2605.18825).  Section references below are to
+ * that paper.
+ *
+ * Conventions
+ *  - Every call returns sae_status (0 = SAE_OK, negative = error) and never
+ *    throws.  Argument validation is synchronous, happens before any launch
+ *    and has no side effect on failure; sae_last_error() gives the message.
+ *  - Pointers documented "device" are caller-owned device memory (e.g. torch
+ *    tensors); they must stay alive until the stream reaches the call.
+ *    Pointers documented "host" are read or written before the call returns.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *    null stream).  A context is not thread-safe: use it from one stream at a
+ *    time.  Calls that overlap on one context race.
+ *  - The context allocates all of its internal device memory in sae_create();
+ *    the hot calls (sae_prefix_match, sae_score_select, sae_feedback_update)
+ *    never allocate.
+ *  - Conditions found on the device (index full, o_b > o_max, a slot reused
+ *    while still valid, last_access in the future, ...) set bits of a device
+ *    status word, read by sae_poll_status().
+ *
+ * Instances
+ *  A context holds n_instances independent caches of blocks_per_instance
+ *  blocks each.  Block ids are instance-local, 0 .. blocks_per_instance-1;
+ *  per-block arrays are [n_instances * blocks_per_instance], instance-major.
+ *
+ * Per-block layout (structure of arrays, 10 bytes read by the scoring pass)
+ *  last_access  int32  time of last access in ticks (the configurations use
+ *                      1 tick = 1 ms); dt = max(now - last_access, 0)
+ *  meta         uint16 bit 0-2  queue q (< n_queues)
+ *                      bit 3-5  token type tau (SAE_TYPE_*), Sec. 3.1
+ *                      bit 6    valid   (block holds cached KV)
+ *                      bit 7    leaf    (no cached child block)
+ *                      bit 8    ref     (referenced by a running request)
+ *                      bit 9-12 num_tokens - 1 (Algorithm 1, stage 1 key)
+ *  off          uint32 bit 0-15 o_b, bit 16-31 o_max: block offset and the
+ *                      maximum offset in its request (Eq. 2)
+ *  hash         uint64 chained content hash (0 and 2^64-1 are reserved)
+ *  parent       int32  parent block id in the prefix tree, or -1
+ *  child_count  int32  number of cached children
+ *  ref_count    int32  number of running requests using the block
+ *  access_count int32  number of prefix-match hits
+ *  The library maintains valid/leaf/ref, child_count, access_count and
+ *  last_access (touch) as its calls change them.  meta must be 4-byte
+ *  aligned (bits are updated with 32-bit atomics).
+ */
+#ifndef SAE_H
+#define SAE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sae_ctx sae_ctx;
+typedef int32_t sae_status;
+typedef void *sae_stream_t; /* hipStream_t */
+
+enum {
+    SAE_OK = 0,
+    SAE_ERR_ARG = -1,   /* invalid argument; nothing was enqueued            */
+    SAE_ERR_ALLOC = -2, /* device allocation failed in sae_create            */
+    SAE_ERR_HIP = -3,   /* a HIP runtime call failed (message has the error) */
+    SAE_ERR_STATE = -4  /* call not valid in the context's state (no pool)   */
+};
+
+/* Queue kinds (Sec. 3.1, queue routing; the kind of each queue is data). */
+enum {
+    SAE_KIND_EVICT_FIRST = 0, /* drained first by num_tokens (Algorithm 1, stage 1) */
+    SAE_KIND_STRUCTURAL = 1,  /* position decay, Eq. 2                              */
+    SAE_KIND_LOGNORMAL = 2,   /* log-normal survival, Eq. 1 (chat / agentic)        */
+    SAE_KIND_RECENCY = 3      /* p = 1: token-weighted recency                      */
+};
+
+/* Token types, in the order of Algorithm 3. */
+enum {
+    SAE_TYPE_SYSTEM = 0,
+    SAE_TYPE_USER = 1,
+    SAE_TYPE_TOOL = 2,
+    SAE_TYPE_RESPONSE = 3,
+    SAE_TYPE_COT = 4,
+    SAE_N_TYPES = 5
+};
+
+#define SAE_MAX_QUEUES 8
+
+#define SAE_META_QUEUE_SHIFT 0
+#define SAE_META_TYPE_SHIFT 3
+#define SAE_META_VALID 0x0040u
+#define SAE_META_LEAF 0x0080u
+#define SAE_META_REF 0x0100u
+#define SAE_META_NTOK_SHIFT 9
+
+/* Device status bits (sae_poll_status). */
+enum {
+    SAE_ST_INDEX_FULL = 1u << 0,      /* an index insert found no free slot          */
+    SAE_ST_GHOST_FULL = 1u << 1,      /* a recently-evicted insert found no slot     */
+    SAE_ST_BAD_OFFSET = 1u << 2,      /* o_b > o_max (scored as o_b = o_max)         */
+    SAE_ST_FUTURE_ACCESS = 1u << 3,   /* last_access > now (scored as dt = 0)        */
+    SAE_ST_SLOT_BUSY = 1u << 4,       /* insert into a valid slot (insert skipped)   */
+    SAE_ST_SELECT_FALLBACK = 1u << 5, /* exact slow path of the pool scan was used   */
+    SAE_ST_BAD_BLOCK = 1u << 6        /* block id out of range (element skipped)     */
+};
+
+typedef struct {
+    int32_t n_instances;               /* >= 1                                         */
+    int32_t blocks_per_instance;       /* >= 1, <= 2^24                               */
+    int32_t n_queues;                  /* 1 .. 8                                       */
+    int32_t queue_kind[SAE_MAX_QUEUES];/* SAE_KIND_*; at most one evict-first queue    */
+    int32_t max_k;                     /* largest k of sae_score_select, 1 .. 8192     */
+    int32_t ghost_window;              /* W of recently_evicted (>= 1; 0 = blocks)     */
+    int32_t index_log2;                /* index slots per instance = 2^index_log2
+                                          (0 = smallest power of two >= 2 blocks)      */
+} sae_config;
+
+/* Learned parameters and learner settings (Sec. 3.1, App. B). */
+typedef struct {
+    float w[SAE_N_TYPES];          /* token-type weights w_tau (Eq. 3)              */
+    float alpha[SAE_MAX_QUEUES];   /* queue weights alpha_q (Eq. 3)                 */
+    float mu[SAE_MAX_QUEUES];      /* log-normal mu_q, in ln(ticks) (Eq. 1)          */
+    float sigma[SAE_MAX_QUEUES];   /* log-normal sigma_q > 0 (Eq. 1)                 */
+    float gamma;                   /* position decay power > 0 (Eq. 2)              */
+    float eta;                     /* token-weight learning rate (Algorithm 3)      */
+    float temperature;             /* T of Algorithm 2, > 0                         */
+    float beta;                    /* EMA factor of Algorithm 2                     */
+    int32_t K;                     /* learners run every K evictions (Algorithm 1)  */
+    uint32_t learn;                /* SAE_LEARN_* bits                              */
+} sae_params;
+
+enum { SAE_LEARN_TOKEN_WEIGHTS = 1u << 0, SAE_LEARN_QUEUE_WEIGHTS = 1u << 1 };
+
+/* Feedback counters of one instance (Algorithms 1-3). */
+typedef struct {
+    int32_t evicted[SAE_N_TYPES];     /* token_stats[tau].evicted                 */
+    int32_t missed[SAE_N_TYPES];      /* token_stats[tau].miss_after_evict        */
+    int32_t hits[SAE_MAX_QUEUES];     /* queue_hits[q]                            */
+    int32_t evictions[SAE_MAX_QUEUES];/* queue_evictions[q]                       */
+    int64_t eviction_count;           /* all evictions so far                     */
+    int32_t pending;                  /* learners due (eviction_count crossed K)  */
+    int32_t n_updates;                /* learner runs so far                      */
+} sae_counters;
+
+/* Caller-owned device arrays of the block pool (layout above). */
+typedef struct {
+    int32_t *last_access;
+    uint16_t *meta;
+    uint32_t *off;
+    uint64_t *hash;
+    int32_t *parent;
+    int32_t *child_count;
+    int32_t *ref_count;
+    int32_t *access_count;
+} sae_pool;
+
+const char *sae_status_str(sae_status s);
+/* Last error message of ctx (or of the last failed sae_create when ctx is NULL). */
+const char *sae_last_error(const sae_ctx *ctx);
+
+/* Create a context and allocate all of its device memory on the current
+ * device: index, recently-evicted table, per-instance parameters and counters,
+ * selection scratch.  *out is set only on success. */
+sae_status sae_create(const sae_config *cfg, sae_ctx **out);
+sae_status sae_destroy(sae_ctx *ctx);
+
+/* Attach the caller's pool arrays (all required, device, sized
+ * n_instances * blocks_per_instance).  Does not read them. */
+sae_status sae_bind_pool(sae_ctx *ctx, const sae_pool *pool);
+
+/* Parameters of one instance (inst >= 0) or of all (inst = -1); host struct
+ * copied before return.  sigma, gamma, temperature must be > 0. */
+sae_status sae_set_params(sae_ctx *ctx, int32_t inst, const sae_params *p, sae_stream_t stream);
+/* Read back parameters / counters of one instance; synchronizes `stream`. */
+sae_status sae_get_params(sae_ctx *ctx, int32_t inst, sae_params *out, sae_stream_t stream);
+sae_status sae_get_counters(sae_ctx *ctx, int32_t inst, sae_counters *out, sae_stream_t stream);
+/* Overwrite one instance's counters (checkpoint / resume). */
+sae_status sae_set_counters(sae_ctx *ctx, int32_t inst, const sae_counters *c, sae_stream_t stream);
+
+/* Block type tau(b) = type of the block's median token (Sec. 3.1), from
+ * per-block token-type counts: counts[n][5] uint8 (device), tau[n] uint8
+ * (device).  Tokens are ranked by type in SAE_TYPE order; the median is the
+ * lower median (rank floor((n_tokens - 1) / 2)). */
+sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_stream_t stream);
+
+/* Rebuild the block index (content hash -> block) from the hash of every
+ * valid block, and clear recently_evicted and all counters.  Use after
+ * filling the pool arrays directly.  Hashes of valid blocks must be distinct
+ * within an instance. */
+sae_status sae_index_build(sae_ctx *ctx, sae_stream_t stream);
+
+/*
+ * Algorithm 1, Add(b, h), for a batch of n new blocks placed in free slots.
+ *  inst[n]   device int32 instance of each block, or NULL (all instance 0)
+ *  ids[n]    device int32 instance-local block id (slot must not be valid)
+ *  hash[n], parent[n] (-1 = root), last_access[n]: device
+ *  meta[n]   device uint16: queue, type and num_tokens fields are used; the
+ *            library sets valid and leaf, clears ref
+ *  off[n]    device uint32 (o_b, o_max)
+ * Each block goes into the index.  A hash still in recently_evicted counts
+ * one miss after eviction for the type recorded at eviction (Algorithm 1,
+ * Add; Algorithm 3's miss_after_evict) and leaves recently_evicted.  Parents
+ * gain a child (and lose their leaf bit).  Hashes must be distinct and absent
+ * from the index.  Busy slots set SAE_ST_SLOT_BUSY and are skipped.
+ */
+sae_status sae_insert_blocks(sae_ctx *ctx, int32_t n, const int32_t *inst, const int32_t *ids,
+                             const uint64_t *hash, const int32_t *parent, const int32_t *last_access,
+                             const uint16_t *meta, const uint32_t *off, sae_stream_t stream);
+
+/* ref_count[b] += delta for n blocks (device inst[n] or NULL, ids[n]); the ref
+ * bit of meta follows ref_count > 0.  A referenced block is not evictable. */
+sae_status sae_ref_blocks(sae_ctx *ctx, int32_t n, const int32_t *inst, const int32_t *ids,
+                          int32_t delta, sae_stream_t stream);
+
+/* Flags of sae_prefix_match */
+enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1 };
+
+/*
+ * HOT 1 — batched strict prefix matching (Sec. 2.1: a later block is reusable
+ * only if every earlier block matches; blocks are identified by content hash).
+ *  hashes[n_req][max_len]  device uint64, request r's block hashes in order
+ *  lens[n_req]             device int32, 0 <= lens[r] <= max_len
+ *  inst[n_req]             device int32 or NULL (instance 0)
+ *  match_len[n_req]        device int32 out: number of leading hashes present
+ *                          in the index (the first miss ends the match)
+ *  matched_ids             device int32 [n_req][max_len] out or NULL: block id
+ *                          of each matched position, -1 elsewhere
+ * Every request sees the index as it was before the call.  SAE_PM_TOUCH sets
+ * last_access = now and adds 1 to access_count for every (request, matched
+ * block); SAE_PM_STATS adds every matched block to queue_hits[its queue]
+ * (Algorithm 2).  Without both flags the call is read-only.
+ */
+sae_status sae_prefix_match(sae_ctx *ctx, int32_t n_req, int32_t max_len, const uint64_t *hashes,
+                            const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
+                            int32_t *match_len, int32_t *matched_ids, sae_stream_t stream);
+
+/* Flags of sae_score_select */
+enum {
+    SAE_SS_COMMIT = 1u << 0,          /* evict the decision (see below)                  */
+    SAE_SS_ENGINE_SCAN = 1u << 1,     /* force the pool-scan engine                      */
+    SAE_SS_ENGINE_BATCHED = 1u << 2,  /* force the one-workgroup-per-instance engine     */
+    SAE_SS_FORCE_FALLBACK = 1u << 3   /* pool-scan engine: take its exact slow path      */
+};
+
+/*
+ * HOT 2 — score every block and select victims.
+ * Score (Sec. 3.1): dt = max(now - last_access, 0);
+ *   p_q(b) = 1 - F_LN(dt; mu_q, sigma_q)       log-normal queues (Eq. 1)
+ *          = 1 - (o_b / o_max)^gamma           structural queues (Eq. 2)
+ *          = 1                                 recency queues
+ *   P(b)   = alpha_q w_tau(b) p_q(b) / dt      (Eq. 3; dt = 0 gives +inf)
+ * evaluated in a fixed fp32 recipe (IEEE + - * /, fma, exact bit operations).
+ * An evict-first queue is ordered by num_tokens (Algorithm 1, stage 1).
+ * A block is evictable iff valid, leaf and unreferenced.
+ * Select: for every instance i and queue q, the c = min(k_i, #evictable in q)
+ * evictable blocks with the smallest (key, block id), ascending:
+ *   victims[i][q][0..c)  device int32, stride max_k per queue
+ *   scores[i][q][0..c)   device float (P, or num_tokens for evict-first) or NULL
+ *   count[i][q]          device int32
+ * Decision (Algorithm 1 applied k_i times to this snapshot): the evict-first
+ * list first, then the other queues merged by (P, id):
+ *   decision[i][0..d)    device int32, stride max_k;  decision_count[i] = d
+ * k_i = k_per_inst[i] (device int32, or NULL for k); 0 <= k_i <= max_k.
+ * SAE_SS_COMMIT then evicts the decision: valid bit cleared, index entry
+ * removed, hash -> (tau, queue) recorded in recently_evicted, evicted[tau] and
+ * queue_evictions[q] incremented, parent's child_count decremented (a parent
+ * left with no child becomes a leaf, eligible from the next call), and the
+ * learners are marked due when eviction_count crosses a multiple of K.
+ * Ties are broken by block id.  Results do not depend on the engine.
+ */
+sae_status sae_score_select(sae_ctx *ctx, int32_t now, int32_t k, const int32_t *k_per_inst,
+                            uint32_t flags, int32_t *victims, float *scores, int32_t *count,
+                            int32_t *decision, int32_t *decision_count, sae_stream_t stream);
+
+/* Flags of sae_feedback_update */
+enum { SAE_FB_FORCE = 1u << 0 };
+
+/*
+ * HOT 3 — eviction-feedback learners of every instance whose learners are due
+ * (or all with SAE_FB_FORCE), in fp32:
+ *  Algorithm 3 (token weights): for each tau with evicted > 10,
+ *    w_tau <- clamp(w_tau * (1 + eta * missed / evicted), 0.1, 5.0);
+ *    then evicted <- floor(0.99 evicted), missed <- floor(0.99 missed)
+ *    (0.99 applied exactly as 99/100).
+ *  Algorithm 2 (queue weights): for each queue but the evict-first one with
+ *    evictions > 5, alpha_q <- clamp(alpha_q + beta (1 + (hits/evictions)/T
+ *    - alpha_q), 0.1, 3.0); then hits and evictions reset to 0.
+ * Each algorithm runs only if its SAE_LEARN_* bit is set.
+ */
+sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream);
+
+/* OR of the device status bits since the last poll (then cleared);
+ * synchronizes `stream`. */
+sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
+
+/* Per-kernel timing of the pool-scan engine's scoring pass: when enabled,
+ * HIP events bracket every launch of that kernel on the call's stream.
+ * sae_profile_read returns the summed milliseconds and launch count since the
+ * last read (synchronizes) and resets them. */
+sae_status sae_profile_enable(sae_ctx *ctx, int32_t enable);
+sae_status sae_profile_read(sae_ctx *ctx, double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAE_H */

@@ -1,0 +1,519 @@
+// Block index, recently_evicted, prefix matching, Add() and eviction commit.
+//
+// Block index: open addressing, linear probing, 16-byte slots {hash, id} in
+// HBM; 0 marks an empty slot and 2^64-1 a deleted one.  Lookups run in
+// kernels that never write the index, so every request of a prefix-match batch
+// sees the same index.
+//
+// recently_evicted (Algorithm 1): victims are appended to a ring of
+// W + max_k entries in eviction order, each stamped with the eviction count
+// right after its decision; an entry is live while fewer than W evictions
+// followed it.  A hash table maps a content hash to its ring entry.  When a
+// ring slot is reused, its old entry (always expired) leaves the table first;
+// removals and inserts run in separate kernels.
+#include "sae_internal.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == h) return tab[s].id;
+        if (v == SAE_EMPTY_HASH) return -1;
+        s = (s + 1) & mask;
+    }
+    return -1;
+}
+
+__device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsigned long long h, int32_t id)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
+            unsigned long long old = atomicCAS(&tab[s].hash, v, h);
+            if (old == v) {
+                tab[s].id = id;
+                return true;
+            }
+            continue;  // lost the slot: look at it again
+        }
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+__device__ __forceinline__ void index_erase(IndexSlot *tab, uint32_t mask, unsigned long long h)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == h) {
+            tab[s].hash = SAE_TOMB_HASH;
+            return;
+        }
+        if (v == SAE_EMPTY_HASH) return;
+        s = (s + 1) & mask;
+    }
+}
+
+// Live, unconsumed ghost entry of hash h: table slot index, or -1.
+__device__ __forceinline__ int ghost_find(const GhostSlot *tab, uint32_t mask, const GhostEntry *ring,
+                                          unsigned long long h, long long ev_now, int W, uint32_t *ring_pos)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == SAE_EMPTY_HASH) return -1;
+        if (v == h) {
+            uint32_t r = tab[s].ring;
+            const GhostEntry &g = ring[r];
+            if (g.hash == h && !(g.tq & 0x100u) && ev_now - g.stamp < (long long)W) {
+                *ring_pos = r;
+                return (int)s;
+            }
+        }
+        s = (s + 1) & mask;
+    }
+    return -1;
+}
+
+__device__ __forceinline__ void ghost_remove(GhostSlot *tab, uint32_t mask, unsigned long long h, uint32_t ring_pos)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == SAE_EMPTY_HASH) return;
+        if (v == h && tab[s].ring == ring_pos) {
+            tab[s].hash = SAE_TOMB_HASH;
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+}
+
+__device__ __forceinline__ bool ghost_insert(GhostSlot *tab, uint32_t mask, unsigned long long h, uint32_t ring_pos)
+{
+    uint32_t s = hash_home(h, mask);
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        unsigned long long v = tab[s].hash;
+        if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
+            unsigned long long old = atomicCAS(&tab[s].hash, v, h);
+            if (old == v) {
+                tab[s].ring = ring_pos;
+                return true;
+            }
+            continue;
+        }
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+// ---------------------------------------------------------------------------
+// tau(b): type holding the lower-median token when tokens are ranked by type.
+__global__ void k_block_type(const uint8_t *counts, long long n, uint8_t *tau)
+{
+    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint8_t *cb = counts + i * SAE_N_TYPES;
+    int total = 0;
+    for (int t = 0; t < SAE_N_TYPES; ++t) total += cb[t];
+    int m = (total - 1) >> 1;  // total >= 1 expected; total 0 gives type 0
+    int run = 0, ty = 0;
+    for (int t = 0; t < SAE_N_TYPES; ++t) {
+        run += cb[t];
+        if (run > m) {
+            ty = t;
+            break;
+        }
+    }
+    tau[i] = (uint8_t)ty;
+}
+
+// Clear index, recently_evicted and counters.
+__global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
+{
+    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    long long nidx = (long long)c.n_inst * ((long long)c.index_mask + 1);
+    if (i < nidx) {
+        c.index[i].hash = SAE_EMPTY_HASH;
+        c.index[i].id = -1;
+    }
+    if (!clear_ghost_and_counters) return;
+    long long ngt = (long long)c.n_inst * ((long long)c.ghost_mask + 1);
+    if (i < ngt) {
+        c.gtab[i].hash = SAE_EMPTY_HASH;
+        c.gtab[i].ring = 0;
+    }
+    long long nring = (long long)c.n_inst * c.ring_cap;
+    if (i < nring) {
+        c.ring[i].hash = 0;
+        c.ring[i].stamp = 0;
+        c.ring[i].tq = 0;
+    }
+    if (i < c.n_inst) {
+        InstState &s = c.state[i];
+        for (int t = 0; t < SAE_N_TYPES; ++t) s.evicted[t] = s.missed[t] = 0;
+        for (int q = 0; q < SAE_MAX_QUEUES; ++q) s.hits[q] = s.evictions[q] = 0;
+        s.ev_count = 0;
+        s.ev_before = 0;
+        s.pending = 0;
+        s.n_updates = 0;
+        s.last_d = 0;
+    }
+}
+
+// Insert every valid block's hash into its instance's index.
+__global__ void k_index_fill(DevCtx c)
+{
+    long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    long long total = (long long)c.n_inst * c.N;
+    if (g >= total) return;
+    if (!(c.meta[g] & SAE_META_VALID)) return;
+    int inst = (int)(g / c.N);
+    int32_t b = (int32_t)(g - (long long)inst * c.N);
+    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+    if (!index_insert(tab, c.index_mask, c.hash[g], b)) set_status(c.status, SAE_ST_INDEX_FULL);
+}
+
+// Rebuild recently_evicted from the ring (drops tombstones).
+__global__ void k_ghost_clear(DevCtx c)
+{
+    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    long long ngt = (long long)c.n_inst * ((long long)c.ghost_mask + 1);
+    if (i < ngt) c.gtab[i].hash = SAE_EMPTY_HASH;
+}
+__global__ void k_ghost_fill(DevCtx c)
+{
+    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    long long nring = (long long)c.n_inst * c.ring_cap;
+    if (i >= nring) return;
+    int inst = (int)(i / c.ring_cap);
+    uint32_t r = (uint32_t)(i - (long long)inst * c.ring_cap);
+    GhostEntry g = c.ring[i];
+    if (g.hash == 0 || (g.tq & 0x100u)) return;
+    if (c.state[inst].ev_count - g.stamp >= (long long)c.W) return;
+    GhostSlot *tab = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    if (!ghost_insert(tab, c.ghost_mask, g.hash, r)) set_status(c.status, SAE_ST_GHOST_FULL);
+}
+
+// ---------------------------------------------------------------------------
+// Add(), phase 1: write the block, index it, consume its recently_evicted entry.
+__global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t *ids, const uint64_t *hash,
+                           const int32_t *parent, const int32_t *la, const uint16_t *meta, const uint32_t *off,
+                           uint8_t *skip)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int inst = inst_a ? inst_a[i] : 0;
+    int32_t b = ids[i];
+    if (inst < 0 || inst >= c.n_inst || b < 0 || b >= c.N) {
+        skip[i] = 1;
+        set_status(c.status, SAE_ST_BAD_BLOCK);
+        return;
+    }
+    long long g = (long long)inst * c.N + b;
+    if (c.meta[g] & SAE_META_VALID) {
+        skip[i] = 1;
+        set_status(c.status, SAE_ST_SLOT_BUSY);
+        return;
+    }
+    skip[i] = 0;
+    unsigned long long h = hash[i];
+    uint32_t m = meta[i] & (0x7u | (0x7u << 3) | (0xFu << 9));
+    c.meta[g] = (uint16_t)(m | SAE_META_VALID | SAE_META_LEAF);
+    c.la[g] = la[i];
+    c.off[g] = off[i];
+    c.hash[g] = h;
+    c.parent[g] = parent[i];
+    c.child_count[g] = 0;
+    c.ref_count[g] = 0;
+    c.access_count[g] = 0;
+    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+    if (!index_insert(tab, c.index_mask, h, b)) set_status(c.status, SAE_ST_INDEX_FULL);
+    // recently_evicted: a hit counts one miss after eviction (Algorithm 1, Add)
+    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    uint32_t rp = 0;
+    int s = ghost_find(gt, c.ghost_mask, ring, h, c.state[inst].ev_count, c.W, &rp);
+    if (s >= 0) {
+        if (atomicCAS(&gt[s].hash, h, SAE_TOMB_HASH) == h) {
+            uint32_t old = atomicOr(&ring[rp].tq, 0x100u);
+            if (!(old & 0x100u)) atomicAdd(&c.state[inst].missed[(old & 7u) % SAE_N_TYPES], 1);
+        }
+    }
+}
+
+// Add(), phase 2: parents gain a child and stop being leaves.
+__global__ void k_insert_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *parent, const uint8_t *skip)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n || skip[i]) return;
+    int inst = inst_a ? inst_a[i] : 0;
+    int32_t p = parent[i];
+    if (p < 0) return;
+    if (p >= c.N) {
+        set_status(c.status, SAE_ST_BAD_BLOCK);
+        return;
+    }
+    long long gp = (long long)inst * c.N + p;
+    atomicAdd(&c.child_count[gp], 1);
+    meta_and(c.meta, gp, (uint32_t)(~SAE_META_LEAF) & 0xFFFFu);
+}
+
+__global__ void k_ref_a(DevCtx c, int n, const int32_t *inst_a, const int32_t *ids, int32_t delta)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int inst = inst_a ? inst_a[i] : 0;
+    int32_t b = ids[i];
+    if (inst < 0 || inst >= c.n_inst || b < 0 || b >= c.N) {
+        set_status(c.status, SAE_ST_BAD_BLOCK);
+        return;
+    }
+    atomicAdd(&c.ref_count[(long long)inst * c.N + b], delta);
+}
+__global__ void k_ref_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *ids)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int inst = inst_a ? inst_a[i] : 0;
+    int32_t b = ids[i];
+    if (inst < 0 || inst >= c.n_inst || b < 0 || b >= c.N) return;
+    long long g = (long long)inst * c.N + b;
+    if (c.ref_count[g] > 0) meta_or(c.meta, g, SAE_META_REF);
+    else meta_and(c.meta, g, (uint32_t)(~SAE_META_REF) & 0xFFFFu);
+}
+
+// ---------------------------------------------------------------------------
+// Strict prefix matching, one wave per request.  Lanes probe 64 consecutive
+// hashes; the lowest missing lane ends the match and no later chunk is probed.
+__global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, int max_len, const uint64_t *hashes,
+                                                          const int32_t *lens, const int32_t *inst_a, int32_t now,
+                                                          uint32_t flags, int32_t *match_len, int32_t *matched_ids)
+{
+    const int lane = (int)__lane_id();
+    const int r = (blockIdx.x * blockDim.x + threadIdx.x) / SAE_WAVE;
+    if (r >= n_req) return;  // the whole wave leaves together
+    const int inst = inst_a ? inst_a[r] : 0;
+    int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
+    int len = lens[r];
+    if (len > max_len) len = max_len;
+    if (len < 0) len = 0;
+    if (inst < 0 || inst >= c.n_inst) {
+        if (mid)
+            for (int j = lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
+        if (lane == 0) {
+            match_len[r] = 0;
+            set_status(c.status, SAE_ST_BAD_BLOCK);
+        }
+        return;
+    }
+    const IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+    const long long base = (long long)inst * c.N;
+    const uint64_t *hr = hashes + (long long)r * max_len;
+    uint32_t qcount[SAE_MAX_QUEUES];
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) qcount[q] = 0;
+    int m = 0;
+    int j0 = 0;
+    for (; j0 < len; j0 += SAE_WAVE) {
+        const int j = j0 + lane;
+        int32_t id = (j < len) ? index_find(tab, c.index_mask, hr[j]) : -1;
+        const bool miss = (j < len) && (id < 0);
+        const unsigned long long mm = __ballot(miss);
+        const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
+        const int lim = min(first, len - j0);
+        const bool hit = lane < lim;
+        int q = 0;
+        if (hit) {
+            const long long g = base + id;
+            q = meta_queue(c.meta[g]);
+            if (flags & SAE_PM_TOUCH) {
+                c.la[g] = now;
+                atomicAdd(&c.access_count[g], 1);
+            }
+            if (mid) mid[j] = id;
+        } else if (mid && j < max_len) {
+            mid[j] = -1;
+        }
+        if (flags & SAE_PM_STATS) {
+#pragma unroll
+            for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) qcount[qq] += (uint32_t)__popcll(__ballot(hit && q == qq));
+        }
+        m = j0 + lim;
+        if (mm) {
+            j0 += SAE_WAVE;
+            break;
+        }
+    }
+    if (mid)
+        for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
+    if (lane == 0) {
+        match_len[r] = m;
+        if (flags & SAE_PM_STATS) {
+#pragma unroll
+            for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
+                if (qq < c.Q && qcount[qq]) atomicAdd(&c.state[inst].hits[qq], (int)qcount[qq]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Commit, phase 1: per victim, free the block, erase its index entry, count
+// it (Algorithm 3 evicted[tau], Algorithm 2 queue_evictions[q]), update its
+// parent, and drop the expired ring entry its ring slot will take.
+__global__ void k_commit_a(DevCtx c, const int32_t *decision)
+{
+    const int inst = blockIdx.y;
+    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    const InstState &s = c.state[inst];
+    const int d = s.last_d;
+    if (j >= d) return;
+    int32_t v = decision[(long long)inst * c.max_k + j];
+    if (v < 0 || v >= c.N) {
+        set_status(c.status, SAE_ST_BAD_BLOCK);
+        return;
+    }
+    const long long g = (long long)inst * c.N + v;
+    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
+    GhostEntry old = ring[rp];
+    if (old.hash != 0 && !(old.tq & 0x100u)) ghost_remove(gt, c.ghost_mask, old.hash, rp);
+
+    uint32_t m = c.meta[g];
+    atomicAdd(&c.state[inst].evicted[meta_type(m) % SAE_N_TYPES], 1);
+    atomicAdd(&c.state[inst].evictions[meta_queue(m)], 1);
+    meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
+    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+    index_erase(tab, c.index_mask, c.hash[g]);
+    int32_t p = c.parent[g];
+    if (p >= 0 && p < c.N) {
+        long long gp = (long long)inst * c.N + p;
+        int before = atomicSub(&c.child_count[gp], 1);
+        if (before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
+    }
+}
+
+// Commit, phase 2: record the victims in recently_evicted.
+__global__ void k_commit_b(DevCtx c, const int32_t *decision)
+{
+    const int inst = blockIdx.y;
+    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    const InstState &s = c.state[inst];
+    const int d = s.last_d;
+    if (j >= d) return;
+    int32_t v = decision[(long long)inst * c.max_k + j];
+    if (v < 0 || v >= c.N) return;
+    const long long g = (long long)inst * c.N + v;
+    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
+    uint32_t m = c.meta[g];
+    unsigned long long h = c.hash[g];
+    GhostEntry e;
+    e.hash = h;
+    e.stamp = s.ev_before + d;
+    e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3);
+    e.pad_ = 0;
+    ring[rp] = e;
+    if (!ghost_insert(gt, c.ghost_mask, h, rp)) set_status(c.status, SAE_ST_GHOST_FULL);
+}
+
+inline unsigned grid_for(long long n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
+}  // namespace
+
+hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_block_type, dim3(grid_for(n)), dim3(kThreads), 0, s, counts, (long long)n, tau);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_build(const DevCtx &c, hipStream_t s)
+{
+    long long nidx = (long long)c.n_inst * ((long long)c.index_mask + 1);
+    long long ngt = (long long)c.n_inst * ((long long)c.ghost_mask + 1);
+    long long nring = (long long)c.n_inst * c.ring_cap;
+    long long n = nidx;
+    if (ngt > n) n = ngt;
+    if (nring > n) n = nring;
+    if (c.n_inst > n) n = c.n_inst;
+    hipLaunchKernelGGL(k_clear_all, dim3(grid_for(n)), dim3(kThreads), 0, s, c, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_rebuild(const DevCtx &c, hipStream_t s)
+{
+    long long nidx = (long long)c.n_inst * ((long long)c.index_mask + 1);
+    hipLaunchKernelGGL(k_clear_all, dim3(grid_for(nidx)), dim3(kThreads), 0, s, c, 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_ghost_rebuild(const DevCtx &c, hipStream_t s)
+{
+    long long ngt = (long long)c.n_inst * ((long long)c.ghost_mask + 1);
+    hipLaunchKernelGGL(k_ghost_clear, dim3(grid_for(ngt)), dim3(kThreads), 0, s, c);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    long long nring = (long long)c.n_inst * c.ring_cap;
+    hipLaunchKernelGGL(k_ghost_fill, dim3(grid_for(nring)), dim3(kThreads), 0, s, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_insert(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids, const uint64_t *hash,
+                         const int32_t *parent, const int32_t *la, const uint16_t *meta, const uint32_t *off,
+                         uint8_t *skip, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_insert_a, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, ids, hash, parent, la, meta,
+                       off, skip);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_insert_b, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, parent, (const uint8_t *)skip);
+    return hipGetLastError();
+}
+
+hipError_t launch_ref(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids, int32_t delta, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_ref_a, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, ids, delta);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_ref_b, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, ids);
+    return hipGetLastError();
+}
+
+hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, const uint64_t *hashes,
+                               const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
+                               int32_t *match_len, int32_t *matched_ids, hipStream_t s)
+{
+    if (n_req <= 0) return hipSuccess;
+    long long threads = (long long)n_req * SAE_WAVE;
+    hipLaunchKernelGGL(k_prefix_match, dim3(grid_for(threads)), dim3(kThreads), 0, s, c, n_req, max_len, hashes, lens,
+                       inst, now, flags, match_len, matched_ids);
+    return hipGetLastError();
+}
+
+hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s)
+{
+    dim3 grid((unsigned)((c.max_k + kThreads - 1) / kThreads), (unsigned)c.n_inst);
+    hipLaunchKernelGGL(k_commit_a, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_commit_b, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
+    return hipGetLastError();
+}

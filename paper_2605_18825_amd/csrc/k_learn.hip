@@ -1,0 +1,58 @@
+// Eviction-feedback learners (Algorithms 2 and 3), one thread per instance.
+// fp32 throughout, in the order the algorithms state them (built with
+// -ffp-contract=off, so no operation is fused).
+#include "sae_internal.h"
+
+namespace {
+
+__device__ __forceinline__ float clampf(float x, float lo, float hi) { return fminf(fmaxf(x, lo), hi); }
+
+__global__ void k_feedback(DevCtx c, uint32_t flags)
+{
+    int inst = blockIdx.x * blockDim.x + threadIdx.x;
+    if (inst >= c.n_inst) return;
+    InstState &s = c.state[inst];
+    if (!s.pending && !(flags & SAE_FB_FORCE)) return;
+    if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
+        // Algorithm 3: raise the weight of types evicted too aggressively;
+        // both counters decay by lambda = 0.99, applied as floor(99 x / 100).
+        for (int t = 0; t < SAE_N_TYPES; ++t) {
+            int32_t ev = s.evicted[t], mi = s.missed[t];
+            if (ev > 10) {
+                float rate = (float)mi / (float)ev;
+                float step = s.eta * rate;
+                float grow = 1.0f + step;
+                s.w[t] = clampf(s.w[t] * grow, 0.1f, 5.0f);
+            }
+            s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
+            s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
+        }
+    }
+    if (s.learn & SAE_LEARN_QUEUE_WEIGHTS) {
+        // Algorithm 2: EMA of the queue weight toward 1 + efficiency / T.
+        for (int q = 0; q < c.Q; ++q) {
+            if (c.kind[q] == SAE_KIND_EVICT_FIRST) continue;
+            int32_t h = s.hits[q], e = s.evictions[q];
+            if (e > 5) {
+                float eff = (float)h / (float)e;
+                float target = 1.0f + eff / s.T;
+                float diff = target - s.alpha[q];
+                float stepq = s.beta * diff;
+                s.alpha[q] = clampf(s.alpha[q] + stepq, 0.1f, 3.0f);
+            }
+            s.hits[q] = 0;
+            s.evictions[q] = 0;
+        }
+    }
+    s.pending = 0;
+    s.n_updates += 1;
+}
+
+}  // namespace
+
+hipError_t launch_feedback(const DevCtx &c, uint32_t flags, hipStream_t s)
+{
+    unsigned grid = (unsigned)((c.n_inst + 63) / 64);
+    hipLaunchKernelGGL(k_feedback, dim3(grid), dim3(64), 0, s, c, flags);
+    return hipGetLastError();
+}

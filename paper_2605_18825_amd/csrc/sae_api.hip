@@ -1,0 +1,521 @@
+// C ABI of libsae: context lifetime, argument validation and launch
+// sequencing.  No call allocates device memory after sae_create.
+#include <stddef.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "sae_internal.h"
+
+struct sae_ctx {
+    sae_config cfg;
+    DevCtx dc;
+    bool pool_bound = false;
+    int device = 0;
+    std::string err;
+    long long index_slots = 0, ghost_slots = 0;
+    double index_tombs = 0, ghost_tombs = 0;
+    uint8_t *skip = nullptr;
+    long long skip_cap = 0;
+    std::vector<void *> allocs;
+    bool prof = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_used;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_free;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+sae_status fail(sae_ctx *c, sae_status s, const std::string &msg)
+{
+    if (c) c->err = msg;
+    else g_err = msg;
+    return s;
+}
+
+sae_status hip_fail(sae_ctx *c, hipError_t e, const char *what)
+{
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    return fail(c, SAE_ERR_HIP, m);
+}
+
+template <typename T>
+bool dev_alloc(sae_ctx *c, T **p, size_t count)
+{
+    size_t bytes = count * sizeof(T);
+    if (bytes == 0) bytes = 256;
+    void *q = nullptr;
+    if (hipMalloc(&q, bytes) != hipSuccess) return false;
+    if (hipMemset(q, 0, bytes) != hipSuccess) {
+        (void)hipFree(q);
+        return false;
+    }
+    c->allocs.push_back(q);
+    *p = static_cast<T *>(q);
+    return true;
+}
+
+int log2_ceil(long long x)
+{
+    int l = 0;
+    while ((1ll << l) < x) ++l;
+    return l;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+void default_params(InstState &s, int max_k)
+{
+    memset(&s, 0, sizeof(s));
+    for (int t = 0; t < SAE_N_TYPES; ++t) s.w[t] = 1.0f;
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+        s.alpha[q] = 1.0f;
+        s.mu[q] = 0.0f;
+        s.sigma[q] = 1.0f;
+    }
+    s.gamma = 1.0f;
+    s.eta = 0.01f;
+    s.T = 1.0f;
+    s.beta = 0.1f;
+    s.K = max_k;
+    s.learn = SAE_LEARN_TOKEN_WEIGHTS | SAE_LEARN_QUEUE_WEIGHTS;
+}
+
+hipStream_t S(sae_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+sae_status check_inst(sae_ctx *c, int32_t inst, bool allow_all)
+{
+    if (inst == -1 && allow_all) return SAE_OK;
+    if (inst < 0 || inst >= c->cfg.n_instances) return fail(c, SAE_ERR_ARG, "instance out of range");
+    return SAE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sae_status_str(sae_status s)
+{
+    switch (s) {
+    case SAE_OK: return "ok";
+    case SAE_ERR_ARG: return "invalid argument";
+    case SAE_ERR_ALLOC: return "device allocation failed";
+    case SAE_ERR_HIP: return "HIP runtime error";
+    case SAE_ERR_STATE: return "invalid state";
+    default: return "unknown status";
+    }
+}
+
+const char *sae_last_error(const sae_ctx *ctx) { return ctx ? ctx->err.c_str() : g_err.c_str(); }
+
+sae_status sae_create(const sae_config *cfg, sae_ctx **out)
+{
+    if (!cfg || !out) return fail(nullptr, SAE_ERR_ARG, "cfg and out must be non-NULL");
+    const sae_config &k = *cfg;
+    if (k.n_instances < 1 || k.n_instances > 65535) return fail(nullptr, SAE_ERR_ARG, "n_instances must be in 1..65535");
+    if (k.blocks_per_instance < 1 || k.blocks_per_instance > (1 << 24))
+        return fail(nullptr, SAE_ERR_ARG, "blocks_per_instance must be in 1..2^24");
+    if (k.n_queues < 1 || k.n_queues > SAE_MAX_QUEUES) return fail(nullptr, SAE_ERR_ARG, "n_queues must be in 1..8");
+    if (k.max_k < 1 || k.max_k > 8192) return fail(nullptr, SAE_ERR_ARG, "max_k must be in 1..8192");
+    if (k.ghost_window < 0) return fail(nullptr, SAE_ERR_ARG, "ghost_window must be >= 0");
+    if (k.index_log2 < 0 || k.index_log2 > 30) return fail(nullptr, SAE_ERR_ARG, "index_log2 must be in 0..30");
+    int n_ef = 0;
+    for (int q = 0; q < k.n_queues; ++q) {
+        if (k.queue_kind[q] < SAE_KIND_EVICT_FIRST || k.queue_kind[q] > SAE_KIND_RECENCY)
+            return fail(nullptr, SAE_ERR_ARG, "unknown queue kind");
+        n_ef += (k.queue_kind[q] == SAE_KIND_EVICT_FIRST);
+    }
+    if (n_ef > 1) return fail(nullptr, SAE_ERR_ARG, "at most one evict-first queue");
+
+    sae_ctx *c = new sae_ctx();
+    c->cfg = k;
+    (void)hipGetDevice(&c->device);
+    DevCtx &d = c->dc;
+    memset(&d, 0, sizeof(d));
+    d.n_inst = k.n_instances;
+    d.N = k.blocks_per_instance;
+    d.Q = k.n_queues;
+    d.max_k = k.max_k;
+    d.ef_queue = -1;
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) d.kind[q] = (q < k.n_queues) ? k.queue_kind[q] : SAE_KIND_RECENCY;
+    for (int q = 0; q < k.n_queues; ++q)
+        if (k.queue_kind[q] == SAE_KIND_EVICT_FIRST) d.ef_queue = q;
+    d.W = k.ghost_window ? k.ghost_window : k.blocks_per_instance;
+    d.ring_cap = d.W + d.max_k;
+    int il = k.index_log2 ? k.index_log2 : log2_ceil(2ll * d.N);
+    if (il < 6) il = 6;
+    if ((1ll << il) < (long long)d.N + 1) {
+        delete c;
+        return fail(nullptr, SAE_ERR_ARG, "index_log2 too small for blocks_per_instance");
+    }
+    int gl = log2_ceil(2ll * d.ring_cap);
+    if (gl < 6) gl = 6;
+    c->index_slots = 1ll << il;
+    c->ghost_slots = 1ll << gl;
+    d.index_mask = (uint32_t)(c->index_slots - 1);
+    d.ghost_mask = (uint32_t)(c->ghost_slots - 1);
+    long long cc = 8ll * d.max_k;
+    if (cc < 32768) cc = 32768;
+    if (cc > d.N) cc = d.N;
+    d.cand_cap = (int32_t)cc;
+
+    const long long I = d.n_inst, Q = d.Q;
+    bool ok = dev_alloc(c, &d.state, I) && dev_alloc(c, &d.status, 1) &&
+              dev_alloc(c, &d.index, I * c->index_slots) && dev_alloc(c, &d.ring, I * d.ring_cap) &&
+              dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) &&
+              dev_alloc(c, &d.shist, I * Q * SAE_BINS) && dev_alloc(c, &d.n_ev, I * Q) &&
+              dev_alloc(c, &d.n_cand, I * Q) && dev_alloc(c, &d.cand, I * Q * d.cand_cap) &&
+              dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
+              dev_alloc(c, &d.done, I) && dev_alloc(c, &c->skip, I * d.N);
+    if (!ok) {
+        for (void *p : c->allocs) (void)hipFree(p);
+        delete c;
+        return fail(nullptr, SAE_ERR_ALLOC, "hipMalloc failed in sae_create");
+    }
+    c->skip_cap = I * d.N;
+    std::vector<InstState> init((size_t)I);
+    for (auto &s : init) default_params(s, d.max_k);
+    hipError_t e = hipMemcpy(d.state, init.data(), sizeof(InstState) * I, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        for (void *p : c->allocs) (void)hipFree(p);
+        delete c;
+        return hip_fail(nullptr, e, "sae_create init");
+    }
+    *out = c;
+    return SAE_OK;
+}
+
+sae_status sae_destroy(sae_ctx *c)
+{
+    if (!c) return SAE_OK;
+    (void)hipDeviceSynchronize();
+    for (auto &p : c->prof_used) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    for (auto &p : c->prof_free) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    for (void *p : c->allocs) (void)hipFree(p);
+    delete c;
+    return SAE_OK;
+}
+
+sae_status sae_bind_pool(sae_ctx *c, const sae_pool *p)
+{
+    if (!c || !p) return fail(c, SAE_ERR_ARG, "ctx and pool must be non-NULL");
+    if (!p->last_access || !p->meta || !p->off || !p->hash || !p->parent || !p->child_count || !p->ref_count ||
+        !p->access_count)
+        return fail(c, SAE_ERR_ARG, "every pool array must be non-NULL");
+    if (!aligned(p->last_access, 16) || !aligned(p->off, 16) || !aligned(p->meta, 8) || !aligned(p->hash, 8) ||
+        !aligned(p->parent, 4) || !aligned(p->child_count, 4) || !aligned(p->ref_count, 4) ||
+        !aligned(p->access_count, 4))
+        return fail(c, SAE_ERR_ARG, "pool alignment: last_access/off 16 B, meta/hash 8 B, others 4 B");
+    DevCtx &d = c->dc;
+    d.la = p->last_access;
+    d.meta = p->meta;
+    d.off = p->off;
+    d.hash = reinterpret_cast<unsigned long long *>(p->hash);
+    d.parent = p->parent;
+    d.child_count = p->child_count;
+    d.ref_count = p->ref_count;
+    d.access_count = p->access_count;
+    c->pool_bound = true;
+    return SAE_OK;
+}
+
+sae_status sae_set_params(sae_ctx *c, int32_t inst, const sae_params *p, sae_stream_t stream)
+{
+    if (!c || !p) return fail(c, SAE_ERR_ARG, "ctx and params must be non-NULL");
+    if (check_inst(c, inst, true) != SAE_OK) return SAE_ERR_ARG;
+    for (int q = 0; q < c->dc.Q; ++q)
+        if (!(p->sigma[q] > 0.0f)) return fail(c, SAE_ERR_ARG, "sigma must be > 0");
+    if (!(p->gamma > 0.0f) || !(p->temperature > 0.0f)) return fail(c, SAE_ERR_ARG, "gamma and temperature must be > 0");
+    if (p->K < 0) return fail(c, SAE_ERR_ARG, "K must be >= 0");
+    InstState h;
+    memset(&h, 0, sizeof(h));
+    memcpy(h.w, p->w, sizeof(h.w));
+    memcpy(h.alpha, p->alpha, sizeof(h.alpha));
+    memcpy(h.mu, p->mu, sizeof(h.mu));
+    memcpy(h.sigma, p->sigma, sizeof(h.sigma));
+    h.gamma = p->gamma;
+    h.eta = p->eta;
+    h.T = p->temperature;
+    h.beta = p->beta;
+    h.K = p->K;
+    h.learn = p->learn;
+    const size_t nbytes = offsetof(InstState, evicted);
+    int lo = inst < 0 ? 0 : inst, hi = inst < 0 ? c->dc.n_inst : inst + 1;
+    for (int i = lo; i < hi; ++i) {
+        hipError_t e = hipMemcpyAsync(c->dc.state + i, &h, nbytes, hipMemcpyHostToDevice, S(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "sae_set_params");
+    }
+    hipError_t e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_set_params sync");
+    return SAE_OK;
+}
+
+sae_status sae_get_params(sae_ctx *c, int32_t inst, sae_params *out, sae_stream_t stream)
+{
+    if (!c || !out) return fail(c, SAE_ERR_ARG, "ctx and out must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    InstState h;
+    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_get_params");
+    memcpy(out->w, h.w, sizeof(out->w));
+    memcpy(out->alpha, h.alpha, sizeof(out->alpha));
+    memcpy(out->mu, h.mu, sizeof(out->mu));
+    memcpy(out->sigma, h.sigma, sizeof(out->sigma));
+    out->gamma = h.gamma;
+    out->eta = h.eta;
+    out->temperature = h.T;
+    out->beta = h.beta;
+    out->K = h.K;
+    out->learn = h.learn;
+    return SAE_OK;
+}
+
+sae_status sae_get_counters(sae_ctx *c, int32_t inst, sae_counters *out, sae_stream_t stream)
+{
+    if (!c || !out) return fail(c, SAE_ERR_ARG, "ctx and out must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    InstState h;
+    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_get_counters");
+    memcpy(out->evicted, h.evicted, sizeof(out->evicted));
+    memcpy(out->missed, h.missed, sizeof(out->missed));
+    memcpy(out->hits, h.hits, sizeof(out->hits));
+    memcpy(out->evictions, h.evictions, sizeof(out->evictions));
+    out->eviction_count = h.ev_count;
+    out->pending = h.pending;
+    out->n_updates = h.n_updates;
+    return SAE_OK;
+}
+
+sae_status sae_set_counters(sae_ctx *c, int32_t inst, const sae_counters *in, sae_stream_t stream)
+{
+    if (!c || !in) return fail(c, SAE_ERR_ARG, "ctx and counters must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    InstState h;
+    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_set_counters read");
+    memcpy(h.evicted, in->evicted, sizeof(h.evicted));
+    memcpy(h.missed, in->missed, sizeof(h.missed));
+    memcpy(h.hits, in->hits, sizeof(h.hits));
+    memcpy(h.evictions, in->evictions, sizeof(h.evictions));
+    h.ev_count = in->eviction_count;
+    h.pending = in->pending;
+    h.n_updates = in->n_updates;
+    e = hipMemcpyAsync(c->dc.state + inst, &h, sizeof(h), hipMemcpyHostToDevice, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_set_counters write");
+    return SAE_OK;
+}
+
+sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_stream_t stream)
+{
+    if (n < 0 || (n > 0 && (!counts || !tau))) return fail(nullptr, SAE_ERR_ARG, "counts/tau must be non-NULL, n >= 0");
+    hipError_t e = launch_block_type(counts, n, tau, S(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "sae_block_type");
+    return SAE_OK;
+}
+
+sae_status sae_index_build(sae_ctx *c, sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
+    hipError_t e = launch_index_build(c->dc, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_index_build");
+    c->index_tombs = 0;
+    c->ghost_tombs = 0;
+    return SAE_OK;
+}
+
+sae_status sae_insert_blocks(sae_ctx *c, int32_t n, const int32_t *inst, const int32_t *ids, const uint64_t *hash,
+                             const int32_t *parent, const int32_t *last_access, const uint16_t *meta,
+                             const uint32_t *off, sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
+    if (n < 0 || n > c->skip_cap) return fail(c, SAE_ERR_ARG, "n must be in 0..n_instances*blocks_per_instance");
+    if (n == 0) return SAE_OK;
+    if (!ids || !hash || !parent || !last_access || !meta || !off)
+        return fail(c, SAE_ERR_ARG, "ids, hash, parent, last_access, meta, off must be non-NULL");
+    hipError_t e = launch_insert(c->dc, n, inst, ids, hash, parent, last_access, meta, off, c->skip, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_insert_blocks");
+    c->ghost_tombs += n;
+    if (c->ghost_tombs > 0.25 * (double)c->ghost_slots) {
+        e = launch_ghost_rebuild(c->dc, S(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "ghost rebuild");
+        c->ghost_tombs = 0;
+    }
+    return SAE_OK;
+}
+
+sae_status sae_ref_blocks(sae_ctx *c, int32_t n, const int32_t *inst, const int32_t *ids, int32_t delta,
+                          sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
+    if (n < 0) return fail(c, SAE_ERR_ARG, "n must be >= 0");
+    if (n == 0) return SAE_OK;
+    if (!ids) return fail(c, SAE_ERR_ARG, "ids must be non-NULL");
+    hipError_t e = launch_ref(c->dc, n, inst, ids, delta, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_ref_blocks");
+    return SAE_OK;
+}
+
+sae_status sae_prefix_match(sae_ctx *c, int32_t n_req, int32_t max_len, const uint64_t *hashes, const int32_t *lens,
+                            const int32_t *inst, int32_t now, uint32_t flags, int32_t *match_len,
+                            int32_t *matched_ids, sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
+    if (n_req < 0 || max_len < 0) return fail(c, SAE_ERR_ARG, "n_req and max_len must be >= 0");
+    if (flags & ~(uint32_t)(SAE_PM_TOUCH | SAE_PM_STATS)) return fail(c, SAE_ERR_ARG, "unknown prefix-match flag");
+    if (n_req == 0) return SAE_OK;
+    if (max_len < 1 || !hashes || !lens || !match_len)
+        return fail(c, SAE_ERR_ARG, "hashes, lens, match_len must be non-NULL and max_len >= 1");
+    if ((long long)n_req * SAE_WAVE > 0x7FFFFFFFll) return fail(c, SAE_ERR_ARG, "n_req too large");
+    hipError_t e = launch_prefix_match(c->dc, n_req, max_len, hashes, lens, inst, now, flags, match_len,
+                                       matched_ids, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_prefix_match");
+    return SAE_OK;
+}
+
+sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k_per_inst, uint32_t flags,
+                            int32_t *victims, float *scores, int32_t *count, int32_t *decision,
+                            int32_t *decision_count, sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
+    const uint32_t known = SAE_SS_COMMIT | SAE_SS_ENGINE_SCAN | SAE_SS_ENGINE_BATCHED | SAE_SS_FORCE_FALLBACK;
+    if (flags & ~known) return fail(c, SAE_ERR_ARG, "unknown score-select flag");
+    if ((flags & SAE_SS_ENGINE_SCAN) && (flags & SAE_SS_ENGINE_BATCHED))
+        return fail(c, SAE_ERR_ARG, "choose at most one engine");
+    if (!k_per_inst && (k < 0 || k > c->dc.max_k)) return fail(c, SAE_ERR_ARG, "k must be in 0..max_k");
+    if (!victims || !count || !decision || !decision_count)
+        return fail(c, SAE_ERR_ARG, "victims, count, decision, decision_count must be non-NULL");
+    bool batched;
+    if (flags & SAE_SS_ENGINE_BATCHED) {
+        if (!batched_engine_fits(c->dc))
+            return fail(c, SAE_ERR_ARG, "batched engine needs <= 65536 blocks per instance and Q*max_k to fit LDS");
+        batched = true;
+    } else if (flags & (SAE_SS_ENGINE_SCAN | SAE_SS_FORCE_FALLBACK)) {
+        batched = false;
+    } else {
+        batched = batched_engine_fits(c->dc) && (c->dc.n_inst >= 32 || c->dc.N <= 16384);
+    }
+    SelectArgs a;
+    a.now = now;
+    a.k = k;
+    a.k_per_inst = k_per_inst;
+    a.flags = flags;
+    a.victims = victims;
+    a.scores = scores;
+    a.count = count;
+    a.decision = decision;
+    a.decision_count = decision_count;
+    hipStream_t s = S(stream);
+    hipError_t e;
+    if (batched) {
+        e = launch_select_batched(c->dc, a, s);
+    } else {
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (c->prof) {
+            if (c->prof_free.empty()) {
+                hipEvent_t x, y;
+                if (hipEventCreate(&x) != hipSuccess || hipEventCreate(&y) != hipSuccess)
+                    return fail(c, SAE_ERR_HIP, "hipEventCreate");
+                c->prof_free.push_back({x, y});
+            }
+            auto pr = c->prof_free.back();
+            c->prof_free.pop_back();
+            c->prof_used.push_back(pr);
+            e0 = pr.first;
+            e1 = pr.second;
+        }
+        e = launch_select_scan(c->dc, a, s, e0, e1);
+        if (e == hipSuccess) e = launch_merge(c->dc, a, s);
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "sae_score_select");
+    if (flags & SAE_SS_COMMIT) {
+        e = launch_commit(c->dc, a, s);
+        if (e != hipSuccess) return hip_fail(c, e, "commit");
+        double d = (double)c->dc.max_k;
+        c->index_tombs += d;
+        c->ghost_tombs += d;
+        if (c->index_tombs > 0.25 * (double)(c->index_slots - c->dc.N)) {
+            e = launch_index_rebuild(c->dc, s);
+            if (e != hipSuccess) return hip_fail(c, e, "index rebuild");
+            c->index_tombs = 0;
+        }
+        if (c->ghost_tombs > 0.25 * (double)c->ghost_slots) {
+            e = launch_ghost_rebuild(c->dc, s);
+            if (e != hipSuccess) return hip_fail(c, e, "ghost rebuild");
+            c->ghost_tombs = 0;
+        }
+    }
+    return SAE_OK;
+}
+
+sae_status sae_feedback_update(sae_ctx *c, uint32_t flags, sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (flags & ~(uint32_t)SAE_FB_FORCE) return fail(c, SAE_ERR_ARG, "unknown feedback flag");
+    hipError_t e = launch_feedback(c->dc, flags, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_feedback_update");
+    return SAE_OK;
+}
+
+sae_status sae_poll_status(sae_ctx *c, sae_stream_t stream, uint32_t *bits)
+{
+    if (!c || !bits) return fail(c, SAE_ERR_ARG, "ctx and bits must be non-NULL");
+    uint32_t h = 0;
+    hipError_t e = hipMemcpyAsync(&h, c->dc.status, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e == hipSuccess) e = hipMemsetAsync(c->dc.status, 0, sizeof(uint32_t), S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_poll_status");
+    *bits = h;
+    return SAE_OK;
+}
+
+sae_status sae_profile_enable(sae_ctx *c, int32_t enable)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    c->prof = enable != 0;
+    return SAE_OK;
+}
+
+sae_status sae_profile_read(sae_ctx *c, double *ms, int64_t *launches)
+{
+    if (!c || !ms || !launches) return fail(c, SAE_ERR_ARG, "ctx, ms, launches must be non-NULL");
+    double tot = 0;
+    int64_t n = 0;
+    for (auto &p : c->prof_used) {
+        hipError_t e = hipEventSynchronize(p.second);
+        if (e != hipSuccess) return hip_fail(c, e, "sae_profile_read");
+        float t = 0;
+        e = hipEventElapsedTime(&t, p.first, p.second);
+        if (e != hipSuccess) return hip_fail(c, e, "sae_profile_read");
+        tot += t;
+        ++n;
+        c->prof_free.push_back(p);
+    }
+    c->prof_used.clear();
+    *ms = tot;
+    *launches = n;
+    return SAE_OK;
+}
+
+}  // extern "C"

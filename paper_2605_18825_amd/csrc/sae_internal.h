@@ -1,0 +1,329 @@
+// Internal definitions shared by the HIP translation units of libsae.
+// Target: gfx950 (CDNA4), wave64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sae.h"
+
+#define SAE_WAVE 64
+#define SAE_EMPTY_HASH 0ull
+#define SAE_TOMB_HASH 0xFFFFFFFFFFFFFFFFull
+#define SAE_MAX_PROBES 65536
+
+// Radix digits of the selection: 11 bits -> 2048 bins.
+#define SAE_DIGIT_BITS 11
+#define SAE_BINS (1 << SAE_DIGIT_BITS)
+
+// ----------------------------------------------------------------------------
+// Per-instance device state: learned parameters, learner settings and the
+// feedback counters of Algorithms 1-3.
+struct InstState {
+    float w[SAE_N_TYPES];
+    float alpha[SAE_MAX_QUEUES];
+    float mu[SAE_MAX_QUEUES];
+    float sigma[SAE_MAX_QUEUES];
+    float gamma, eta, T, beta;
+    int32_t K;
+    uint32_t learn;
+    int32_t evicted[SAE_N_TYPES];
+    int32_t missed[SAE_N_TYPES];
+    int32_t hits[SAE_MAX_QUEUES];
+    int32_t evictions[SAE_MAX_QUEUES];
+    long long ev_count;   // evictions so far
+    long long ev_before;  // ev_count before the last committed decision
+    int32_t pending;      // learners due
+    int32_t n_updates;
+    int32_t last_d;       // size of the last committed decision
+    int32_t pad_;
+};
+
+// Open-addressing slot of the block index: content hash -> block id.
+struct IndexSlot {
+    unsigned long long hash;  // SAE_EMPTY_HASH, SAE_TOMB_HASH or a content hash
+    int32_t id;
+    int32_t pad_;
+};
+
+// recently_evicted: a ring in eviction order plus a hash table into it.
+struct GhostEntry {
+    unsigned long long hash;  // 0 when the ring slot was never written
+    long long stamp;          // eviction_count right after the entry's decision
+    uint32_t tq;              // tau | queue << 3 | consumed << 8
+    uint32_t pad_;
+};
+struct GhostSlot {
+    unsigned long long hash;
+    uint32_t ring;  // ring position of the entry
+    uint32_t pad_;
+};
+
+// Everything a kernel needs about a context, passed by value.
+struct DevCtx {
+    int32_t n_inst, N, Q, max_k;
+    int32_t kind[SAE_MAX_QUEUES];
+    int32_t ef_queue;  // index of the evict-first queue or -1
+    int32_t W;         // ghost window
+    int32_t ring_cap;  // W + max_k
+    uint32_t index_mask, ghost_mask;
+    int32_t cand_cap;  // candidate capacity per (instance, queue), scan engine
+    // pool (caller-owned)
+    int32_t *la;
+    uint16_t *meta;
+    uint32_t *off;
+    unsigned long long *hash;
+    int32_t *parent;
+    int32_t *child_count;
+    int32_t *ref_count;
+    int32_t *access_count;
+    // context-owned
+    InstState *state;
+    uint32_t *status;
+    IndexSlot *index;     // [n_inst][index_mask + 1]
+    GhostEntry *ring;     // [n_inst][ring_cap]
+    GhostSlot *gtab;      // [n_inst][ghost_mask + 1]
+    uint32_t *thr;        // [n_inst][Q] candidate key bound (scan engine)
+    uint32_t *shist;      // [n_inst][Q][SAE_BINS] sampled key histogram
+    uint32_t *n_ev;       // [n_inst][Q] evictable blocks
+    uint32_t *n_cand;     // [n_inst][Q] candidates emitted
+    unsigned long long *cand;  // [n_inst][Q][cand_cap] (key << 32 | id)
+    unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
+    int32_t *sel_count;        // [n_inst][Q]
+    uint32_t *done;            // [n_inst] last-workgroup counters
+};
+
+// ----------------------------------------------------------------------------
+// Meta field access.
+__device__ __forceinline__ int meta_queue(uint32_t m) { return (int)(m & 7u); }
+__device__ __forceinline__ int meta_type(uint32_t m) { return (int)((m >> 3) & 7u); }
+__device__ __forceinline__ int meta_ntok(uint32_t m) { return (int)((m >> 9) & 15u) + 1; }
+__device__ __forceinline__ bool meta_evictable(uint32_t m)
+{
+    return (m & (SAE_META_VALID | SAE_META_LEAF | SAE_META_REF)) == (SAE_META_VALID | SAE_META_LEAF);
+}
+
+// 32-bit atomics on the 16-bit meta of block `b` (meta base is 4-byte aligned).
+__device__ __forceinline__ void meta_and(uint16_t *meta, long long b, uint32_t mask16)
+{
+    uint32_t *w = reinterpret_cast<uint32_t *>(meta + (b & ~1ll));
+    uint32_t sh = (uint32_t)(b & 1) * 16u;
+    atomicAnd(w, ~((~mask16 & 0xFFFFu) << sh));
+}
+__device__ __forceinline__ void meta_or(uint16_t *meta, long long b, uint32_t bits16)
+{
+    uint32_t *w = reinterpret_cast<uint32_t *>(meta + (b & ~1ll));
+    uint32_t sh = (uint32_t)(b & 1) * 16u;
+    atomicOr(w, (bits16 & 0xFFFFu) << sh);
+}
+
+__device__ __forceinline__ void set_status(uint32_t *status, uint32_t bits)
+{
+    if (bits) atomicOr(status, bits);
+}
+
+// Hash -> home slot.
+__device__ __forceinline__ uint32_t hash_home(unsigned long long h, uint32_t mask)
+{
+    unsigned long long z = h ^ (h >> 31);
+    z *= 0x9E3779B97F4A7C15ull;
+    return (uint32_t)(z >> 32) & mask;
+}
+
+// ----------------------------------------------------------------------------
+// Deterministic fp32 realisation of Eq. 1-3.  Only IEEE binary32 + - * /,
+// fmaf, int<->float conversion and exact bit operations, in a fixed order
+// (built with -ffp-contract=off).  The same recipe is evaluated on the CPU by
+// the test oracle; both are transcriptions of one specification, so the
+// selection -- an argmin decided in fp32 -- comes out identical.
+//   ln:   x = 2^e m, m in (sqrt(1/2), sqrt(2)]; ln m = 2 atanh(s), s = (m-1)/(m+1),
+//         atanh series through s^9/9; ln 2 = head (15 bits) + tail (Cody-Waite).
+//   exp:  n = rint(y / ln 2), r = y - n ln 2 (head, then tail), Taylor series of
+//         e^r through r^7/7!, times 2^n built in the exponent field;
+//         0 below y = -86, +inf above 88.
+//   erfc: x >= 0: t exp(-x^2 + g(t)), t = 1/(1 + x/2), g of degree 9 with the
+//         Chebyshev-fitted coefficients of Press et al., Numerical Recipes
+//         (2nd ed., Sec. 6.2); x^2 kept as an exact head + tail.
+//         erfc(0) = 1, erfc(x >= 9) = 0.
+namespace dsr {
+
+__device__ __forceinline__ float pow2i(int n) { return __uint_as_float((uint32_t)(n + 127) << 23); }
+
+// e^r, |r| <= ~0.35
+__device__ __forceinline__ float exp_series(float r)
+{
+    float p = 1.0f / 5040.0f;
+    p = fmaf(p, r, 1.0f / 720.0f);
+    p = fmaf(p, r, 1.0f / 120.0f);
+    p = fmaf(p, r, 1.0f / 24.0f);
+    p = fmaf(p, r, 1.0f / 6.0f);
+    p = fmaf(p, r, 0.5f);
+    p = fmaf(p, r, 1.0f);
+    p = fmaf(p, r, 1.0f);
+    return p;
+}
+
+constexpr float kLn2Hi = 0x1.62e400p-1f;
+constexpr float kLn2Lo = 0x1.7f7d1cp-20f;
+constexpr float kInvLn2 = 0x1.715476p+0f;
+constexpr float kRound = 0x1.8p+23f;
+constexpr float kSqrt2 = 0x1.6a09e6p+0f;
+
+__device__ __forceinline__ float exp(float y)
+{
+    if (y < -86.0f) return 0.0f;
+    if (y > 88.0f) return __uint_as_float(0x7F800000u);
+    float n = (y * kInvLn2 + kRound) - kRound;
+    float r = fmaf(-n, kLn2Hi, y);
+    r = fmaf(-n, kLn2Lo, r);
+    return exp_series(r) * pow2i((int)n);
+}
+
+__device__ __forceinline__ float ln(float x)
+{
+    uint32_t bits = __float_as_uint(x);
+    int e = (int)(bits >> 23) - 127;
+    uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
+    if (mb > 0x3FB504F3u) {
+        mb -= 0x00800000u;
+        e += 1;
+    }
+    float f = __uint_as_float(mb) - 1.0f;
+    float s = f / (2.0f + f);
+    float z = s * s;
+    float q = fmaf(z, 1.0f / 9.0f, 1.0f / 7.0f);
+    q = fmaf(z, q, 1.0f / 5.0f);
+    q = fmaf(z, q, 1.0f / 3.0f);
+    float s2 = s + s;
+    float lnm = fmaf(s2 * z, q, s2);
+    float ef = (float)e;
+    return fmaf(ef, kLn2Hi, fmaf(ef, kLn2Lo, lnm));
+}
+
+__device__ __forceinline__ float erfc(float x)
+{
+    if (x == 0.0f) return 1.0f;
+    if (!(x < 9.0f)) return 0.0f;
+    float t = 1.0f / fmaf(0.5f, x, 1.0f);
+    float g = 0.17087277f;
+    g = fmaf(g, t, -0.82215223f);
+    g = fmaf(g, t, 1.48851587f);
+    g = fmaf(g, t, -1.13520398f);
+    g = fmaf(g, t, 0.27886807f);
+    g = fmaf(g, t, -0.18628806f);
+    g = fmaf(g, t, 0.09678418f);
+    g = fmaf(g, t, 0.37409196f);
+    g = fmaf(g, t, 1.00002368f);
+    g = fmaf(g, t, -1.26551223f);
+    float xx = x * x;
+    float xxl = fmaf(x, x, -xx);
+    float n = ((g - xx) * kInvLn2 + kRound) - kRound;
+    float r = fmaf(-n, kLn2Hi, -xx);
+    r = r + g;
+    r = r - xxl;
+    r = fmaf(-n, kLn2Lo, r);
+    return t * (exp_series(r) * pow2i((int)n));
+}
+
+}  // namespace dsr
+
+// Per-instance scoring constants, staged in LDS by every workgroup.
+struct ScoreTab {
+    float aw[SAE_MAX_QUEUES][8];  // fl(alpha_q * w_tau)
+    float mu[SAE_MAX_QUEUES];
+    float c[SAE_MAX_QUEUES];      // fl(1 / fl(sigma_q * sqrt 2))
+    int32_t kind[SAE_MAX_QUEUES];
+    float gamma;
+};
+
+__device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, const DevCtx &c)
+{
+    int tid = threadIdx.x;
+    if (tid < SAE_MAX_QUEUES * 8) {
+        int q = tid >> 3, ty = tid & 7;
+        t.aw[q][ty] = (ty < SAE_N_TYPES) ? s.alpha[q] * s.w[ty] : 0.0f;
+    }
+    if (tid < SAE_MAX_QUEUES) {
+        t.mu[tid] = s.mu[tid];
+        t.c[tid] = 1.0f / (s.sigma[tid] * dsr::kSqrt2);
+        t.kind[tid] = c.kind[tid];
+    }
+    if (tid == 0) t.gamma = s.gamma;
+}
+
+// Selection key of one block: IEEE bits of P(b) (Eq. 3), or of (float)
+// num_tokens for an evict-first queue (Algorithm 1, stage 1).  P >= +0 always,
+// so unsigned order of the bits is the numeric order; +inf sorts last.
+__device__ __forceinline__ uint32_t block_key(int32_t now, int32_t la, uint32_t m, uint32_t off,
+                                              const ScoreTab &t, uint32_t &st)
+{
+    int q = meta_queue(m);
+    int kind = t.kind[q];
+    int32_t dt = now - la;
+    if (dt < 0) {
+        st |= SAE_ST_FUTURE_ACCESS;
+        dt = 0;
+    }
+    if (kind == SAE_KIND_EVICT_FIRST) return __float_as_uint((float)meta_ntok(m));
+    float p = 1.0f;
+    if (kind == SAE_KIND_LOGNORMAL) {
+        if (dt > 0) {
+            float u = (dsr::ln((float)dt) - t.mu[q]) * t.c[q];
+            float a = fabsf(u);
+            float h = 0.5f * dsr::erfc(a);
+            p = (u >= 0.0f) ? h : 1.0f - h;
+        }
+    } else if (kind == SAE_KIND_STRUCTURAL) {
+        int ob = (int)(off & 0xFFFFu), om = (int)(off >> 16);
+        float r;
+        if (om == 0) {
+            r = 0.0f;
+        } else if (ob >= om) {
+            if (ob > om) st |= SAE_ST_BAD_OFFSET;
+            r = 1.0f;
+        } else {
+            r = (float)ob / (float)om;
+        }
+        float pw;
+        if (r == 0.0f) pw = 0.0f;
+        else if (r == 1.0f || t.gamma == 1.0f) pw = r;
+        else pw = dsr::exp(t.gamma * dsr::ln(r));
+        p = 1.0f - pw;
+    }
+    float nn = t.aw[q][meta_type(m)] * p;
+    if (dt == 0) return 0x7F800000u;
+    return __float_as_uint(nn / (float)dt);
+}
+
+// ----------------------------------------------------------------------------
+// Launchers (defined in the .hip files).
+struct SelectArgs {
+    int32_t now, k;
+    const int32_t *k_per_inst;
+    uint32_t flags;
+    int32_t *victims;
+    float *scores;
+    int32_t *count;
+    int32_t *decision;
+    int32_t *decision_count;
+};
+
+hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s);
+hipError_t launch_index_build(const DevCtx &c, hipStream_t s);
+hipError_t launch_insert(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids,
+                         const uint64_t *hash, const int32_t *parent, const int32_t *la,
+                         const uint16_t *meta, const uint32_t *off, uint8_t *skip, hipStream_t s);
+hipError_t launch_ref(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids,
+                      int32_t delta, hipStream_t s);
+hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, const uint64_t *hashes,
+                               const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
+                               int32_t *match_len, int32_t *matched_ids, hipStream_t s);
+hipError_t launch_ghost_rebuild(const DevCtx &c, hipStream_t s);
+hipError_t launch_index_rebuild(const DevCtx &c, hipStream_t s);
+hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s,
+                              hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_feedback(const DevCtx &c, uint32_t flags, hipStream_t s);
+bool batched_engine_fits(const DevCtx &c);

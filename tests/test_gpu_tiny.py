@@ -1,0 +1,192 @@
+"""GPU parity, tiny pool (4,096 blocks of 16 tokens, 3 queues, k = 64, 256
+requests of up to 32 hashes): every step of the hot path against the oracle,
+element by element, plus edge cases."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+import synth  # noqa: E402
+from harness import Pair, say  # noqa: E402
+from paper_2605_18825_amd import api  # noqa: E402
+
+
+def tiny_pair(**over):
+    cfg = synth.pool_config("tiny")
+    n = over.pop("n_blocks", cfg["n_blocks"])
+    pool = synth.make_pool(cfg, n_blocks=n, seed=over.pop("seed", None))
+    k = over.pop("max_k", cfg["k"])
+    kinds = over.pop("kinds", cfg["kinds"])
+    mu = over.pop("mu", cfg["mu"][:len(kinds)] + [0.0] * max(0, len(kinds) - len(cfg["mu"])))
+    sigma = over.pop("sigma", cfg["sigma"][:len(kinds)] + [1.0] * max(0, len(kinds) - len(cfg["sigma"])))
+    return Pair(kinds, pool, k, mu=mu, sigma=sigma, **over), pool, cfg
+
+
+@pytest.fixture
+def tiny():
+    p, pool, cfg = tiny_pair()
+    yield p, pool, cfg
+    p.close()
+
+
+def test_block_types(tiny):
+    p, _, _ = tiny
+    p.check_tau()
+
+
+@pytest.mark.parametrize("engine", ["auto", "scan", "batched", "fallback"])
+def test_score_select(tiny, engine):
+    p, pool, cfg = tiny
+    flags = {"auto": 0, "scan": api.SS_ENGINE_SCAN, "batched": api.SS_ENGINE_BATCHED,
+             "fallback": api.SS_FORCE_FALLBACK}[engine]
+    say("tiny score_select engine=%s" % engine)
+    for k in (64, 1, 17, 0):
+        p.select(pool["now"], k, flags)
+    st = p.status()
+    assert set(st) <= {"SELECT_FALLBACK"}, st
+
+
+def test_prefix_match_and_stats(tiny):
+    p, pool, cfg = tiny
+    R, L = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], 77)
+    say("tiny prefix_match read-only")
+    p.prefix_match(R, L, pool["now"], 0)
+    say("tiny prefix_match touch+stats")
+    m = p.prefix_match(R, L, pool["now"] + 5, api.PM_TOUCH | api.PM_STATS)
+    assert (m > 0).mean() > 0.4
+    p.check_pool()
+    p.check_counters()
+    # the touched blocks are now the most recent: the selection changes accordingly
+    p.select(pool["now"] + 10, 64)
+
+
+def test_commit_insert_feedback_cycle(tiny):
+    p, pool, cfg = tiny
+    now = pool["now"]
+    rng = np.random.default_rng(5)
+    for step in range(6):
+        say("tiny cycle step %d" % step)
+        lists, key, dec = p.select(now, 64, commit=True)
+        p.check_pool()
+        p.check_counters()
+        # re-request some victims (Add() finds them in recently_evicted), refill the rest
+        d = len(dec)
+        re = rng.choice(d, size=min(d, 8), replace=False)
+        ids = dec.astype(np.int32)
+        hashes = pool["hash"][ids].copy()
+        fresh = ~np.isin(np.arange(d), re)
+        hashes[fresh] = rng.integers(1, 2 ** 62, int(fresh.sum()), dtype=np.uint64)
+        pool["hash"][ids] = hashes
+        counts = synth.pools.token_type_counts(rng, d)
+        p.insert(ids, hashes, np.full(d, -1, np.int32), np.full(d, now, np.int32), rng.integers(0, 3, d),
+                 counts, np.full(d, 16), rng.integers(0, 30, d), np.full(d, 30))
+        p.check_pool()
+        p.check_counters()
+        p.feedback()
+        p.check_params()
+        p.check_counters()
+        now += 1000
+    assert sum(p.oc.missed) > 0
+    assert p.oc.n_updates > 0
+    assert not p.status()
+
+
+def test_learners_forced_and_trigger():
+    p, pool, cfg = tiny_pair(K=100, eta=0.05)
+    try:
+        now = pool["now"]
+        for step in range(4):
+            p.select(now, 64, commit=True)
+            if step == 2:
+                p.feedback(force=True)
+            else:
+                p.feedback()
+            p.check_params()
+            p.check_counters()
+            now += 500
+    finally:
+        p.close()
+
+
+# ------------------------------------------------------------------ edge cases
+def test_ragged_pool_and_evict_first_queue():
+    """A pool size that is not a multiple of 4 (scalar tail of the scan) and the
+    5-queue layout with an evict-first queue and varying num_tokens."""
+    kinds = [0, 1, 2, 2, 3]
+    p, pool, cfg = tiny_pair(n_blocks=4099, kinds=kinds, mu=[0, 0, 11.7, 9.2, 0], sigma=[1, 1, 1.25, 1.34, 1],
+                             max_k=200, gamma=0.8, w=[2.0, 1.5, 1.0, 1.0, 0.1], alpha=[1, 0.5, 2.0, 1.5, 1])
+    try:
+        rng = np.random.default_rng(1)
+        p.oc.ntok[:] = rng.integers(1, 17, p.N)
+        m = p.dp.meta.cpu().numpy().astype(np.int32) & 0xFFFF
+        m = (m & ~(15 << 9)) | ((p.oc.ntok - 1) << 9)
+        import torch
+        p.dp.meta.copy_(torch.as_tensor(m.astype(np.int16)))
+        for flags in (0, api.SS_ENGINE_SCAN, api.SS_ENGINE_BATCHED, api.SS_FORCE_FALLBACK):
+            for k in (200, 5, 199):
+                p.select(pool["now"], k, flags)
+    finally:
+        p.close()
+
+
+def test_nothing_evictable_and_all_evictable():
+    p, pool, cfg = tiny_pair(n_blocks=1000)
+    try:
+        import torch
+        # everything referenced: nothing to evict
+        ids = torch.arange(1000, dtype=torch.int32, device="cuda")
+        api.sae_ref_blocks(p.ctx, ids, 1)
+        p.oc.ref(np.arange(1000), 1)
+        p.check_pool()
+        for flags in (api.SS_ENGINE_SCAN, api.SS_ENGINE_BATCHED):
+            p.select(pool["now"], 64, flags)
+        assert int(p.out.decision_count[0]) == 0
+        api.sae_ref_blocks(p.ctx, ids, -1)
+        p.oc.ref(np.arange(1000), -1)
+        p.check_pool()
+        # k larger than every queue's evictable count takes all of them
+        for flags in (api.SS_ENGINE_SCAN, api.SS_ENGINE_BATCHED):
+            p.select(pool["now"], 64, flags)
+    finally:
+        p.close()
+
+
+def test_ties_and_recent_blocks():
+    """Many identical scores (same dt, type, offsets) and blocks touched at
+    `now` (dt = 0, score +inf): ties go to the lower block id."""
+    p, pool, cfg = tiny_pair(n_blocks=2048, max_k=512)
+    try:
+        import torch
+        la = (pool["last_access"] // 200000) * 200000
+        la[::7] = pool["now"]
+        p.oc.la[:] = la
+        p.dp.last_access.copy_(torch.as_tensor(la.astype(np.int32)))
+        ob = pool["ob"] // 50 * 50
+        p.oc.ob[:] = ob
+        off = api.off_to_u32(api.pack_off(torch.as_tensor(ob.astype(np.int64)), torch.as_tensor(pool["omax"].astype(np.int64))))
+        p.dp.off.copy_(off)
+        for flags in (api.SS_ENGINE_SCAN, api.SS_ENGINE_BATCHED, api.SS_FORCE_FALLBACK):
+            for k in (512, 300, 64):
+                p.select(pool["now"], k, flags)
+    finally:
+        p.close()
+
+
+def test_prefix_match_edge_lengths():
+    p, pool, cfg = tiny_pair(n_blocks=4096)
+    try:
+        ch = pool["chains"]
+        R = np.zeros((6, 130), np.uint64)
+        L = np.array([0, 1, 64, 65, 130, 32], np.int32)
+        R[1, 0] = ch[0, 0]
+        R[2, :32] = ch[1]
+        R[2, 32:64] = ch[2]                 # another chain: every hash is still indexed, match = 64
+        R[3, :32] = ch[3]
+        R[3, 32:65] = 12345
+        R[4, :] = 999
+        R[4, :32] = ch[4]
+        R[5, :32] = ch[5]
+        p.prefix_match(R, L, pool["now"], api.PM_STATS | api.PM_TOUCH)
+        p.check_counters()
+    finally:
+        p.close()
