@@ -1,0 +1,213 @@
+"""Benchmark of the eviction hot path on one MI355X.
+
+Workload: one cache of 4,194,304 blocks (64M tokens), 5 queues (evict-first,
+structural, chat log-normal, agent log-normal, recency), k = 4,096 victims per
+queue, and a batch of 4,096 prefix-match requests of 128 block hashes.
+
+A step is one full pass of the hot path on one cache:
+  sae_prefix_match (touch + stats) -> sae_score_select (every block scored,
+  per-queue k smallest, Algorithm 1 decision, commit) -> sae_feedback_update.
+Steps rotate over R independent caches (own pool, index and recently-evicted
+table) so that the working set exceeds the 256 MB last-level cache and the
+pool is read from HBM.
+
+value = blocks scored+selected per second over the timed steps (G blk/s).
+The JSON line also carries the score+select call alone, the roofline of the
+scoring kernel (bytes per block x blocks / its HIP-event-timed duration) and
+the CPU oracle timed on a bounded sample on the host.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "cached blocks scored+selected per sec (G blk/s) at 4M blocks; % HBM peak"
+HBM_PEAK_GBS = 8000.0
+BYTES_PER_BLOCK = 10  # last_access 4 + meta 2 + off 4: what the scoring pass must read
+SCAN_KERNEL_SOURCES = ["paper_2605_18825_amd/csrc/k_select.hip", "paper_2605_18825_amd/csrc/sae_internal.h"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in SCAN_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the scoring kernel from rocprofv3 counters, if the
+    committed measurement was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "k_scan_large_pool_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, pool, reqs, lens, budget_s):
+    """The oracle as it stands, single-threaded on the host, on a bounded number
+    of full steps of the same workload."""
+    import numpy as np
+    import oracle
+    prm = oracle.Params(len(cfg["kinds"]), mu=cfg["mu"], sigma=cfg["sigma"], K=cfg["k"])
+    oc = oracle.OracleCache(pool["n_blocks"], cfg["kinds"], prm)
+    oc.bind(pool["last_access"], pool["queue"], oracle.block_type(pool["counts"]), pool["ntok"], pool["ob"],
+            pool["omax"], pool["valid"], pool["ref_count"], pool["parent"], pool["hash"], pool["access_count"])
+    now = pool["now"]
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        oc.prefix_match(reqs, lens, now, touch=True, stats=True)
+        oc.score_select(now, cfg["k"], commit=True)
+        oc.feedback()
+        steps += 1
+        now += 1000
+        el = time.perf_counter() - t0
+        if el >= budget_s or steps >= 50:
+            break
+    return dict(value=pool["n_blocks"] * steps / el / 1e9, unit="G blk/s", cores=1, kind="oracle",
+                sample="%d full step(s) (prefix match of 4096x128 hashes, score+select+commit of 4,194,304 "
+                       "blocks, feedback) on one host core, %.1f s" % (steps, el))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--replicas", type=int, default=8)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU: this build has no multi-GPU path (see DESIGN.md, sharding).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2605_18825_amd import api
+    from paper_2605_18825_amd.pool import DevicePool, SelectBuffers
+
+    torch.cuda.set_device(0)
+    cfg = synth.pool_config("large")
+    pool = synth.make_pool(cfg)
+    N, Q, k = pool["n_blocks"], len(cfg["kinds"]), cfg["k"]
+    reqs, lens = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], cfg["seed"] + 1)
+    R = max(1, args.replicas)
+    caches = []
+    for r in range(R):
+        ctx = api.sae_create(1, N, cfg["kinds"], max_k=k)
+        dp = DevicePool(1, N)
+        dp.fill_instance(0, pool)
+        dp.bind(ctx)
+        api.sae_index_build(ctx)
+        api.sae_set_params(ctx, -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k))
+        caches.append(dict(ctx=ctx, dp=dp, out=SelectBuffers(1, Q, k), now=pool["now"]))
+    d_reqs = torch.as_tensor(np.asarray(reqs, np.uint64).view(np.int64)).cuda()
+    d_lens = torch.as_tensor(lens).cuda()
+    d_ml = torch.zeros(len(lens), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.Stream()  # default priority
+    torch.cuda.synchronize()
+
+    def step(i):
+        c = caches[i % R]
+        api.sae_prefix_match(c["ctx"], d_reqs, d_lens, c["now"], api.PM_TOUCH | api.PM_STATS, d_ml, stream=stream)
+        c["out"].run(c["ctx"], c["now"], k, api.SS_COMMIT, stream=stream)
+        api.sae_feedback_update(c["ctx"], 0, stream=stream)
+        c["now"] += 1000
+
+    def select_only(i):
+        c = caches[i % R]
+        c["out"].run(c["ctx"], c["now"], k, 0, stream=stream)
+
+    with torch.cuda.stream(stream):
+        # --- full steps
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        for c in caches:
+            api.sae_profile_enable(c["ctx"], True)
+            api.sae_profile_read(c["ctx"])
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(args.warmup + i)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        scan_ms, scan_n = 0.0, 0
+        for c in caches:
+            ms, n = api.sae_profile_read(c["ctx"])
+            api.sae_profile_enable(c["ctx"], False)
+            scan_ms += ms
+            scan_n += n
+        # --- score+select alone (no commit), same rotation
+        for i in range(args.warmup):
+            select_only(i)
+        torch.cuda.synchronize()
+        s0 = time.perf_counter()
+        for i in range(args.steps):
+            select_only(i)
+        torch.cuda.synchronize()
+        s1 = time.perf_counter()
+    st = 0
+    for c in caches:
+        st |= api.sae_poll_status(c["ctx"])
+    bad = [s for s in api.status_names(st) if s not in ("SELECT_FALLBACK",)]
+    if bad:
+        print("device status: %s" % bad, file=sys.stderr)
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    ms_sel = (s1 - s0) * 1e3 / args.steps
+    scan_avg_ms = scan_ms / max(scan_n, 1)
+    alg_bytes = BYTES_PER_BLOCK * N
+    achieved = alg_bytes / (scan_avg_ms * 1e-3) / 1e9
+    traffic = measured_traffic()
+    line = {
+        "metric": METRIC,
+        "value": N / (ms_step * 1e-3) / 1e9,
+        "unit": "G blk/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "one 4,194,304-block cache, 5 queues, k=4096; step = prefix match of 4096x128 hashes "
+                        "+ score/select/commit + feedback",
+            "blocks": N, "queues": Q, "k": k, "requests": int(len(lens)), "hashes_per_request": int(reqs.shape[1]),
+            "replicas": R,
+        },
+        "score_select": {
+            "value": N / (ms_sel * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_sel,
+            "hbm_frac_at_10B_per_block": BYTES_PER_BLOCK * N / (ms_sel * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        },
+        "roofline": {
+            "kernel": "k_scan", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "avg_launch_ms": scan_avg_ms,
+            "launches": scan_n, "bytes_per_launch_alg": alg_bytes,
+        },
+        "device_status": api.status_names(st),
+    }
+    for c in caches:
+        api.sae_destroy(c["ctx"])
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(cfg, pool, reqs, lens, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -296,6 +296,12 @@ sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream
  * synchronizes `stream`. */
 sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
 
+/* Diagnostics of the last pool-scan selection of one instance: for each
+ * queue q, out[4q..4q+3] = {evictable blocks, candidates in workgroup regions,
+ * candidates spilled, 1 if the exact slow path ran}.  out is host memory of
+ * 4 * n_queues words; synchronizes `stream`. */
+sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_stream_t stream);
+
 /* Per-kernel timing of the pool-scan engine's scoring pass: when enabled,
  * HIP events bracket every launch of that kernel on the call's stream.
  * sae_profile_read returns the summed milliseconds and launch count since the

@@ -52,13 +52,8 @@ def block_type(counts):
     n = counts.sum(axis=1)
     m = (n - 1) // 2
     cum = np.cumsum(counts, axis=1)
-    tau = np.zeros(len(counts), np.int32)
-    for i in range(len(counts)):
-        for t in range(N_TYPES):
-            if cum[i, t] > m[i]:
-                tau[i] = t
-                break
-    return tau
+    # first type whose cumulative count passes the median rank
+    return np.argmax(cum > m[:, None], axis=1).astype(np.int32)
 
 
 def clamp(x, lo, hi):
@@ -135,10 +130,8 @@ class OracleCache:
         self.hash[:] = hashes
         self.access_count[:] = 0 if access_count is None else access_count
         self.child_count[:] = 0
-        for b in range(self.N):
-            p = int(self.parent[b])
-            if self.valid[b] and p >= 0:
-                self.child_count[p] += 1
+        has = self.valid & (self.parent >= 0)
+        np.add.at(self.child_count, self.parent[has].astype(np.int64), 1)
         self.index = {int(self.hash[b]): b for b in np.nonzero(self.valid)[0].tolist()}
 
     def evictable(self):

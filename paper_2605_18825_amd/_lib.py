@@ -80,6 +80,7 @@ SIGNATURES = {
     "sae_score_select": (_I32, [_P, _I32, _I32, _P, _U32, _P, _P, _P, _P, _P, _P]),
     "sae_feedback_update": (_I32, [_P, _U32, _P]),
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
+    "sae_select_stats": (_I32, [_P, _I32, _P, _P]),
     "sae_profile_enable": (_I32, [_P, _I32]),
     "sae_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),
 }

@@ -189,6 +189,12 @@ def sae_poll_status(ctx, stream=None):
     return b.value
 
 
+def sae_select_stats(ctx, inst, n_queues, stream=None):
+    buf = (ctypes.c_uint32 * (4 * n_queues))()
+    _check(ctx, _lib.load().sae_select_stats(ctx, inst, ctypes.cast(buf, ctypes.c_void_p), _stream(stream)))
+    return [tuple(buf[4 * q:4 * q + 4]) for q in range(n_queues)]
+
+
 def sae_profile_enable(ctx, enable=True):
     _check(ctx, _lib.load().sae_profile_enable(ctx, 1 if enable else 0))
 

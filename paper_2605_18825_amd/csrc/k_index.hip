@@ -156,6 +156,8 @@ __global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
         c.ring[i].stamp = 0;
         c.ring[i].tq = 0;
     }
+    long long ncp = (long long)c.n_inst * SAE_CSLOTS * SAE_CF_STRIDE;
+    if (i < ncp) c.cpart[i] = 0;
     if (i < c.n_inst) {
         InstState &s = c.state[i];
         for (int t = 0; t < SAE_N_TYPES; ++t) s.evicted[t] = s.missed[t] = 0;
@@ -244,7 +246,7 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     if (s >= 0) {
         if (atomicCAS(&gt[s].hash, h, SAE_TOMB_HASH) == h) {
             uint32_t old = atomicOr(&ring[rp].tq, 0x100u);
-            if (!(old & 0x100u)) atomicAdd(&c.state[inst].missed[(old & 7u) % SAE_N_TYPES], 1);
+            if (!(old & 0x100u)) atomicAdd(counter_slot(c, inst, i) + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
         }
     }
 }
@@ -293,74 +295,101 @@ __global__ void k_ref_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *i
 // ---------------------------------------------------------------------------
 // Strict prefix matching, one wave per request.  Lanes probe 64 consecutive
 // hashes; the lowest missing lane ends the match and no later chunk is probed.
+// queue_hits are summed per workgroup in LDS (when its requests share an
+// instance) and added into one striped counter copy.
 __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, int max_len, const uint64_t *hashes,
                                                           const int32_t *lens, const int32_t *inst_a, int32_t now,
                                                           uint32_t flags, int32_t *match_len, int32_t *matched_ids)
 {
+    __shared__ int32_t winst[kThreads / SAE_WAVE];
+    __shared__ uint32_t wg_hits[SAE_MAX_QUEUES];
     const int lane = (int)__lane_id();
+    const int wave = threadIdx.x / SAE_WAVE;
     const int r = (blockIdx.x * blockDim.x + threadIdx.x) / SAE_WAVE;
-    if (r >= n_req) return;  // the whole wave leaves together
-    const int inst = inst_a ? inst_a[r] : 0;
-    int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
-    int len = lens[r];
-    if (len > max_len) len = max_len;
-    if (len < 0) len = 0;
-    if (inst < 0 || inst >= c.n_inst) {
-        if (mid)
-            for (int j = lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
-        if (lane == 0) {
-            match_len[r] = 0;
-            set_status(c.status, SAE_ST_BAD_BLOCK);
-        }
-        return;
-    }
-    const IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    const long long base = (long long)inst * c.N;
-    const uint64_t *hr = hashes + (long long)r * max_len;
+    const bool active = r < n_req;
+    int inst = (active && inst_a) ? inst_a[r] : 0;
+    const bool inst_ok = inst >= 0 && inst < c.n_inst;
+    if (threadIdx.x < SAE_MAX_QUEUES) wg_hits[threadIdx.x] = 0;
+    if (lane == 0) winst[wave] = (active && inst_ok) ? inst : -1;
     uint32_t qcount[SAE_MAX_QUEUES];
 #pragma unroll
     for (int q = 0; q < SAE_MAX_QUEUES; ++q) qcount[q] = 0;
-    int m = 0;
-    int j0 = 0;
-    for (; j0 < len; j0 += SAE_WAVE) {
-        const int j = j0 + lane;
-        int32_t id = (j < len) ? index_find(tab, c.index_mask, hr[j]) : -1;
-        const bool miss = (j < len) && (id < 0);
-        const unsigned long long mm = __ballot(miss);
-        const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
-        const int lim = min(first, len - j0);
-        const bool hit = lane < lim;
-        int q = 0;
-        if (hit) {
-            const long long g = base + id;
-            q = meta_queue(c.meta[g]);
-            if (flags & SAE_PM_TOUCH) {
-                c.la[g] = now;
-                atomicAdd(&c.access_count[g], 1);
+    if (active) {
+        int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
+        int len = lens[r];
+        if (len > max_len) len = max_len;
+        if (len < 0) len = 0;
+        if (!inst_ok) {
+            if (mid)
+                for (int j = lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
+            if (lane == 0) {
+                match_len[r] = 0;
+                set_status(c.status, SAE_ST_BAD_BLOCK);
             }
-            if (mid) mid[j] = id;
-        } else if (mid && j < max_len) {
-            mid[j] = -1;
-        }
-        if (flags & SAE_PM_STATS) {
+        } else {
+            const IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+            const long long base = (long long)inst * c.N;
+            const uint64_t *hr = hashes + (long long)r * max_len;
+            int m = 0;
+            int j0 = 0;
+            for (; j0 < len; j0 += SAE_WAVE) {
+                const int j = j0 + lane;
+                const int32_t id = (j < len) ? index_find(tab, c.index_mask, hr[j]) : -1;
+                const bool miss = (j < len) && (id < 0);
+                const unsigned long long mm = __ballot(miss);
+                const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
+                const int lim = min(first, len - j0);
+                const bool hit = lane < lim;
+                int q = 0;
+                if (hit) {
+                    const long long g = base + id;
+                    q = meta_queue(c.meta[g]);
+                    if (flags & SAE_PM_TOUCH) {
+                        c.la[g] = now;
+                        atomicAdd(&c.access_count[g], 1);
+                    }
+                    if (mid) mid[j] = id;
+                } else if (mid && j < max_len) {
+                    mid[j] = -1;
+                }
+                if (flags & SAE_PM_STATS) {
 #pragma unroll
-            for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) qcount[qq] += (uint32_t)__popcll(__ballot(hit && q == qq));
-        }
-        m = j0 + lim;
-        if (mm) {
-            j0 += SAE_WAVE;
-            break;
+                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
+                        qcount[qq] += (uint32_t)__popcll(__ballot(hit && q == qq));
+                }
+                m = j0 + lim;
+                if (mm) {
+                    j0 += SAE_WAVE;
+                    break;
+                }
+            }
+            if (mid)
+                for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
+            if (lane == 0) match_len[r] = m;
         }
     }
-    if (mid)
-        for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
-    if (lane == 0) {
-        match_len[r] = m;
-        if (flags & SAE_PM_STATS) {
-#pragma unroll
+    __syncthreads();
+    if (!(flags & SAE_PM_STATS)) return;
+    // one instance for the whole workgroup?  then sum in LDS
+    int i0 = -1;
+    bool uniform = true;
+    for (int w = 0; w < kThreads / SAE_WAVE; ++w) {
+        const int v = winst[w];
+        if (v < 0) continue;
+        if (i0 < 0) i0 = v;
+        else if (v != i0) uniform = false;
+    }
+    if (i0 < 0) return;
+    if (uniform) {
+        if (lane == 0 && active && inst_ok)
             for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
-                if (qq < c.Q && qcount[qq]) atomicAdd(&c.state[inst].hits[qq], (int)qcount[qq]);
-        }
+                if (qcount[qq]) atomicAdd(&wg_hits[qq], qcount[qq]);
+        __syncthreads();
+        if (threadIdx.x < c.Q && wg_hits[threadIdx.x])
+            atomicAdd(counter_slot(c, i0, blockIdx.x) + SAE_CF_HITS + threadIdx.x, (int)wg_hits[threadIdx.x]);
+    } else if (lane == 0 && active && inst_ok) {
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
+            if (qq < c.Q && qcount[qq]) atomicAdd(counter_slot(c, inst, blockIdx.x) + SAE_CF_HITS + qq, (int)qcount[qq]);
     }
 }
 
@@ -370,35 +399,41 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
 // parent, and drop the expired ring entry its ring slot will take.
 __global__ void k_commit_a(DevCtx c, const int32_t *decision)
 {
+    __shared__ int32_t sums[SAE_CF_N];
     const int inst = blockIdx.y;
     const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (threadIdx.x < SAE_CF_N) sums[threadIdx.x] = 0;
+    __syncthreads();
     const InstState &s = c.state[inst];
     const int d = s.last_d;
-    if (j >= d) return;
-    int32_t v = decision[(long long)inst * c.max_k + j];
-    if (v < 0 || v >= c.N) {
+    int32_t v = (j < d) ? decision[(long long)inst * c.max_k + j] : -1;
+    if (j < d && (v < 0 || v >= c.N)) {
         set_status(c.status, SAE_ST_BAD_BLOCK);
-        return;
+        v = -1;
     }
-    const long long g = (long long)inst * c.N + v;
-    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
-    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-    const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
-    GhostEntry old = ring[rp];
-    if (old.hash != 0 && !(old.tq & 0x100u)) ghost_remove(gt, c.ghost_mask, old.hash, rp);
-
-    uint32_t m = c.meta[g];
-    atomicAdd(&c.state[inst].evicted[meta_type(m) % SAE_N_TYPES], 1);
-    atomicAdd(&c.state[inst].evictions[meta_queue(m)], 1);
-    meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
-    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    index_erase(tab, c.index_mask, c.hash[g]);
-    int32_t p = c.parent[g];
-    if (p >= 0 && p < c.N) {
-        long long gp = (long long)inst * c.N + p;
-        int before = atomicSub(&c.child_count[gp], 1);
-        if (before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
+    if (v >= 0) {
+        const long long g = (long long)inst * c.N + v;
+        GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+        GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+        const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
+        const GhostEntry old = ring[rp];
+        if (old.hash != 0 && !(old.tq & 0x100u)) ghost_remove(gt, c.ghost_mask, old.hash, rp);
+        const uint32_t m = c.meta[g];
+        atomicAdd(&sums[SAE_CF_EVICTED + meta_type(m) % SAE_N_TYPES], 1);
+        atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
+        meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
+        IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+        index_erase(tab, c.index_mask, c.hash[g]);
+        const int32_t p = c.parent[g];
+        if (p >= 0 && p < c.N) {
+            const long long gp = (long long)inst * c.N + p;
+            const int before = atomicSub(&c.child_count[gp], 1);
+            if (before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
+        }
     }
+    __syncthreads();
+    if (threadIdx.x < SAE_CF_N && sums[threadIdx.x])
+        atomicAdd(counter_slot(c, inst, blockIdx.x) + threadIdx.x, sums[threadIdx.x]);
 }
 
 // Commit, phase 2: record the victims in recently_evicted.
@@ -446,6 +481,7 @@ hipError_t launch_index_build(const DevCtx &c, hipStream_t s)
     if (ngt > n) n = ngt;
     if (nring > n) n = nring;
     if (c.n_inst > n) n = c.n_inst;
+    if ((long long)c.n_inst * SAE_CSLOTS * SAE_CF_STRIDE > n) n = (long long)c.n_inst * SAE_CSLOTS * SAE_CF_STRIDE;
     hipLaunchKernelGGL(k_clear_all, dim3(grid_for(n)), dim3(kThreads), 0, s, c, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

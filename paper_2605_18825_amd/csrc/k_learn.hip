@@ -7,11 +7,30 @@ namespace {
 
 __device__ __forceinline__ float clampf(float x, float lo, float hi) { return fminf(fmaxf(x, lo), hi); }
 
-__global__ void k_feedback(DevCtx c, uint32_t flags)
+// One workgroup of 64 threads per instance: first fold the striped counter
+// copies into the instance state (thread f sums field f over the copies),
+// then, if asked and due, thread 0 runs the learners.
+__global__ void k_feedback(DevCtx c, uint32_t flags, int learn)
 {
-    int inst = blockIdx.x * blockDim.x + threadIdx.x;
-    if (inst >= c.n_inst) return;
+    const int inst = blockIdx.x;
     InstState &s = c.state[inst];
+    const int f = threadIdx.x;
+    if (f < SAE_CF_N) {
+        int32_t *base = c.cpart + (long long)inst * SAE_CSLOTS * SAE_CF_STRIDE + f;
+        int32_t sum = 0;
+        for (int k = 0; k < SAE_CSLOTS; ++k) {
+            sum += base[k * SAE_CF_STRIDE];
+            base[k * SAE_CF_STRIDE] = 0;
+        }
+        if (sum) {
+            if (f < SAE_CF_MISSED) s.evicted[f - SAE_CF_EVICTED] += sum;
+            else if (f < SAE_CF_HITS) s.missed[f - SAE_CF_MISSED] += sum;
+            else if (f < SAE_CF_EVICTIONS) s.hits[f - SAE_CF_HITS] += sum;
+            else s.evictions[f - SAE_CF_EVICTIONS] += sum;
+        }
+    }
+    __syncthreads();
+    if (!learn || f != 0) return;
     if (!s.pending && !(flags & SAE_FB_FORCE)) return;
     if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
         // Algorithm 3: raise the weight of types evicted too aggressively;
@@ -50,9 +69,8 @@ __global__ void k_feedback(DevCtx c, uint32_t flags)
 
 }  // namespace
 
-hipError_t launch_feedback(const DevCtx &c, uint32_t flags, hipStream_t s)
+hipError_t launch_feedback(const DevCtx &c, uint32_t flags, int learn, hipStream_t s)
 {
-    unsigned grid = (unsigned)((c.n_inst + 63) / 64);
-    hipLaunchKernelGGL(k_feedback, dim3(grid), dim3(64), 0, s, c, flags);
+    hipLaunchKernelGGL(k_feedback, dim3(c.n_inst), dim3(64), 0, s, c, flags, learn);
     return hipGetLastError();
 }

@@ -164,13 +164,19 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     d.cand_cap = (int32_t)cc;
 
     const long long I = d.n_inst, Q = d.Q;
+    d.scan_gx = scan_grid_x(d.n_inst, d.N);
+    const long long GX = d.scan_gx;
     bool ok = dev_alloc(c, &d.state, I) && dev_alloc(c, &d.status, 1) &&
               dev_alloc(c, &d.index, I * c->index_slots) && dev_alloc(c, &d.ring, I * d.ring_cap) &&
               dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) &&
-              dev_alloc(c, &d.shist, I * Q * SAE_BINS) && dev_alloc(c, &d.n_ev, I * Q) &&
-              dev_alloc(c, &d.n_cand, I * Q) && dev_alloc(c, &d.cand, I * Q * d.cand_cap) &&
+              dev_alloc(c, &d.shist, I * SAE_HIST_STRIPES * Q * SAE_SBINS) &&
+              dev_alloc(c, &d.nev_part, I * GX * Q) && dev_alloc(c, &d.creg, I * GX * Q * SAE_CAND_REGION) &&
+              dev_alloc(c, &d.creg_n, I * GX * Q) && dev_alloc(c, &d.spill, I * Q * d.cand_cap) &&
+              dev_alloc(c, &d.spill_n, I * Q) && dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
               dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
-              dev_alloc(c, &d.done, I) && dev_alloc(c, &c->skip, I * d.N);
+              dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
+              dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&
+              dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);
         delete c;
@@ -286,8 +292,9 @@ sae_status sae_get_counters(sae_ctx *c, int32_t inst, sae_counters *out, sae_str
 {
     if (!c || !out) return fail(c, SAE_ERR_ARG, "ctx and out must be non-NULL");
     if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    hipError_t e = launch_feedback(c->dc, 0, 0, S(stream));  // fold the striped counters
     InstState h;
-    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
     if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_get_counters");
     memcpy(out->evicted, h.evicted, sizeof(out->evicted));
@@ -304,8 +311,9 @@ sae_status sae_set_counters(sae_ctx *c, int32_t inst, const sae_counters *in, sa
 {
     if (!c || !in) return fail(c, SAE_ERR_ARG, "ctx and counters must be non-NULL");
     if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    hipError_t e = launch_feedback(c->dc, 0, 0, S(stream));  // fold the striped counters
     InstState h;
-    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
     if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_set_counters read");
     memcpy(h.evicted, in->evicted, sizeof(h.evicted));
@@ -472,7 +480,7 @@ sae_status sae_feedback_update(sae_ctx *c, uint32_t flags, sae_stream_t stream)
 {
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
     if (flags & ~(uint32_t)SAE_FB_FORCE) return fail(c, SAE_ERR_ARG, "unknown feedback flag");
-    hipError_t e = launch_feedback(c->dc, flags, S(stream));
+    hipError_t e = launch_feedback(c->dc, flags, 1, S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_feedback_update");
     return SAE_OK;
 }
@@ -487,6 +495,17 @@ sae_status sae_poll_status(sae_ctx *c, sae_stream_t stream, uint32_t *bits)
     if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_poll_status");
     *bits = h;
+    return SAE_OK;
+}
+
+sae_status sae_select_stats(sae_ctx *c, int32_t inst, uint32_t *out, sae_stream_t stream)
+{
+    if (!c || !out) return fail(c, SAE_ERR_ARG, "ctx and out must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    hipError_t e = hipMemcpyAsync(out, c->dc.sel_stats + (long long)inst * c->dc.Q * 4, sizeof(uint32_t) * 4 * c->dc.Q,
+                                  hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_select_stats");
     return SAE_OK;
 }
 

@@ -5,7 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/sae.h"
+#include "sae.h"
 
 #define SAE_WAVE 64
 #define SAE_EMPTY_HASH 0ull
@@ -15,6 +15,25 @@
 // Radix digits of the selection: 11 bits -> 2048 bins.
 #define SAE_DIGIT_BITS 11
 #define SAE_BINS (1 << SAE_DIGIT_BITS)
+
+// Sampling of the pool-scan engine: chunks per instance and blocks per chunk.
+#define SAE_SAMPLE_WGS 256
+#define SAE_SAMPLE_CHUNK 256
+#define SAE_HIST_STRIPES 32  // copies of the sampled histogram (fewer same-address atomics)
+#define SAE_SBINS 512        // sampled histogram bins: top 9 key bits (one bin per octave of P)
+#define SAE_CAND_REGION 128  // candidate slots per (scan workgroup, queue)
+
+// Feedback counters are added into one of SAE_CSLOTS striped copies (chosen by
+// the adding workgroup) and folded into InstState by the learner kernel:
+// device-wide atomics on one address serialise, so many workgroups must not
+// add into the same word.
+#define SAE_CSLOTS 64
+#define SAE_CF_EVICTED 0     // 5 fields, token_stats[tau].evicted
+#define SAE_CF_MISSED 5      // 5 fields, token_stats[tau].miss_after_evict
+#define SAE_CF_HITS 10       // 8 fields, queue_hits[q]
+#define SAE_CF_EVICTIONS 18  // 8 fields, queue_evictions[q]
+#define SAE_CF_N 26
+#define SAE_CF_STRIDE 32
 
 // ----------------------------------------------------------------------------
 // Per-instance device state: learned parameters, learner settings and the
@@ -83,14 +102,20 @@ struct DevCtx {
     IndexSlot *index;     // [n_inst][index_mask + 1]
     GhostEntry *ring;     // [n_inst][ring_cap]
     GhostSlot *gtab;      // [n_inst][ghost_mask + 1]
-    uint32_t *thr;        // [n_inst][Q] candidate key bound (scan engine)
-    uint32_t *shist;      // [n_inst][Q][SAE_BINS] sampled key histogram
-    uint32_t *n_ev;       // [n_inst][Q] evictable blocks
-    uint32_t *n_cand;     // [n_inst][Q] candidates emitted
-    unsigned long long *cand;  // [n_inst][Q][cand_cap] (key << 32 | id)
+    unsigned long long *thr;   // [n_inst][Q] candidate bound on (key << 32 | id), scan engine
+    uint32_t *shist;      // [n_inst][SAE_HIST_STRIPES][Q][SAE_SBINS] sampled key histogram
+    unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
+    uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
+    uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, in regions, spilled, slow path
+    uint32_t *nev_part;        // [n_inst][scan_gx][Q] evictable blocks per scan workgroup
+    unsigned long long *creg;  // [n_inst][scan_gx][Q][SAE_CAND_REGION] candidates per scan workgroup
+    uint32_t *creg_n;          // [n_inst][scan_gx][Q]
+    unsigned long long *spill; // [n_inst][Q][cand_cap] candidates beyond a region
+    uint32_t *spill_n;         // [n_inst][Q]
+    int32_t scan_gx;           // scan workgroups per instance
+    int32_t *cpart;            // [n_inst][SAE_CSLOTS][SAE_CF_STRIDE] feedback counters, striped
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
     int32_t *sel_count;        // [n_inst][Q]
-    uint32_t *done;            // [n_inst] last-workgroup counters
 };
 
 // ----------------------------------------------------------------------------
@@ -115,6 +140,11 @@ __device__ __forceinline__ void meta_or(uint16_t *meta, long long b, uint32_t bi
     uint32_t *w = reinterpret_cast<uint32_t *>(meta + (b & ~1ll));
     uint32_t sh = (uint32_t)(b & 1) * 16u;
     atomicOr(w, (bits16 & 0xFFFFu) << sh);
+}
+
+__device__ __forceinline__ int32_t *counter_slot(const DevCtx &c, int inst, int slot)
+{
+    return c.cpart + ((long long)inst * SAE_CSLOTS + (slot & (SAE_CSLOTS - 1))) * SAE_CF_STRIDE;
 }
 
 __device__ __forceinline__ void set_status(uint32_t *status, uint32_t bits)
@@ -169,14 +199,18 @@ constexpr float kInvLn2 = 0x1.715476p+0f;
 constexpr float kRound = 0x1.8p+23f;
 constexpr float kSqrt2 = 0x1.6a09e6p+0f;
 
+// Branch-free: the arithmetic runs on y clamped into [-86, 88]; results
+// outside are then replaced (identical values for every finite y).
 __device__ __forceinline__ float exp(float y)
 {
-    if (y < -86.0f) return 0.0f;
-    if (y > 88.0f) return __uint_as_float(0x7F800000u);
-    float n = (y * kInvLn2 + kRound) - kRound;
-    float r = fmaf(-n, kLn2Hi, y);
+    const float yc = fminf(fmaxf(y, -86.0f), 88.0f);
+    const float n = (yc * kInvLn2 + kRound) - kRound;
+    float r = fmaf(-n, kLn2Hi, yc);
     r = fmaf(-n, kLn2Lo, r);
-    return exp_series(r) * pow2i((int)n);
+    float v = exp_series(r) * pow2i((int)n);
+    v = (y < -86.0f) ? 0.0f : v;
+    v = (y > 88.0f) ? __uint_as_float(0x7F800000u) : v;
+    return v;
 }
 
 __device__ __forceinline__ float ln(float x)
@@ -200,11 +234,12 @@ __device__ __forceinline__ float ln(float x)
     return fmaf(ef, kLn2Hi, fmaf(ef, kLn2Lo, lnm));
 }
 
+// x >= 0.  Branch-free: the arithmetic runs on min(x, 9); erfc(0) = 1 and
+// erfc(x >= 9) = 0 are selected afterwards.
 __device__ __forceinline__ float erfc(float x)
 {
-    if (x == 0.0f) return 1.0f;
-    if (!(x < 9.0f)) return 0.0f;
-    float t = 1.0f / fmaf(0.5f, x, 1.0f);
+    const float xc = fminf(x, 9.0f);
+    const float t = 1.0f / fmaf(0.5f, xc, 1.0f);
     float g = 0.17087277f;
     g = fmaf(g, t, -0.82215223f);
     g = fmaf(g, t, 1.48851587f);
@@ -215,14 +250,17 @@ __device__ __forceinline__ float erfc(float x)
     g = fmaf(g, t, 0.37409196f);
     g = fmaf(g, t, 1.00002368f);
     g = fmaf(g, t, -1.26551223f);
-    float xx = x * x;
-    float xxl = fmaf(x, x, -xx);
-    float n = ((g - xx) * kInvLn2 + kRound) - kRound;
+    const float xx = xc * xc;
+    const float xxl = fmaf(xc, xc, -xx);
+    const float n = ((g - xx) * kInvLn2 + kRound) - kRound;
     float r = fmaf(-n, kLn2Hi, -xx);
     r = r + g;
     r = r - xxl;
     r = fmaf(-n, kLn2Lo, r);
-    return t * (exp_series(r) * pow2i((int)n));
+    float v = t * (exp_series(r) * pow2i((int)n));
+    v = (x == 0.0f) ? 1.0f : v;
+    v = (x < 9.0f) ? v : 0.0f;
+    return v;
 }
 
 }  // namespace dsr
@@ -254,45 +292,74 @@ __device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, 
 // Selection key of one block: IEEE bits of P(b) (Eq. 3), or of (float)
 // num_tokens for an evict-first queue (Algorithm 1, stage 1).  P >= +0 always,
 // so unsigned order of the bits is the numeric order; +inf sorts last.
+// One function per queue kind (the pool scan groups blocks by kind so that a
+// wave runs one of them without divergence); block_key dispatches.
+__device__ __forceinline__ int32_t block_dt(int32_t now, int32_t la, uint32_t &st)
+{
+    const int32_t dt = now - la;
+    st |= (dt < 0) ? (uint32_t)SAE_ST_FUTURE_ACCESS : 0u;
+    return dt < 0 ? 0 : dt;
+}
+
+// P bits from n = fl(aw p) and dt; dt = 0 gives +inf.  Branch-free.
+__device__ __forceinline__ uint32_t priority_bits(float aw, float p, int32_t dt)
+{
+    const float nn = aw * p;
+    const float d = (float)(dt > 0 ? dt : 1);
+    const uint32_t b = __float_as_uint(nn / d);
+    return dt == 0 ? 0x7F800000u : b;
+}
+
+// Eq. 1: 1 - F_LN(dt) = erfc(u)/2, u = (ln dt - mu) c, c = 1 / (sigma sqrt 2).
+// Branch-free; dt = 0 (p unused) is evaluated at dt = 1.
+__device__ __forceinline__ uint32_t key_lognormal(int32_t now, int32_t la, uint32_t m, const ScoreTab &t,
+                                                  uint32_t &st)
+{
+    const int q = meta_queue(m);
+    const int32_t dt = block_dt(now, la, st);
+    const float u = (dsr::ln((float)(dt > 0 ? dt : 1)) - t.mu[q]) * t.c[q];
+    const float a = fabsf(u);
+    const float h = 0.5f * dsr::erfc(a);
+    float p = (u >= 0.0f) ? h : 1.0f - h;
+    p = dt > 0 ? p : 1.0f;
+    return priority_bits(t.aw[q][meta_type(m)], p, dt);
+}
+
+// Eq. 2: 1 - (o_b / o_max)^gamma.  Branch-free except on gamma == 1, which is
+// the same for every block.
+__device__ __forceinline__ uint32_t key_structural(int32_t now, int32_t la, uint32_t m, uint32_t off,
+                                                   const ScoreTab &t, uint32_t &st)
+{
+    const int q = meta_queue(m);
+    const int32_t dt = block_dt(now, la, st);
+    const int ob = (int)(off & 0xFFFFu), om = (int)(off >> 16);
+    st |= (om != 0 && ob > om) ? (uint32_t)SAE_ST_BAD_OFFSET : 0u;
+    const float rq = (float)ob / (float)(om != 0 ? om : 1);
+    const float r = (om == 0) ? 0.0f : ((ob >= om) ? 1.0f : rq);
+    float pw = r;
+    if (t.gamma != 1.0f) {
+        const float pg = dsr::exp(t.gamma * dsr::ln(r == 0.0f ? 1.0f : r));
+        pw = (r == 0.0f) ? 0.0f : ((r == 1.0f) ? r : pg);
+    }
+    return priority_bits(t.aw[q][meta_type(m)], 1.0f - pw, dt);
+}
+
+// Evict-first (num_tokens) and recency (p = 1) queues.
+__device__ __forceinline__ uint32_t key_cheap(int kind, int32_t now, int32_t la, uint32_t m, const ScoreTab &t,
+                                              uint32_t &st)
+{
+    const int32_t dt = block_dt(now, la, st);
+    const uint32_t rec = priority_bits(t.aw[meta_queue(m)][meta_type(m)], 1.0f, dt);
+    return kind == SAE_KIND_EVICT_FIRST ? __float_as_uint((float)meta_ntok(m)) : rec;
+}
+
 __device__ __forceinline__ uint32_t block_key(int32_t now, int32_t la, uint32_t m, uint32_t off,
                                               const ScoreTab &t, uint32_t &st)
 {
-    int q = meta_queue(m);
-    int kind = t.kind[q];
-    int32_t dt = now - la;
-    if (dt < 0) {
-        st |= SAE_ST_FUTURE_ACCESS;
-        dt = 0;
-    }
-    if (kind == SAE_KIND_EVICT_FIRST) return __float_as_uint((float)meta_ntok(m));
-    float p = 1.0f;
-    if (kind == SAE_KIND_LOGNORMAL) {
-        if (dt > 0) {
-            float u = (dsr::ln((float)dt) - t.mu[q]) * t.c[q];
-            float a = fabsf(u);
-            float h = 0.5f * dsr::erfc(a);
-            p = (u >= 0.0f) ? h : 1.0f - h;
-        }
-    } else if (kind == SAE_KIND_STRUCTURAL) {
-        int ob = (int)(off & 0xFFFFu), om = (int)(off >> 16);
-        float r;
-        if (om == 0) {
-            r = 0.0f;
-        } else if (ob >= om) {
-            if (ob > om) st |= SAE_ST_BAD_OFFSET;
-            r = 1.0f;
-        } else {
-            r = (float)ob / (float)om;
-        }
-        float pw;
-        if (r == 0.0f) pw = 0.0f;
-        else if (r == 1.0f || t.gamma == 1.0f) pw = r;
-        else pw = dsr::exp(t.gamma * dsr::ln(r));
-        p = 1.0f - pw;
-    }
-    float nn = t.aw[q][meta_type(m)] * p;
-    if (dt == 0) return 0x7F800000u;
-    return __float_as_uint(nn / (float)dt);
+    const int kind = t.kind[meta_queue(m)];
+    if (kind == SAE_KIND_LOGNORMAL) return key_lognormal(now, la, m, t, st);
+    if (kind == SAE_KIND_STRUCTURAL) return key_structural(now, la, m, off, t, st);
+    return key_cheap(kind, now, la, m, t, st);
 }
 
 // ----------------------------------------------------------------------------
@@ -325,5 +392,6 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s);
-hipError_t launch_feedback(const DevCtx &c, uint32_t flags, hipStream_t s);
+hipError_t launch_feedback(const DevCtx &c, uint32_t flags, int learn, hipStream_t s);
+int scan_grid_x(int n_inst, int N);
 bool batched_engine_fits(const DevCtx &c);
