@@ -86,6 +86,9 @@ def main():
     ap.add_argument("--replicas", type=int, default=8)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed region, copy this many MiB device-to-device 4 times "
+                         "(a plain copy of known size for calibrating HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU: this build has no multi-GPU path (see DESIGN.md, sharding).",
@@ -204,6 +207,14 @@ def main():
     }
     for c in caches:
         api.sae_destroy(c["ctx"])
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        line["calib_copy_bytes"] = n * 4
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(cfg, pool, reqs, lens, args.cpu_seconds)
     print(json.dumps(line), flush=True)
