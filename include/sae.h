@@ -186,6 +186,35 @@ sae_status sae_set_counters(sae_ctx *ctx, int32_t inst, const sae_counters *c, s
  * lower median (rank floor((n_tokens - 1) / 2)). */
 sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_stream_t stream);
 
+/* Cache hints of a block (one byte each), the input of Algorithm 1's Classify. */
+enum {
+    SAE_HINT_DECODE = 1u << 0,        /* holds decode-phase (generated) tokens                 */
+    SAE_HINT_UNTEMPLATED = 1u << 1,   /* prefill content outside any shared template          */
+    SAE_HINT_MULTI_TURN = 1u << 2,    /* its request is (or is predicted to be) multi-turn    */
+    SAE_HINT_AGENTIC = 1u << 3,       /* its request is agentic / tool use                    */
+    SAE_HINT_CONVERSATION = 1u << 4,  /* its request carries a conversation id (has history)  */
+    SAE_HINT_SHARED_PREFIX = 1u << 5  /* lies in a prompt template shared across requests     */
+};
+/* Queues that Classify routes to: roles[SAE_ROLE_*] is a queue index. */
+enum { SAE_ROLE_EVICT = 0, SAE_ROLE_STRUCT = 1, SAE_ROLE_CHAT = 2, SAE_ROLE_AGENT = 3, SAE_N_ROLES = 4 };
+
+/*
+ * Algorithm 1 Classify (queue routing, Sec. 3.1): for n blocks, from the hint
+ * byte and the block type tau already in meta, the first rule that holds:
+ *   tau = cot, or decode, or untemplated  -> evict-first
+ *   multi-turn and agentic                -> agent
+ *   multi-turn, or conversation           -> chat
+ *   shared prefix, or tau = system        -> structural
+ *   otherwise                             -> evict-first
+ *  hint[n]   device uint8
+ *  meta[n]   device uint16, in/out: the queue bits are replaced by
+ *            roles[rule] (the other bits are kept)
+ *  roles[4]  host int32 queue indices, each in 0 .. n_queues-1
+ * Returns SAE_ERR_ARG (nothing launched) for a bad role or a NULL array.
+ */
+sae_status sae_classify_blocks(sae_ctx *ctx, int32_t n, const uint8_t *hint, uint16_t *meta,
+                               const int32_t *roles, sae_stream_t stream);
+
 /* Rebuild the block index (content hash -> block) from the hash of every
  * valid block, and clear recently_evicted and all counters.  Use after
  * filling the pool arrays directly.  Hashes of valid blocks must be distinct

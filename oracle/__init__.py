@@ -13,7 +13,7 @@ cpu_baseline leg may import, call, link or execute anything in this package.
 """
 from . import _native, fp64, policy  # noqa: F401
 from .policy import (EVICT_FIRST, LOGNORMAL, N_TYPES, RECENCY, STRUCTURAL,  # noqa: F401
-                     OracleCache, Params, block_type)
+                     OracleCache, Params, block_type, classify)
 
 
 def build():

@@ -56,6 +56,37 @@ def block_type(counts):
     return np.argmax(cum > m[:, None], axis=1).astype(np.int32)
 
 
+# Cache hint bits of a block (Algorithm 1's Classify reads them).
+HINT_DECODE = 1         # decode-phase (generated) tokens
+HINT_UNTEMPLATED = 2    # prefill content outside any shared template
+HINT_MULTI_TURN = 4     # request is (or is predicted to be) multi-turn
+HINT_AGENTIC = 8        # agentic / tool-use request
+HINT_CONVERSATION = 16  # request carries a conversation id
+HINT_SHARED_PREFIX = 32  # inside a prompt template shared across requests
+# Queues Classify can return
+ROLE_EVICT, ROLE_STRUCT, ROLE_CHAT, ROLE_AGENT = 0, 1, 2, 3
+SYSTEM, COT = 0, 4
+
+
+def classify_one(tau, hint):
+    """Algorithm 1 Classify for one block: the first rule that holds, in the
+    paper's order."""
+    if tau == COT or hint & HINT_DECODE or hint & HINT_UNTEMPLATED:
+        return ROLE_EVICT
+    if hint & HINT_MULTI_TURN and hint & HINT_AGENTIC:
+        return ROLE_AGENT
+    if hint & HINT_MULTI_TURN or hint & HINT_CONVERSATION:
+        return ROLE_CHAT
+    if hint & HINT_SHARED_PREFIX or tau == SYSTEM:
+        return ROLE_STRUCT
+    return ROLE_EVICT
+
+
+def classify(tau, hint, roles):
+    """Queue index of every block: roles[Classify(tau, hint)]."""
+    return np.array([roles[classify_one(int(t), int(h))] for t, h in zip(tau, hint)], np.int32)
+
+
 def clamp(x, lo, hi):
     return min(max(x, F32(lo)), F32(hi))
 

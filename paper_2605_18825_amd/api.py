@@ -16,6 +16,8 @@ META_VALID, META_LEAF, META_REF = 0x40, 0x80, 0x100
 PM_TOUCH, PM_STATS = 1, 2
 SS_COMMIT, SS_ENGINE_SCAN, SS_ENGINE_BATCHED, SS_FORCE_FALLBACK = 1, 2, 4, 8
 FB_FORCE = 1
+HINT_DECODE, HINT_UNTEMPLATED, HINT_MULTI_TURN, HINT_AGENTIC, HINT_CONVERSATION, HINT_SHARED_PREFIX = 1, 2, 4, 8, 16, 32
+ROLE_EVICT, ROLE_STRUCT, ROLE_CHAT, ROLE_AGENT = 0, 1, 2, 3
 LEARN_TOKEN_WEIGHTS, LEARN_QUEUE_WEIGHTS = 1, 2
 ST_NAMES = {1: "INDEX_FULL", 2: "GHOST_FULL", 4: "BAD_OFFSET", 8: "FUTURE_ACCESS",
             16: "SLOT_BUSY", 32: "SELECT_FALLBACK", 64: "BAD_BLOCK"}
@@ -150,6 +152,13 @@ def sae_set_counters(ctx, inst, counters, stream=None):
 def sae_block_type(counts_u8, tau_u8, stream=None):
     n = counts_u8.shape[0]
     _check(None, _lib.load().sae_block_type(_ptr(counts_u8), n, _ptr(tau_u8), _stream(stream)))
+
+
+def sae_classify_blocks(ctx, hint_u8, meta_u16, roles, stream=None):
+    """Algorithm 1 Classify on the device: rewrites the queue bits of meta."""
+    r = (ctypes.c_int32 * 4)(*[int(x) for x in roles])
+    _check(ctx, _lib.load().sae_classify_blocks(ctx, hint_u8.numel(), _ptr(hint_u8), _ptr(meta_u16), r,
+                                                _stream(stream)))
 
 
 def sae_index_build(ctx, stream=None):

@@ -135,6 +135,24 @@ __global__ void k_block_type(const uint8_t *counts, long long n, uint8_t *tau)
     tau[i] = (uint8_t)ty;
 }
 
+// Algorithm 1 Classify: queue of a block from its hints and its type.
+__global__ void k_classify(int n, const uint8_t *hint, uint16_t *meta, int r_evict, int r_struct, int r_chat,
+                           int r_agent)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    unsigned h = hint[i];
+    unsigned m = meta[i];
+    unsigned tau = (unsigned)meta_type(m);
+    int q;
+    if (tau == SAE_TYPE_COT || (h & (SAE_HINT_DECODE | SAE_HINT_UNTEMPLATED))) q = r_evict;
+    else if ((h & SAE_HINT_MULTI_TURN) && (h & SAE_HINT_AGENTIC)) q = r_agent;
+    else if (h & (SAE_HINT_MULTI_TURN | SAE_HINT_CONVERSATION)) q = r_chat;
+    else if ((h & SAE_HINT_SHARED_PREFIX) || tau == SAE_TYPE_SYSTEM) q = r_struct;
+    else q = r_evict;
+    meta[i] = (uint16_t)((m & ~7u) | (unsigned)q);
+}
+
 // Clear index, recently_evicted and counters.
 __global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
 {
@@ -469,6 +487,14 @@ hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hip
 {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_block_type, dim3(grid_for(n)), dim3(kThreads), 0, s, counts, (long long)n, tau);
+    return hipGetLastError();
+}
+
+hipError_t launch_classify(int n, const uint8_t *hint, uint16_t *meta, const int32_t *roles, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_classify, dim3(grid_for(n)), dim3(kThreads), 0, s, n, hint, meta, roles[0], roles[1],
+                       roles[2], roles[3]);
     return hipGetLastError();
 }
 

@@ -337,6 +337,21 @@ sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_st
     return SAE_OK;
 }
 
+sae_status sae_classify_blocks(sae_ctx *c, int32_t n, const uint8_t *hint, uint16_t *meta, const int32_t *roles,
+                               sae_stream_t stream)
+{
+    if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
+    if (n < 0) return fail(c, SAE_ERR_ARG, "n must be >= 0");
+    if (n == 0) return SAE_OK;
+    if (!hint || !meta || !roles) return fail(c, SAE_ERR_ARG, "hint, meta, roles must be non-NULL");
+    for (int r = 0; r < SAE_N_ROLES; ++r)
+        if (roles[r] < 0 || roles[r] >= c->cfg.n_queues)
+            return fail(c, SAE_ERR_ARG, "roles[] must be queue indices below n_queues");
+    hipError_t e = launch_classify(n, hint, meta, roles, S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_classify_blocks");
+    return SAE_OK;
+}
+
 sae_status sae_index_build(sae_ctx *c, sae_stream_t stream)
 {
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");

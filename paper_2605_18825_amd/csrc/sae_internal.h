@@ -376,6 +376,7 @@ struct SelectArgs {
 };
 
 hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s);
+hipError_t launch_classify(int n, const uint8_t *hint, uint16_t *meta, const int32_t *roles, hipStream_t s);
 hipError_t launch_index_build(const DevCtx &c, hipStream_t s);
 hipError_t launch_insert(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids,
                          const uint64_t *hash, const int32_t *parent, const int32_t *la,

@@ -1,0 +1,31 @@
+"""GPU parity on trace replay.
+
+* Balanced mix (Table 2), one cache of 2,250 blocks (36K tokens), online
+  learning on: every step's match length and every eviction decision equal the
+  oracle's; counters, learned weights and the pool state agree.
+* Batched sweep: 256 caches of 65,536 blocks in one context (half
+  single-turn-dominated, half multi-turn-dominated traces), decisions of at
+  least 256 victims; two sampled instances (one of each half) are replayed by
+  the oracle beside the GPU and compared the same way."""
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+from trace_pair import run_pair  # noqa: E402
+
+
+def test_trace_balanced_first_1500_requests():
+    rd, ro, _ = run_pair("trace_balanced", 1500, [0], check_every=250)
+    s = rd.summary()
+    assert s["evicted"] > 0 and s["hit_blocks"] > 0
+
+
+def test_trace_balanced_fixed_weights():
+    rd, ro, _ = run_pair("trace_balanced", 400, [0], learn=0, check_every=200)
+    assert rd.summary()["evicted"] > 0
+
+
+def test_batched_sweep_sampled_instances():
+    rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], check_every=150)
+    s = rd.summary()
+    assert s["evicted"] > 0 and s["decisions"] > 0

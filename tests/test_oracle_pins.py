@@ -318,6 +318,48 @@ def test_block_type_median_token():
         assert tokens[(len(tokens) - 1) // 2] == t
 
 
+# ------------------------------------------------------------ Classify
+def test_classify_routing_cases():
+    """Algorithm 1 Classify, cases worked from the queue definitions of Sec. 3.1:
+    decode and CoT blocks and untemplated prefill go to the evict-first queue;
+    multi-turn blocks to the chat or agentic queue; templated single-turn
+    prefill to the structural queue."""
+    from oracle.policy import (HINT_AGENTIC as AG, HINT_CONVERSATION as CV, HINT_DECODE as DE,
+                               HINT_MULTI_TURN as MT, HINT_SHARED_PREFIX as SP, HINT_UNTEMPLATED as UT,
+                               ROLE_AGENT, ROLE_CHAT, ROLE_EVICT, ROLE_STRUCT, classify_one)
+    SYS, USER, TOOL, RESP, COT = range(5)
+    cases = [
+        (COT, MT | AG | CV | SP, ROLE_EVICT),   # chain-of-thought is never kept by queue
+        (RESP, DE, ROLE_EVICT),                 # decode block of a single-turn request
+        (SYS, UT, ROLE_EVICT),                  # untemplated wins over the system type
+        (USER, MT | AG, ROLE_AGENT),            # agentic multi-turn history
+        (TOOL, MT | AG | CV | SP, ROLE_AGENT),
+        (USER, MT, ROLE_CHAT),                  # chat multi-turn history
+        (SYS, CV | SP, ROLE_CHAT),              # later turn: the conversation id routes the template too
+        (RESP, AG | CV, ROLE_CHAT),             # agentic but not flagged multi-turn: chat rule
+        (TOOL, AG | SP, ROLE_STRUCT),           # single-turn tool-use template
+        (SYS, 0, ROLE_STRUCT),                  # system prompt with no hint
+        (USER, SP, ROLE_STRUCT),
+        (USER, 0, ROLE_EVICT),                  # fall-through
+        (TOOL, AG, ROLE_EVICT),
+    ]
+    for tau, hint, want in cases:
+        assert classify_one(tau, hint) == want, (tau, hint, want)
+
+
+def test_classify_properties_over_all_hints():
+    from oracle.policy import (HINT_AGENTIC as AG, HINT_DECODE as DE, HINT_MULTI_TURN as MT,
+                               HINT_UNTEMPLATED as UT, ROLE_AGENT, ROLE_EVICT, classify)
+    tau = np.repeat(np.arange(5), 64)
+    hint = np.tile(np.arange(64), 5)
+    roles = [3, 0, 2, 1]  # a non-identity role -> queue map
+    q = classify(tau, hint, roles)
+    role = np.array([roles.index(x) for x in q])
+    assert np.all(role[(tau == 4) | ((hint & (DE | UT)) != 0)] == ROLE_EVICT)
+    assert np.all(((hint & MT) != 0)[role == ROLE_AGENT] & ((hint & AG) != 0)[role == ROLE_AGENT])
+    assert set(role.tolist()) == {0, 1, 2, 3}
+
+
 # ------------------------------------------------------------ learners (fp32)
 def _learner_cache(kinds=(STRUCTURAL, LOGNORMAL, RECENCY)):
     return OracleCache(4, list(kinds), Params(len(kinds), w=1.0, alpha=1.0, eta=0.01, T=1.0, beta=0.1, K=1))
