@@ -326,8 +326,8 @@ sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream
 sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
 
 /* Diagnostics of the last pool-scan selection of one instance: for each
- * queue q, out[4q..4q+3] = {evictable blocks, candidates in workgroup regions,
- * candidates spilled, 1 if the exact slow path ran}.  out is host memory of
+ * queue q, out[4q..4q+3] = {evictable blocks, candidates under the bound,
+ * candidates beyond a scan workgroup's region, 1 if the exact slow path ran}.  out is host memory of
  * 4 * n_queues words; synchronizes `stream`. */
 sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_stream_t stream);
 

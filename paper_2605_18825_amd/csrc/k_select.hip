@@ -1,15 +1,16 @@
 // Scoring and selection kernels (Eq. 1-3, Algorithm 1) for gfx950.
 //
 // Two engines give identical results:
-//  * pool scan (any pool size): a sampling kernel estimates, per instance and
-//    queue, a key bound that admits a few times k blocks; one streaming pass
-//    over the 10-byte-per-block features scores every block and appends the
-//    evictable blocks under the bound to a candidate list; one workgroup per
-//    (instance, queue) then radix-selects and sorts the exact k smallest
-//    (key, id) among the candidates.  If the bound admitted too few (or too
-//    many) blocks, that workgroup falls back to an exact radix select that
-//    streams the instance's pool again (slow, rare).  A merge kernel forms the
-//    Algorithm 1 decision.
+//  * pool scan (any pool size): a sampling kernel scores a sample of every
+//    instance; per (instance, queue) a key bound that admits about 1.25 k
+//    blocks and ~k/64-block buckets below it are read off the sorted sample;
+//    one streaming pass over the 10-byte-per-block features scores every block
+//    and drops the evictable blocks under the bound into their buckets; one
+//    workgroup per bucket sorts it and writes the part of it that falls among
+//    the k smallest (key, id).  If the bound admitted too few blocks (or a
+//    bucket cannot be sorted), the merge kernel recomputes that queue's list
+//    by an exact radix select that streams the pool again (slow, rare), then
+//    forms the Algorithm 1 decision.
 //  * batched (pools of <= 65,536 blocks): one workgroup of 1024 threads per
 //    instance keeps every key in registers and does scoring, the radix select
 //    of all queues, the sort and the merge in one launch.
@@ -307,18 +308,30 @@ __device__ __forceinline__ int lower_bound_u64(const unsigned long long *a, int 
     return lo;
 }
 
-// Algorithm 1 applied k times to one snapshot: the evict-first list first,
-// then the other (sorted) lists merged by (key, id).  lists: Q segments of
+// Algorithm 1 applied k times to one snapshot: the evict-first list first
+// (copied unless copy1 is false: the caller wrote it), then the other (sorted)
+// lists merged by (key, id).  lists: Q segments of
 // `stride` elements (key << 32 | id), cnt[q] valid in each.  Each element's
 // rank in the merged order is its own position plus, for every other list,
 // the number of smaller elements (binary search); ids are unique, so ranks are
 // distinct.  Returns the decision size.
 __device__ int merge_decision(const unsigned long long *lists, int stride, const int32_t *cnt, int Q,
-                              int qe, int k, int32_t *dec)
+                              int qe, int k, int32_t *dec, bool copy1 = true)
 {
     int n1 = (qe >= 0) ? min(k, (int)cnt[qe]) : 0;
-    for (int j = threadIdx.x; j < n1; j += blockDim.x)
-        dec[j] = (int32_t)(uint32_t)(lists[(long long)qe * stride + j] & 0xFFFFFFFFull);
+    for (int j0 = threadIdx.x; copy1 && j0 < n1; j0 += 8 * blockDim.x) {  // loads first, then stores
+        unsigned long long v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = j0 + u * (int)blockDim.x;
+            v[u] = (j < n1) ? lists[(long long)qe * stride + j] : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = j0 + u * (int)blockDim.x;
+            if (j < n1) dec[j] = (int32_t)(uint32_t)(v[u] & 0xFFFFFFFFull);
+        }
+    }
     int rest = k - n1;
     int total = 0;
     for (int q = 0; q < Q; ++q)
@@ -362,40 +375,47 @@ __device__ __forceinline__ int inst_k(const SelectArgs &a, int inst, int max_k)
 // LDS working set of the per-(instance, queue) selection kernels.
 #define LCAP 16384  // elements (128 KiB of LDS)
 
-// Scratch for lds_select_bound (LDS).
+// Scratch for lds_select_bound and lds_select_rank (LDS).
+#define SEL_PIVOTS 64
+#define SEL_TMP 1024
 struct BoundScratch {
     uint32_t hist[SAE_BINS];
-    uint32_t rem[SAE_MAX_QUEUES];
-    int32_t act[SAE_MAX_QUEUES];
-    Crossing cr[SAE_MAX_QUEUES];
-    uint32_t seg_tot[16];
+    uint32_t wsum[SEL_THREADS / SAE_WAVE];
     unsigned long long mn, mx;
+    uint32_t bin, below, cnt;
+    unsigned long long piv[SEL_PIVOTS], tmp[SEL_TMP], res;
+    uint32_t pcnt[SEL_PIVOTS + 1], kb, kbelow, kn, fill;
 };
 
-// Among n distinct elements held in LDS, the bound B such that exactly `need`
+// Among n distinct elements held in LDS, a bound B such that exactly `need`
 // of them are <= B (1 <= need < n).  Radix select with 11-bit digits starting
-// below the common prefix of the smallest and largest element, so a run of
-// equal keys costs only the digits where the ids differ.  All threads call.
+// below the common prefix of the smallest and largest element (a run of equal
+// keys costs only the digits where the ids differ); it stops at the first
+// digit whose crossing bin ends exactly at the need-th element, and returns
+// that bin's upper edge.  All threads call; blockDim.x a multiple of 64.
 __device__ unsigned long long lds_select_bound(const unsigned long long *el, int n, uint32_t need, BoundScratch &b)
 {
     const int tid = threadIdx.x;
+    const int nt = blockDim.x;
+    const int lane = lane_id();
+    const int wave = tid / SAE_WAVE;
     if (tid == 0) {
         b.mn = ~0ull;
         b.mx = 0;
     }
     __syncthreads();
     unsigned long long mn = ~0ull, mx = 0;
-    for (int i = tid; i < n; i += blockDim.x) {
-        unsigned long long e = el[i];
+    for (int i = tid; i < n; i += nt) {
+        const unsigned long long e = el[i];
         mn = e < mn ? e : mn;
         mx = e > mx ? e : mx;
     }
     for (int d = 32; d > 0; d >>= 1) {
-        unsigned long long o1 = __shfl_xor(mn, d, SAE_WAVE), o2 = __shfl_xor(mx, d, SAE_WAVE);
+        const unsigned long long o1 = __shfl_xor(mn, d, SAE_WAVE), o2 = __shfl_xor(mx, d, SAE_WAVE);
         mn = o1 < mn ? o1 : mn;
         mx = o2 > mx ? o2 : mx;
     }
-    if (lane_id() == 0) {
+    if (lane == 0) {
         atomicMin(&b.mn, mn);
         atomicMax(&b.mx, mx);
     }
@@ -409,39 +429,163 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
     while (true) {
         const int w = sh < SAE_DIGIT_BITS ? sh : SAE_DIGIT_BITS;
         sh -= w;
-        for (int i = tid; i < SAE_BINS; i += blockDim.x) b.hist[i] = 0;
-        if (tid < SAE_MAX_QUEUES) {
-            b.rem[tid] = (tid == 0) ? rem : 0u;
-            b.act[tid] = (tid == 0);
+        const int nb = 1 << w;
+        for (int i = tid; i < nb; i += nt) b.hist[i] = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += nt) {
+            const unsigned long long e = el[i];
+            if ((sh + w >= 64) || (e >> (sh + w)) == prefix) atomicAdd(&b.hist[(uint32_t)(e >> sh) & (nb - 1)], 1u);
         }
         __syncthreads();
-        const uint32_t mask = (1u << w) - 1u;
-        for (int i = tid; i < n; i += blockDim.x) {
-            unsigned long long e = el[i];
-            if ((sh + w >= 64) || (e >> (sh + w)) == prefix) atomicAdd(&b.hist[(uint32_t)(e >> sh) & mask], 1u);
+        // the bin holding the rem-th element: block scan, each thread owning `per` bins
+        const int per = (nb + nt - 1) / nt;
+        uint32_t s = 0;
+        for (int j = 0; j < per; ++j) {
+            const int bi = tid * per + j;
+            s += (bi < nb) ? b.hist[bi] : 0u;
+        }
+        const uint32_t inc = wave_incl_scan(s);
+        if (lane == 63) b.wsum[wave] = inc;
+        __syncthreads();
+        uint32_t run = inc - s;
+        for (int w2 = 0; w2 < wave; ++w2) run += b.wsum[w2];
+        if (run < rem && rem <= run + s) {
+            for (int j = 0; j < per; ++j) {
+                const int bi = tid * per + j;
+                const uint32_t v = (bi < nb) ? b.hist[bi] : 0u;
+                if (run < rem && rem <= run + v) {
+                    b.bin = (uint32_t)bi;
+                    b.below = run;
+                    b.cnt = v;
+                }
+                run += v;
+            }
         }
         __syncthreads();
-        find_crossing(b.hist, 1, b.rem, b.act, b.cr, b.seg_tot);
-        const Crossing c = b.cr[0];
-        prefix = (prefix << w) | (unsigned long long)c.bin;
-        const bool done = (c.cnt == rem) || (sh == 0);
-        rem -= c.below;
+        const uint32_t bin = b.bin, below = b.below, cnt = b.cnt;
         __syncthreads();
-        if (done) break;
+        prefix = (prefix << w) | (unsigned long long)bin;
+        rem -= below;
+        if (cnt == rem || sh == 0) break;
     }
     return (sh == 0) ? prefix : ((prefix << sh) | ((1ull << sh) - 1ull));
 }
 
+// The r-th smallest (1 <= r <= n) of n distinct elements held in LDS.
+// Sample select: SEL_PIVOTS elements taken at evenly spaced positions are
+// ranked into sorted pivots, every element is counted into the pivot interval
+// it falls in, and only the interval holding the r-th element is ranked
+// exactly.  An interval too large for the scratch falls back to the radix
+// select.  All threads call; blockDim.x a multiple of 64 and >= 128.
+__device__ unsigned long long lds_select_rank(const unsigned long long *el, int n, uint32_t r, BoundScratch &b)
+{
+    const int tid = threadIdx.x;
+    const int nt = blockDim.x;
+    const int lane = lane_id();
+    if (n <= SEL_PIVOTS * 2) {
+        for (int t = tid; t < n; t += nt) {
+            const unsigned long long e = el[t];
+            uint32_t rk = 0;
+            for (int i = 0; i < n; ++i) rk += (el[i] < e) ? 1u : 0u;
+            if (rk == r - 1) b.res = e;
+        }
+        __syncthreads();
+        return b.res;
+    }
+    if (tid < SAE_WAVE) {
+        // pivots: one element per lane from evenly spaced positions, ranked within the wave
+        const unsigned long long p = el[(int)(((long long)tid * n) / SEL_PIVOTS)];
+        b.tmp[tid] = p;
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        uint32_t rk = 0;
+#pragma unroll
+        for (int i = 0; i < SEL_PIVOTS; ++i) rk += (b.tmp[i] < p) ? 1u : 0u;
+        b.piv[rk] = p;
+    }
+    if (tid < SEL_PIVOTS + 1) b.pcnt[tid] = 0;
+    if (tid == 0) b.fill = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += nt) {
+        const unsigned long long e = el[i];
+        int k = 0;  // pivots below e
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1)
+            if (b.piv[k + st - 1] < e) k += st;
+        k += (b.piv[SEL_PIVOTS - 1] < e && k == SEL_PIVOTS - 1) ? 1 : 0;
+        atomicAdd(&b.pcnt[k], 1u);
+    }
+    __syncthreads();
+    if (tid < SAE_WAVE) {
+        // the interval holding the r-th element (interval SEL_PIVOTS counted by lane 63)
+        const uint32_t v = b.pcnt[tid] + ((tid == SAE_WAVE - 1) ? b.pcnt[SEL_PIVOTS] : 0u);
+        const uint32_t inc = wave_incl_scan(v);
+        const uint32_t ex = inc - v;
+        if (ex < r && r <= inc) {
+            // lane 63 owns two intervals: split them
+            if (tid == SAE_WAVE - 1 && r > ex + b.pcnt[tid]) {
+                b.kb = SEL_PIVOTS;
+                b.kbelow = ex + b.pcnt[tid];
+                b.kn = b.pcnt[SEL_PIVOTS];
+            } else {
+                b.kb = (uint32_t)tid;
+                b.kbelow = ex;
+                b.kn = b.pcnt[tid];
+            }
+        }
+    }
+    __syncthreads();
+    const uint32_t kb = b.kb, kbelow = b.kbelow, kn = b.kn;
+    if (kn > SEL_TMP) {
+        __syncthreads();
+        const unsigned long long B = lds_select_bound(el, n, r, b);  // exactly r elements <= B
+        // the r-th smallest is the largest element <= B
+        if (tid == 0) b.mx = 0;
+        __syncthreads();
+        unsigned long long mx = 0;
+        for (int i = tid; i < n; i += nt) mx = (el[i] <= B && el[i] > mx) ? el[i] : mx;
+        for (int d = 32; d > 0; d >>= 1) {
+            const unsigned long long o = __shfl_xor(mx, d, SAE_WAVE);
+            mx = o > mx ? o : mx;
+        }
+        if (lane == 0) atomicMax(&b.mx, mx);
+        __syncthreads();
+        return b.mx;
+    }
+    for (int i = tid; i < n; i += nt) {
+        const unsigned long long e = el[i];
+        const bool lo_ok = (kb == 0) || (b.piv[kb - 1] < e);
+        const bool hi_ok = (kb == SEL_PIVOTS) || (e <= b.piv[kb]);
+        if (lo_ok && hi_ok) b.tmp[atomicAdd(&b.fill, 1u)] = e;
+    }
+    __syncthreads();
+    const uint32_t want = r - kbelow - 1;
+    for (int t = tid; t < (int)kn; t += nt) {
+        const unsigned long long e = b.tmp[t];
+        uint32_t rk = 0, i = 0;
+        for (; i + 8 <= kn; i += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) rk += (b.tmp[i + u] < e) ? 1u : 0u;
+        }
+        for (; i < kn; ++i) rk += (b.tmp[i] < e) ? 1u : 0u;
+        if (rk == want) b.res = e;
+    }
+    __syncthreads();
+    return b.res;
+}
+
 // ---------------------------------------------------------------------------
-// Pool-scan engine, step 1: score a sample of every instance -- SAMPLE_WGS
-// contiguous chunks spread evenly over the pool (the whole pool when it has
-// at most SAMPLE_WGS * SAMPLE_CHUNK blocks) -- and record, per chunk, the
-// (key << 32 | id) of every evictable sampled block with its queue, plus a
-// per-queue histogram of the top 11 key bits (spread over SAE_HIST_STRIPES
-// copies so that few workgroups add into the same counter).
+// Pool-scan engine, step 1: score a sample of every instance and record, per
+// sampling workgroup ("chunk"), the (key << 32 | id) of every evictable
+// sampled block grouped by queue, with the count per queue.  A pool of at most
+// SAMPLE_WGS * SAMPLE_CHUNK blocks is sampled whole, a larger one as
+// SAMPLE_WGS * SAMPLE_CHUNK / 4 groups of four consecutive blocks spread
+// evenly over it: a sample without long runs of consecutive ids keeps the
+// buckets of an id-ordered queue (equal keys) small.
+static_assert(SCAN_THREADS == SAMPLE_CHUNK, "one sampled block per thread");
+static_assert(SAMPLE_WGS / SAE_SPLIT_G <= SAE_WAVE, "a group's chunks fit one wave");
 __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
 {
-    extern __shared__ uint32_t sh_hist[];  // [Q][SAE_SBINS]
     __shared__ ScoreTab tab;
     __shared__ unsigned long long tmp[SAMPLE_CHUNK];
     __shared__ uint8_t tq[SAMPLE_CHUNK];
@@ -452,8 +596,24 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
     const int Q = c.Q;
     const long long N = c.N;
     const long long base = (long long)inst * N;
+    long long b = -1;
+    if (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) {
+        const long long start = ((long long)chunk * N) / SAMPLE_WGS;
+        const long long end = (((long long)chunk + 1) * N) / SAMPLE_WGS;  // end - start <= SAMPLE_CHUNK
+        if (start + threadIdx.x < end) b = start + threadIdx.x;
+    } else {
+        const long long G = (long long)SAMPLE_WGS * SAMPLE_CHUNK / 4;
+        const long long g = (long long)chunk * (SAMPLE_CHUNK / 4) + (threadIdx.x >> 2);
+        b = (g * N) / G + (threadIdx.x & 3);  // N / G > 4, so b < N
+    }
+    uint32_t m = 0, off = 0;
+    int32_t la = 0;
+    if (b >= 0) {
+        m = c.meta[base + b];
+        la = c.la[base + b];
+        off = c.off[base + b];
+    }
     load_score_tab(tab, c.state[inst], c);
-    for (int i = threadIdx.x; i < Q * SAE_SBINS; i += blockDim.x) sh_hist[i] = 0;
     if (threadIdx.x < SAE_MAX_QUEUES) {
         qcnt[threadIdx.x] = 0;
         qfill[threadIdx.x] = 0;
@@ -463,18 +623,10 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
         st_s = 0;
     }
     __syncthreads();
-
-    const bool whole = N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK;
-    const long long start = ((long long)chunk * N) / SAMPLE_WGS;
-    const long long end = whole ? (((long long)chunk + 1) * N) / SAMPLE_WGS : start + SAMPLE_CHUNK;
-    const long long reg = ((long long)inst * SAMPLE_WGS + chunk) * SAMPLE_CHUNK;
     uint32_t st = 0;
-    for (long long b = start + threadIdx.x; b < end; b += blockDim.x) {
-        const uint32_t m = c.meta[base + b];
-        const int q = meta_queue(m);
-        if (!meta_evictable(m) || q >= Q) continue;
-        const uint32_t key = block_key(a.now, c.la[base + b], m, c.off[base + b], tab, st);
-        atomicAdd(&sh_hist[q * SAE_SBINS + (key >> 23)], 1u);
+    const int q = meta_queue(m);
+    if (b >= 0 && meta_evictable(m) && q < Q) {
+        const uint32_t key = block_key(a.now, la, m, off, tab, st);
         atomicAdd(&qcnt[q], 1u);
         const uint32_t p = atomicAdd(&pos_s, 1u);  // p < SAMPLE_CHUNK: one slot per sampled block
         tmp[p] = ((unsigned long long)key << 32) | (uint32_t)b;
@@ -484,145 +636,293 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
     __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t o = 0;
-        for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
-            qoff[q] = o;
-            o += qcnt[q];
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+            qoff[qq] = o;
+            o += qcnt[qq];
         }
     }
     if (threadIdx.x < SAE_MAX_QUEUES)
         c.samp_qn[((long long)inst * SAMPLE_WGS + chunk) * SAE_MAX_QUEUES + threadIdx.x] = qcnt[threadIdx.x];
     __syncthreads();
-    // the region holds queue 0's elements, then queue 1's, ...
+    // the chunk's region holds queue 0's elements, then queue 1's, ...
+    const long long reg = ((long long)inst * SAMPLE_WGS + chunk) * SAMPLE_CHUNK;
     const uint32_t n = pos_s;
     for (uint32_t p = threadIdx.x; p < n; p += blockDim.x) {
-        const int q = tq[p];
-        const uint32_t pos = qoff[q] + atomicAdd(&qfill[q], 1u);
+        const int qq = tq[p];
+        const uint32_t pos = qoff[qq] + atomicAdd(&qfill[qq], 1u);
         c.samp[reg + pos] = tmp[p];
-    }
-    uint32_t *gh = c.shist + ((long long)inst * SAE_HIST_STRIPES + (chunk % SAE_HIST_STRIPES)) * Q * SAE_SBINS;
-    for (int i = threadIdx.x; i < Q * SAE_SBINS; i += blockDim.x) {
-        const uint32_t v = sh_hist[i];
-        if (v) atomicAdd(&gh[i], v);
     }
     if (threadIdx.x == 0) set_status(c.status, st_s);
 }
 
-// Pool-scan engine, step 2: per (instance, queue), the candidate bound
-// B = the r-th smallest sampled (key, id), r sized so that the pool holds
-// about 1.5 need + a few standard deviations of blocks <= B.  The top key
-// digit comes from the histogram; the rest from an exact select over the
-// sampled elements of that bin, staged in LDS (a bin of equal keys --
-// num_tokens of an evict-first queue, P = 0 of the last template blocks -- is
-// split by block id).
-__global__ void __launch_bounds__(SEL_THREADS) k_threshold(DevCtx c, SelectArgs a)
+__device__ __forceinline__ int pow2_ge(int x)
+{
+    return x <= 1 ? 1 : 1 << (32 - __clz(x - 1));
+}
+
+// Largest of n elements in LDS (all threads call; n >= 1).
+__device__ unsigned long long lds_max(const unsigned long long *el, int n, unsigned long long *slot)
+{
+    if (threadIdx.x == 0) *slot = 0;
+    __syncthreads();
+    unsigned long long mx = 0;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) mx = el[i] > mx ? el[i] : mx;
+    for (int d = 32; d > 0; d >>= 1) {
+        const unsigned long long o = __shfl_xor(mx, d, SAE_WAVE);
+        mx = o > mx ? o : mx;
+    }
+    if (lane_id() == 0) atomicMax(slot, mx);
+    __syncthreads();
+    return *slot;
+}
+
+// Fixed-step binary searches: every step is unrolled, so that the searches of
+// the several elements one thread holds overlap instead of running one after
+// the other.
+// Last index l < n with a[l] <= x, for a non-decreasing a with a[0] <= x, n <= 2^LOG.
+template <int LOG>
+__device__ __forceinline__ int last_le(const uint32_t *a, int n, uint32_t x)
+{
+    int l = 0;
+#pragma unroll
+    for (int st = 1 << (LOG - 1); st > 0; st >>= 1)
+        if (l + st < n && a[l + st] <= x) l += st;
+    return l;
+}
+
+// Number of elements of the ascending a[0..n) below x (n <= 256, result <= 255).
+__device__ __forceinline__ int count_lt256(const unsigned long long *a, int n, unsigned long long x)
+{
+    int l = 0;
+#pragma unroll
+    for (int st = 128; st > 0; st >>= 1)
+        if (l + st <= n && a[l + st - 1] < x) l += st;
+    return l;
+}
+
+// Ascending sort of n distinct elements src[0..n) (LDS) into dst[0..n) (LDS):
+// each element's position is the number of smaller elements, counted with
+// reads that every lane of a wave makes at the same address.  All threads call.
+__device__ void rank_sort(const unsigned long long *src, int n, unsigned long long *dst)
+{
+    for (int t = threadIdx.x; t < n; t += blockDim.x) {
+        const unsigned long long e = src[t];
+        int rank = 0, i = 0;
+        for (; i + 8 <= n; i += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) rank += (src[i + u] < e) ? 1 : 0;
+        }
+        for (; i < n; ++i) rank += (src[i] < e) ? 1 : 0;
+        dst[rank] = e;
+    }
+    __syncthreads();
+}
+
+// Sample rank r of the candidate bound: with f the sampled fraction and need
+// the expected number of victims, ceil(1.25 f need + 3 sqrt(f need) + 6): the
+// pool then holds about 1.25 need plus a few standard deviations of evictable
+// blocks at or below the r-th smallest sampled (key, id).
+__device__ __forceinline__ uint32_t bound_rank(double need, double f)
+{
+    const double nf = need * f;
+    return (uint32_t)ceil(nf * 1.25 + 3.0 * sqrt(nf) + 6.0);
+}
+
+__device__ __forceinline__ double sample_fraction(long long N)
+{
+    const long long S = (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) ? N : (long long)SAMPLE_WGS * SAMPLE_CHUNK;
+    return (double)S / (double)N;
+}
+
+// Pool-scan engine, step 2a: per (instance, queue) and group of
+// SAMPLE_WGS / SAE_SPLIT_G chunks, keep the group's r_max smallest sampled
+// elements (r_max: the bound rank for need = k), unordered.  The bound's
+// r-th smallest sampled element is then among the kept ones.
+#define GROUP_CHUNKS (SAMPLE_WGS / SAE_SPLIT_G)
+#define GROUP_CAP (GROUP_CHUNKS * SAMPLE_CHUNK)
+__global__ void __launch_bounds__(SEL_THREADS) k_split1(DevCtx c, SelectArgs a)
+{
+    extern __shared__ unsigned long long el[];  // [GROUP_CAP]
+    __shared__ BoundScratch bs;
+    __shared__ uint32_t cbase[GROUP_CHUNKS], cpre[GROUP_CHUNKS + 1];
+    __shared__ uint32_t kept_s;
+    const int g = blockIdx.x;
+    const int q = blockIdx.y;
+    const int inst = blockIdx.z;
+    const int Q = c.Q;
+    const int tid = threadIdx.x;
+    const long long iqg = ((long long)inst * Q + q) * SAE_SPLIT_G + g;
+    const int chunk0 = g * GROUP_CHUNKS;
+    if (tid == 0) kept_s = 0;
+    if (tid < GROUP_CHUNKS) {
+        // chunk tid: where queue q's elements start in its region, and how many (a scan over one wave)
+        const uint32_t *qn = c.samp_qn + ((long long)inst * SAMPLE_WGS + chunk0 + tid) * SAE_MAX_QUEUES;
+        uint32_t v[SAE_MAX_QUEUES];
+#pragma unroll
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) v[qq] = qn[qq];
+        uint32_t o = 0, cnt = 0;
+#pragma unroll
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+            o += (qq < q) ? v[qq] : 0u;
+            cnt = (qq == q) ? v[qq] : cnt;
+        }
+        cbase[tid] = o;
+        const uint32_t inc = wave_incl_scan(cnt);
+        cpre[tid] = inc - cnt;
+        if (tid == GROUP_CHUNKS - 1) cpre[GROUP_CHUNKS] = inc;
+    }
+    __syncthreads();
+    const uint32_t ng = cpre[GROUP_CHUNKS];
+    const unsigned long long *sp = c.samp + ((long long)inst * SAMPLE_WGS + chunk0) * SAMPLE_CHUNK;
+    unsigned long long ev[GROUP_CAP / SEL_THREADS];
+#pragma unroll
+    for (int m = 0; m < GROUP_CAP / SEL_THREADS; ++m) {
+        const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
+        const int ch = last_le<5>(cpre, GROUP_CHUNKS, i);  // the chunk holding element i
+        ev[m] = (i < ng) ? sp[(long long)ch * SAMPLE_CHUNK + cbase[ch] + (i - cpre[ch])] : ~0ull;
+    }
+#pragma unroll
+    for (int m = 0; m < GROUP_CAP / SEL_THREADS; ++m) {
+        const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
+        if (i < ng) el[i] = ev[m];
+    }
+    __syncthreads();
+    const uint32_t rmax = bound_rank((double)inst_k(a, inst, c.max_k), sample_fraction(c.N));
+    unsigned long long *out = c.kept + iqg * SAE_SPLIT_RCAP;
+    if (rmax > SAE_SPLIT_RCAP) {
+        if (tid == 0) c.kept_n[iqg] = ~0u;  // beyond this engine's bound search: exact path
+    } else if (ng <= rmax) {
+        for (uint32_t i = tid; i < ng; i += blockDim.x) out[i] = el[i];
+        if (tid == 0) c.kept_n[iqg] = ng;
+    } else {
+        const unsigned long long B = lds_select_rank(el, (int)ng, rmax, bs);  // exactly rmax elements <= B
+        for (uint32_t i = tid; i < ng; i += blockDim.x) {
+            const unsigned long long e = el[i];
+            if (e <= B) out[atomicAdd(&kept_s, 1u)] = e;
+        }
+        if (tid == 0) c.kept_n[iqg] = rmax;
+    }
+    if (tid == 0) c.samp_tot[iqg] = ng;
+}
+
+// Pool-scan engine, step 2b: per (instance, queue), the candidate bound and the
+// candidate buckets.  The bound is the r-th smallest sampled (key, id); a
+// queue that is estimated small takes every evictable block, and one the
+// sample missed gets a single bucket for all of them.  Bucket upper ends are
+// the sampled elements at or below the bound -- all of them up to
+// SAE_NBUCKET - 1, else an evenly spread subset -- and the last one is the
+// bound.  Resets the scan's spill list.
+#define ALL_EST 2048.0
+__global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
 {
     extern __shared__ unsigned long long el[];  // [LCAP]
     __shared__ BoundScratch bs;
-    __shared__ uint32_t qbase[SAMPLE_WGS], qpre[SAMPLE_WGS + 1], csum[SEL_THREADS / SAE_WAVE];
-    __shared__ uint32_t tot_s, ns_s, bin_s, below_s;
-    __shared__ unsigned long long bound_s;
+    __shared__ uint32_t kn_s[SAE_SPLIT_G], st_s[SAE_SPLIT_G], kpre[SAE_SPLIT_G + 1], tot_s, nsp_s;
+    __shared__ int32_t bad_s, nb_s;
+    __shared__ unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s, mx_s;
     const int q = blockIdx.x;
     const int inst = blockIdx.y;
     const int Q = c.Q;
-    const long long N = c.N;
     const int tid = threadIdx.x;
-    if (tid == 0) {
-        tot_s = 0;
-        ns_s = 0;
-        bound_s = ~0ull;
-    }
-    {
-        // where queue q's elements start in each chunk's region, and how many
-        uint32_t cnt = 0;
-        if (tid < SAMPLE_WGS) {
-            const uint32_t *qn = c.samp_qn + ((long long)inst * SAMPLE_WGS + tid) * SAE_MAX_QUEUES;
-            uint32_t o = 0;
-            for (int qq = 0; qq < q; ++qq) o += qn[qq];
-            qbase[tid] = o;
-            cnt = qn[q];
-        }
-        const uint32_t inc = wave_incl_scan(cnt);
-        if (lane_id() == 63) csum[tid >> 6] = inc;
-        __syncthreads();
-        uint32_t pre = 0;
-        for (int w = 0; w < (tid >> 6); ++w) pre += csum[w];
-        if (tid < SAMPLE_WGS) qpre[tid] = pre + inc - cnt;
-        if (tid == SAMPLE_WGS - 1) qpre[SAMPLE_WGS] = pre + inc;
+    const long long iq = (long long)inst * Q + q;
+    if (tid < SAE_SPLIT_G) kn_s[tid] = c.kept_n[iq * SAE_SPLIT_G + tid];
+    if (tid >= SAE_SPLIT_G && tid < 2 * SAE_SPLIT_G) st_s[tid - SAE_SPLIT_G] = c.samp_tot[iq * SAE_SPLIT_G + tid - SAE_SPLIT_G];
+    if (tid == SEL_THREADS - 1) {
+        c.spill_n[iq] = 0;  // this call's spill list starts empty
+        nsp_s = 0;
+        nb_s = 0;
+        bound_s = 0;
     }
     __syncthreads();
-    // histogram of the top 9 key bits over all stripes; thread t < 512 owns bin t
-    uint32_t v = 0;
-    if (tid < SAE_SBINS) {
-#pragma unroll 8
-        for (int st = 0; st < SAE_HIST_STRIPES; ++st) {
-            uint32_t *g = c.shist + (((long long)inst * SAE_HIST_STRIPES + st) * Q + q) * SAE_SBINS + tid;
-            v += *g;
-            *g = 0;  // ready for the next call
+    if (tid < SAE_WAVE) {
+        const bool in = tid < SAE_SPLIT_G;
+        const uint32_t kn = in ? kn_s[tid] : 0u;
+        const uint32_t kv = (kn == ~0u) ? 0u : kn;
+        const uint32_t inc = wave_incl_scan(kv);
+        uint32_t t = in ? st_s[tid] : 0u;
+        for (int d = 32; d > 0; d >>= 1) t += __shfl_xor(t, d, SAE_WAVE);
+        const bool bad = __ballot(kn == ~0u) != 0ull;
+        if (in) kpre[tid] = inc - kv;
+        if (tid == SAE_SPLIT_G - 1) kpre[SAE_SPLIT_G] = inc;
+        if (tid == 0) {
+            tot_s = t;
+            bad_s = bad ? 1 : 0;
         }
     }
-    const uint32_t incl = wave_incl_scan(v);
-    if (lane_id() == 63) csum[tid >> 6] = incl;
-    __syncthreads();
-    uint32_t pre = 0;
-    for (int w = 0; w < (tid >> 6); ++w) pre += csum[w];
-    const uint32_t cum = pre + incl;  // inclusive prefix over bins
-    if (tid == SEL_THREADS - 1) tot_s = cum;
     __syncthreads();
     const uint32_t tot = tot_s;
-    const long long S = (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) ? N : (long long)SAMPLE_WGS * SAMPLE_CHUNK;
-    const double f = (double)S / (double)N;
+    const int kq = inst_k(a, inst, c.max_k);
+    const double f = sample_fraction(c.N);
     const double est = (double)tot / f;
-    const double need = fmin((double)inst_k(a, inst, c.max_k), est);
-    const double nf = need * f;
-    const uint32_t r = (uint32_t)ceil(nf * 1.25 + 3.0 * sqrt(nf) + 6.0);
-    if (!(need > 0.0)) {
-        if (tid == 0) bound_s = 0ull;
-    } else if (est > 0.5 * (double)c.cand_cap && r < tot) {
-        // the bin where the r-th sampled element lies
-        if (tid < SAE_SBINS && cum - v < r && r <= cum) {
-            bin_s = (uint32_t)tid;
-            below_s = cum - v;
+    const uint32_t r = bound_rank(fmin((double)kq, est), f);
+    if (kq == 0) {
+        // nothing to select: no candidates
+    } else if (bad_s) {
+        if (tid == 0) nb_s = -1;  // exact path
+    } else if (tot == 0) {
+        // the sample holds no block of this queue: all its evictable blocks, one bucket
+        if (tid == 0) {
+            bound_s = ~0ull;
+            spl[0] = ~0ull;
+            nb_s = 1;
         }
-        __syncthreads();
-        const uint32_t bin = bin_s;
-        const uint32_t rem = r - below_s;
-        const unsigned long long edge = (((unsigned long long)bin + 1ull) << 55) - 1ull;
-        // stage the sampled elements of queue q in that bin: index math first,
-        // then every load in flight, then the LDS writes
-        const unsigned long long *sp = c.samp + (long long)inst * SAMPLE_WGS * SAMPLE_CHUNK;
-        const uint32_t nq = qpre[SAMPLE_WGS];
-        for (uint32_t r0 = 0; r0 < nq; r0 += 16 * SEL_THREADS) {
-            unsigned long long ev[16];
+    } else {
+        const bool all = (r >= tot) || (est <= ALL_EST);
+        const uint32_t K = kpre[SAE_SPLIT_G];  // kept elements, <= SAE_SPLIT_G * SAE_SPLIT_RCAP = LCAP
+        const unsigned long long *kp = c.kept + iq * SAE_SPLIT_G * SAE_SPLIT_RCAP;
+        for (uint32_t i0 = 0; i0 < K; i0 += 4 * SEL_THREADS) {
+            unsigned long long ev[4];
 #pragma unroll
-            for (int m = 0; m < 16; ++m) {
-                const uint32_t i = r0 + tid + (uint32_t)m * SEL_THREADS;
-                ev[m] = ~0ull;
-                if (i < nq) {
-                    int lo = 0, hi = SAMPLE_WGS - 1;  // last chunk with qpre <= i
-                    while (lo < hi) {
-                        const int mid = (lo + hi + 1) >> 1;
-                        if (qpre[mid] <= i) lo = mid;
-                        else hi = mid - 1;
-                    }
-                    ev[m] = sp[(long long)lo * SAMPLE_CHUNK + qbase[lo] + (i - qpre[lo])];
-                }
+            for (int m = 0; m < 4; ++m) {
+                const uint32_t i = i0 + tid + (uint32_t)m * SEL_THREADS;
+                const int g = last_le<3>(kpre, SAE_SPLIT_G, i);
+                ev[m] = (i < K) ? kp[(long long)g * SAE_SPLIT_RCAP + (i - kpre[g])] : ~0ull;
             }
 #pragma unroll
-            for (int m = 0; m < 16; ++m) {
-                if (ev[m] != ~0ull && (uint32_t)(ev[m] >> 55) == bin) {
-                    const uint32_t pos = atomicAdd(&ns_s, 1u);
-                    if (pos < LCAP) el[pos] = ev[m];
-                }
+            for (int m = 0; m < 4; ++m) {
+                const uint32_t i = i0 + tid + (uint32_t)m * SEL_THREADS;
+                if (i < K) el[i] = ev[m];
             }
         }
         __syncthreads();
-        const uint32_t ns = ns_s;
-        unsigned long long bnd = edge;  // the whole bin
-        if (rem < ns && ns <= LCAP) bnd = lds_select_bound(el, (int)ns, rem, bs);
-        if (tid == 0) bound_s = bnd;
+        unsigned long long bound;
+        uint32_t rr;  // kept elements at or below the bound
+        if (all) {
+            bound = ~0ull;
+            rr = K;
+        } else if (r < K) {
+            bound = lds_select_rank(el, (int)K, r, bs);
+            rr = r;
+        } else {
+            bound = lds_max(el, (int)K, &mx_s);
+            rr = K;
+        }
+        // upper ends: the elements <= bound, or every stride-th kept one of them
+        const uint32_t stride = rr <= SAE_NBUCKET - 1 ? 1u : (rr + SAE_NBUCKET - 3) / (SAE_NBUCKET - 2);
+        for (uint32_t i = tid; i < K; i += blockDim.x) {
+            const unsigned long long e = el[i];
+            if (e <= bound && (stride == 1u || (i % stride) == 0u)) {
+                const uint32_t p = atomicAdd(&nsp_s, 1u);
+                if (p < SAE_NBUCKET - 1) spl_raw[p] = e;
+            }
+        }
+        __syncthreads();
+        const int np = nsp_s < SAE_NBUCKET - 1 ? (int)nsp_s : SAE_NBUCKET - 1;
+        rank_sort(spl_raw, np, spl);
+        if (tid == 0) {
+            int nb = np;
+            if (nb == 0 || spl[nb - 1] != bound) spl[nb++] = bound;  // the last upper end is the bound
+            bound_s = bound;
+            nb_s = nb;
+        }
     }
     __syncthreads();
-    if (tid == 0) c.thr[(long long)inst * Q + q] = bound_s;
+    const int nb = nb_s;
+    if (tid < nb) c.split[iq * SAE_NBUCKET + tid] = spl[tid];
+    if (tid == 0) {
+        c.thr[iq] = bound_s;
+        c.nsplit[iq] = nb;
+    }
 }
 
 // Pool-scan engine, step 3: one streaming pass over the whole pool.
@@ -834,129 +1134,384 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
     if (threadIdx.x == 0) set_status(c.status, st_s);
 }
 
-// Pool-scan engine, step 4: exact k smallest (key, id) of one (instance,
-// queue).  The candidates (every evictable block of the queue with
-// (key, id) <= bound) are gathered into LDS; if the bound admitted fewer than
-// needed, or more than fit, the workgroup instead streams the instance's pool
-// and radix-selects exactly (slow; SAE_ST_SELECT_FALLBACK).
-__global__ void __launch_bounds__(SEL_THREADS) k_select(DevCtx c, SelectArgs a, int P)
+// Sum over a wave of n words p[0], p[stride], ... (n <= 32 * SAE_WAVE): every
+// load is issued before the first is used.
+__device__ uint32_t wave_sum_strided(const uint32_t *p, int n, long long stride)
 {
-    extern __shared__ unsigned long long el[];  // [LCAP]
-    __shared__ BoundScratch bs;
-    __shared__ SelState st;
-    __shared__ ScoreTab tab;
+    uint32_t t[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+        const int w = u * SAE_WAVE + lane_id();
+        t[u] = (w < n) ? p[(long long)w * stride] : 0u;
+    }
+    uint32_t s = 0;
+#pragma unroll
+    for (int u = 0; u < 32; ++u) s += t[u];
+    for (int d = 32; d > 0; d >>= 1) s += __shfl_xor(s, d, SAE_WAVE);
+    return s;
+}
+
+// Pool-scan engine, step 4: per (instance, queue) and slice, where the
+// candidates in scan order (the workgroups' regions, then the spill list) are
+// cut into SAE_GATHER_S equal slices: stage the slice in LDS, find each
+// candidate's bucket (the first upper end >= it) and write the slice grouped by
+// bucket (counting sort) to its place in cand: slice s starts at g_base[s],
+// its bucket b at g_rel[s][b] with g_cnt[s][b] elements.  Also sums the
+// evictable blocks of a 1 / SAE_GATHER_S share of the scan workgroups.
+#define GATHER_THREADS 256
+#define GATHER_RPT (2048 / GATHER_THREADS)  // scan workgroups per thread (scan_gx <= 2048)
+__global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs a)
+{
+    extern __shared__ unsigned long long el[];  // [SAE_LCAP / SAE_GATHER_S + 1]
+    __shared__ unsigned long long spl[SAE_NBUCKET];
     __shared__ uint32_t offs[2048 + 1];
-    __shared__ uint32_t nev_s, lcount, wsum[16];
-    const int q = blockIdx.x;
-    const int inst = blockIdx.y;
+    __shared__ uint32_t hist[SAE_NBUCKET], boff[SAE_NBUCKET], wsum[GATHER_THREADS / SAE_WAVE];
+    __shared__ uint32_t nev_s;
+    const int s = blockIdx.x;
+    const int q = blockIdx.y;
+    const int inst = blockIdx.z;
     const int Q = c.Q;
     const int gx = c.scan_gx;
-    const long long iq = (long long)inst * Q + q;
-    const long long N = c.N;
-    const long long base = (long long)inst * N;
     const int tid = threadIdx.x;
-    if (tid == 0) {
-        nev_s = 0;
-        lcount = 0;
+    const int lane = lane_id();
+    const long long iq = (long long)inst * Q + q;
+    const long long iqs = iq * SAE_GATHER_S + s;
+    const int w0 = (s * gx) / SAE_GATHER_S, w1 = ((s + 1) * gx) / SAE_GATHER_S;  // evictable-count share
+    // one round of loads: every workgroup's candidate count, this share's evictable
+    // counts, the bucket upper ends
+    const int NB = c.nsplit[iq];
+    const uint32_t ns = c.spill_n[iq];
+    uint32_t cv[GATHER_RPT];
+#pragma unroll
+    for (int u = 0; u < GATHER_RPT; ++u) {
+        const int w = tid * GATHER_RPT + u;
+        cv[u] = (w < gx) ? c.creg_n[((long long)inst * gx + w) * Q + q] : 0u;
     }
-    load_score_tab(tab, c.state[inst], c);
+    const uint32_t nv = (w0 + tid < w1) ? c.nev_part[((long long)inst * gx + w0 + tid) * Q + q] : 0u;
+    const unsigned long long sv = c.split[iq * SAE_NBUCKET + tid];
+    if (tid == 0) nev_s = 0;
+    hist[tid] = 0;
+    spl[tid] = (tid < NB) ? sv : ~0ull;
+    uint32_t loc = 0;
+#pragma unroll
+    for (int u = 0; u < GATHER_RPT; ++u) loc += cv[u];
+    const uint32_t inc = wave_incl_scan(loc);
+    if (lane == 63) wsum[tid >> 6] = inc;
+    uint32_t nvs = nv;
+    for (int d = 32; d > 0; d >>= 1) nvs += __shfl_xor(nvs, d, SAE_WAVE);
     __syncthreads();
-    // evictable count and candidate-region offsets (exclusive scan over workgroups)
-    uint32_t nv = 0, r0 = 0, r1 = 0;
-    const int w0 = 2 * tid, w1 = 2 * tid + 1;
-    if (w0 < gx) {
-        nv += c.nev_part[((long long)inst * gx + w0) * Q + q];
-        r0 = c.creg_n[((long long)inst * gx + w0) * Q + q];
-    }
-    if (w1 < gx) {
-        nv += c.nev_part[((long long)inst * gx + w1) * Q + q];
-        r1 = c.creg_n[((long long)inst * gx + w1) * Q + q];
-    }
+    if (lane == 0 && nvs) atomicAdd(&nev_s, nvs);
     {
-        uint32_t v = wave_incl_scan(nv);
-        if (lane_id() == 63 && v) atomicAdd(&nev_s, v);
-        uint32_t loc = r0 + r1;
-        uint32_t inc = wave_incl_scan(loc);
-        if (lane_id() == 63) wsum[tid >> 6] = inc;
+        uint32_t o = inc - loc;
+        for (int w = 0; w < (tid >> 6); ++w) o += wsum[w];
+#pragma unroll
+        for (int u = 0; u < GATHER_RPT; ++u) {
+            const int w = tid * GATHER_RPT + u;
+            if (w < gx) offs[w] = o;
+            o += cv[u];
+        }
+        if (tid == GATHER_THREADS - 1) offs[gx] = o;  // cv is 0 beyond gx
+    }
+    __syncthreads();
+    const uint32_t total_r = offs[gx];
+    const uint32_t nsp = ns < (uint32_t)c.cand_cap ? ns : (uint32_t)c.cand_cap;
+    const uint32_t C = total_r + nsp;
+    const uint32_t lo = (uint32_t)(((unsigned long long)s * C) / SAE_GATHER_S);
+    const uint32_t hi = (uint32_t)(((unsigned long long)(s + 1) * C) / SAE_GATHER_S);
+    const uint32_t n = hi - lo;
+    if (tid == 0) {
+        c.g_nev[iqs] = nev_s;
+        c.g_base[iqs] = lo;
+        c.g_tot[iqs] = (NB <= 0) ? 0u : (C > SAE_LCAP ? (uint32_t)SAE_LCAP + 1u : n);
+    }
+    if (NB <= 0 || C > SAE_LCAP) return;  // uniform: nothing wanted, exact path, or too many candidates
+    // stage the slice: index math first, then every load in flight
+    const unsigned long long *reg = c.creg + (long long)inst * gx * Q * SAE_CAND_REGION;
+    const unsigned long long *spill = c.spill + iq * c.cand_cap;
+    for (uint32_t i0 = 0; i0 < n; i0 += 4 * GATHER_THREADS) {
+        unsigned long long ev[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const uint32_t i = lo + i0 + tid + (uint32_t)m * GATHER_THREADS;
+            const int l = last_le<11>(offs, gx, i);  // the workgroup holding candidate i
+            ev[m] = (i < total_r) ? reg[((long long)l * Q + q) * SAE_CAND_REGION + (i - offs[l])]
+                                  : ((i < hi) ? spill[i - total_r] : ~0ull);
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const uint32_t i = i0 + tid + (uint32_t)m * GATHER_THREADS;
+            if (i < n) {
+                el[i] = ev[m];
+                atomicAdd(&hist[count_lt256(spl, NB, ev[m])], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    {
+        const uint32_t v = hist[tid];
+        const uint32_t inc2 = wave_incl_scan(v);
+        if (lane == 63) wsum[tid >> 6] = inc2;
         __syncthreads();
         uint32_t pre = 0;
         for (int w = 0; w < (tid >> 6); ++w) pre += wsum[w];
-        const uint32_t ex = pre + inc - loc;
-        if (w0 < gx) offs[w0] = ex;
-        if (w1 < gx) offs[w1] = ex + r0;
+        boff[tid] = pre + inc2 - v;
+        c.g_rel[iqs * SAE_NBUCKET + tid] = pre + inc2 - v;
+        c.g_cnt[iqs * SAE_NBUCKET + tid] = v;
+    }
+    __syncthreads();
+    unsigned long long *out = c.cand + iq * SAE_LCAP + lo;
+    for (uint32_t i = tid; i < n; i += GATHER_THREADS) {
+        const unsigned long long e = el[i];
+        out[atomicAdd(&boff[count_lt256(spl, NB, e)], 1u)] = e;
+    }
+}
+
+// Pool-scan engine, step 5: one workgroup per bucket of one (instance, queue).
+// The bucket's elements are its pieces in the slices; its offset in the
+// queue's sorted list is the sum over slices of the elements below it.  It is
+// sorted (rank counting; sort_lds when larger than a workgroup) and the part
+// that falls within the first need = min(k, evictable) positions is written
+// (for the evict-first queue also to the decision, whose first positions it
+// fills: Algorithm 1, stage 1).  Nothing is written when the queue needs the
+// exact path (too few or too many candidates, a full spill list, a bucket too
+// large to sort): the merge kernel then recomputes that queue's whole list.
+#define BUCKET_THREADS 256
+__global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs a)
+{
+    extern __shared__ unsigned long long bel[];  // [2 * SAE_BSORT]
+    __shared__ uint32_t base_v[SAE_GATHER_S], rel_v[SAE_GATHER_S], pre_v[SAE_GATHER_S + 1];
+    __shared__ uint32_t C_s, nev_s, off_s;
+    const int j = blockIdx.x;
+    const int q = blockIdx.y;
+    const int inst = blockIdx.z;
+    const int Q = c.Q;
+    const int tid = threadIdx.x;
+    const long long iq = (long long)inst * Q + q;
+    // one round of loads; the first wave sums the slices
+    const int NB = c.nsplit[iq];
+    const uint32_t ns = c.spill_n[iq];
+    if (tid < SAE_WAVE) {
+        const bool in = tid < SAE_GATHER_S;
+        const long long iqs = iq * SAE_GATHER_S + tid;
+        uint32_t tv = in ? c.g_tot[iqs] : 0u;
+        uint32_t nv = in ? c.g_nev[iqs] : 0u;
+        const uint32_t bv = in ? c.g_base[iqs] : 0u;
+        uint32_t rv = in ? c.g_rel[iqs * SAE_NBUCKET + j] : 0u;
+        const uint32_t cv = in ? c.g_cnt[iqs * SAE_NBUCKET + j] : 0u;
+        const uint32_t inc = wave_incl_scan(cv);
+        if (in) {
+            base_v[tid] = bv;
+            rel_v[tid] = rv;
+            pre_v[tid] = inc - cv;
+        }
+        if (tid == SAE_GATHER_S - 1) pre_v[SAE_GATHER_S] = inc;
+        for (int d = 32; d > 0; d >>= 1) {
+            tv += __shfl_xor(tv, d, SAE_WAVE);
+            nv += __shfl_xor(nv, d, SAE_WAVE);
+            rv += __shfl_xor(rv, d, SAE_WAVE);
+        }
         if (tid == 0) {
-            uint32_t t = 0;
-            for (int w = 0; w < 16; ++w) t += wsum[w];
-            offs[2048] = t;
+            C_s = tv;
+            nev_s = nv;
+            off_s = rv;
         }
     }
     __syncthreads();
-    const uint32_t nev = nev_s;
-    const uint32_t total_r = offs[2048];
-    const uint32_t ns = c.spill_n[iq];
-    const uint32_t nsp = ns < (uint32_t)c.cand_cap ? ns : (uint32_t)c.cand_cap;
-    const uint32_t nc = total_r + nsp;
-    const uint32_t need = (uint32_t)min((long long)inst_k(a, inst, c.max_k), (long long)nev);
-    const bool fb = (a.flags & SAE_SS_FORCE_FALLBACK) || ns > (uint32_t)c.cand_cap || nc < need || nc > LCAP;
+    if (j >= NB) return;  // uniform per workgroup
+    const uint32_t C = C_s, off = off_s, n = pre_v[SAE_GATHER_S];
     if (tid == 0) {
-        if (fb && need > 0) set_status(c.status, SAE_ST_SELECT_FALLBACK);
-        uint32_t *dbg = c.sel_stats + iq * 4;
-        dbg[0] = nev;
-        dbg[1] = total_r;
-        dbg[2] = ns;
-        dbg[3] = fb ? 1u : 0u;
+        c.bsize[iq * SAE_NBUCKET + j] = n;
+        c.bbelow[iq * SAE_NBUCKET + j] = off;
     }
-    uint32_t dummy = 0;
+    const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
+    const uint32_t need = nev_s < kq ? nev_s : kq;
+    if ((a.flags & SAE_SS_FORCE_FALLBACK) || C > SAE_LCAP || ns > (uint32_t)c.cand_cap || C < need) return;
+    if (off >= need || n == 0 || n > SAE_BSORT) return;
+    const unsigned long long *cand = c.cand + iq * SAE_LCAP;
+    const uint32_t m = (need - off) < n ? (need - off) : n;
+    const long long ob = iq * c.max_k + off;
+    int32_t *dec = (q == c.ef_queue) ? a.decision + (long long)inst * c.max_k + off : nullptr;
+    auto elem = [&](uint32_t t) {
+        const int sl = last_le<4>(pre_v, SAE_GATHER_S, t);  // the slice holding element t
+        return cand[base_v[sl] + rel_v[sl] + (t - pre_v[sl])];
+    };
+    if (n <= BUCKET_THREADS) {
+        const unsigned long long e0 = (tid < (int)n) ? elem((uint32_t)tid) : ~0ull;
+        if (tid < (int)n) bel[tid] = e0;
+        __syncthreads();
+        if (tid < (int)n) {
+            uint32_t rank = 0, i = 0;
+            for (; i + 8 <= n; i += 8) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) rank += (bel[i + u] < e0) ? 1u : 0u;  // LDS broadcast reads
+            }
+            for (; i < n; ++i) rank += (bel[i] < e0) ? 1u : 0u;
+            if (rank < m) {
+                const int32_t id = (int32_t)(uint32_t)(e0 & 0xFFFFFFFFull);
+                a.victims[ob + rank] = id;
+                if (a.scores) a.scores[ob + rank] = __uint_as_float((uint32_t)(e0 >> 32));
+                c.sel[ob + rank] = e0;
+                if (dec) dec[rank] = id;
+            }
+        }
+        return;
+    }
+    // a larger bucket: sample sort inside it -- SEL_PIVOTS pivots from evenly
+    // spaced positions, sub-buckets by counting, rank counting within each
+    __shared__ unsigned long long piv[SEL_PIVOTS];
+    __shared__ uint32_t sh[SEL_PIVOTS + 2], sfill[SEL_PIVOTS + 1];
+    __shared__ uint8_t sk[SAE_BSORT];
+    unsigned long long *bel2 = bel + SAE_BSORT;
+    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) bel[t] = elem(t);
+    if (tid <= SEL_PIVOTS) {
+        sh[tid] = 0;
+        sfill[tid] = 0;
+    }
+    __syncthreads();
+    __shared__ unsigned long long praw[SEL_PIVOTS];
+    if (tid < SAE_WAVE) {
+        const unsigned long long p = bel[(uint32_t)(((unsigned long long)tid * n) / SEL_PIVOTS)];
+        praw[tid] = p;
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        uint32_t rk = 0;
+#pragma unroll
+        for (int i = 0; i < SEL_PIVOTS; ++i) rk += (praw[i] < p) ? 1u : 0u;
+        piv[rk] = p;
+    }
+    __syncthreads();
+    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
+        const unsigned long long e = bel[t];
+        int k = 0;  // pivots below e
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1)
+            if (piv[k + st - 1] < e) k += st;
+        k += (k == SEL_PIVOTS - 1 && piv[SEL_PIVOTS - 1] < e) ? 1 : 0;
+        sk[t] = (uint8_t)k;
+        atomicAdd(&sh[k], 1u);
+    }
+    __syncthreads();
+    if (tid < SAE_WAVE) {
+        // exclusive offsets of the SEL_PIVOTS + 1 sub-buckets (lane 63 also owns the last one)
+        const uint32_t v = sh[tid] + ((tid == SAE_WAVE - 1) ? sh[SEL_PIVOTS] : 0u);
+        const uint32_t inc = wave_incl_scan(v);
+        const uint32_t ex = inc - v;
+        const uint32_t h0 = sh[tid];
+        __builtin_amdgcn_wave_barrier();
+        sh[tid] = ex;
+        if (tid == SAE_WAVE - 1) {
+            sh[SEL_PIVOTS] = ex + h0;
+            sh[SEL_PIVOTS + 1] = inc;
+        }
+    }
+    __syncthreads();
+    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
+        const int k = sk[t];
+        bel2[sh[k] + atomicAdd(&sfill[k], 1u)] = bel[t];
+    }
+    __syncthreads();
+    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
+        // position t of the sub-bucket order: rank within its sub-bucket
+        const unsigned long long e = bel2[t];
+        int k = 0;
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1)
+            if (sh[k + st] <= t) k += st;
+        k += (k == SEL_PIVOTS - 1 && sh[SEL_PIVOTS] <= t) ? 1 : 0;
+        const uint32_t lo = sh[k], hi = sh[k + 1];
+        uint32_t rk = lo, i = lo;
+        for (; i + 8 <= hi; i += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) rk += (bel2[i + u] < e) ? 1u : 0u;
+        }
+        for (; i < hi; ++i) rk += (bel2[i] < e) ? 1u : 0u;
+        if (rk < m) {
+            const int32_t id = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
+            a.victims[ob + rk] = id;
+            if (a.scores) a.scores[ob + rk] = __uint_as_float((uint32_t)(e >> 32));
+            c.sel[ob + rk] = e;
+            if (dec) dec[rk] = id;
+        }
+    }
+}
 
-    if (!fb) {
-        // gather the candidates: index math first, then every load in flight
-        const unsigned long long *reg = c.creg + ((long long)inst * gx) * Q * SAE_CAND_REGION;
-        {
-            unsigned long long ev[LCAP / SEL_THREADS];
+// Pool-scan engine, step 6, per instance: the final list size of every queue;
+// the exact path for a queue whose buckets cannot give its list (or when
+// forced): stream the instance's pool, radix-select the need smallest
+// (key, id) and sort them; then the Algorithm 1 decision.
+__global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, int P, long long lds_bytes)
+{
+    extern __shared__ unsigned long long el[];  // exact path [2 * max(P, 256)]; sorted lists
+    __shared__ SelState st;
+    __shared__ ScoreTab tab;
+    __shared__ int32_t cnt[SAE_MAX_QUEUES];
+    __shared__ uint32_t need_s[SAE_MAX_QUEUES], nev_s[SAE_MAX_QUEUES], cand_s[SAE_MAX_QUEUES];
+    __shared__ int32_t fb_s[SAE_MAX_QUEUES];
+    __shared__ uint32_t lcount, st_s;
+    const int inst = blockIdx.x;
+    const int Q = c.Q;
+    const int tid = threadIdx.x;
+    const int wave = tid / SAE_WAVE;
+    const int lane = lane_id();
+    const long long N = c.N;
+    const long long base = (long long)inst * N;
+    const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
+    load_score_tab(tab, c.state[inst], c);
+    if (tid == 0) st_s = 0;
+    // one wave per queue: candidates, evictable blocks, whether the buckets suffice
+    if (wave < Q) {
+        const int q = wave;
+        const long long iq = (long long)inst * Q + q;
+        // every load of this wave in one round
+        const int NB = c.nsplit[iq];
+        const uint32_t ns = c.spill_n[iq];
+        const uint32_t gt = (lane < SAE_GATHER_S) ? c.g_tot[iq * SAE_GATHER_S + lane] : 0u;
+        const uint32_t gn = (lane < SAE_GATHER_S) ? c.g_nev[iq * SAE_GATHER_S + lane] : 0u;
+        uint32_t bb[SAE_NBUCKET / SAE_WAVE], bz[SAE_NBUCKET / SAE_WAVE];
 #pragma unroll
-            for (int m = 0; m < LCAP / SEL_THREADS; ++m) {
-                const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
-                ev[m] = 0;
-                if (i < total_r) {
-                    int lo = 0, hi = gx - 1;  // last region with offs <= i
-                    while (lo < hi) {
-                        const int mid = (lo + hi + 1) >> 1;
-                        if (offs[mid] <= i) lo = mid;
-                        else hi = mid - 1;
-                    }
-                    ev[m] = reg[((long long)lo * Q + q) * SAE_CAND_REGION + (i - offs[lo])];
-                }
-            }
-#pragma unroll
-            for (int m = 0; m < LCAP / SEL_THREADS; ++m) {
-                const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
-                if (i < total_r) el[i] = ev[m];
-            }
+        for (int u = 0; u < SAE_NBUCKET / SAE_WAVE; ++u) {
+            bb[u] = c.bbelow[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
+            bz[u] = c.bsize[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
         }
-        const unsigned long long *spill = c.spill + iq * c.cand_cap;
-        for (uint32_t j = tid; j < nsp; j += blockDim.x) el[total_r + j] = spill[j];
-        __syncthreads();
-        if (need > 0 && need < nc) {
-            const unsigned long long T = lds_select_bound(el, (int)nc, need, bs);
-            // keep the `need` elements <= T, packed at the front
-            unsigned long long mine[LCAP / SEL_THREADS];
-#pragma unroll
-            for (int j = 0; j < LCAP / SEL_THREADS; ++j) {
-                const int i = tid + j * SEL_THREADS;
-                mine[j] = (i < (int)nc) ? el[i] : ~0ull;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int j = 0; j < LCAP / SEL_THREADS; ++j) {
-                if (mine[j] <= T) {
-                    const uint32_t pos = atomicAdd(&lcount, 1u);
-                    el[pos] = mine[j];
-                }
-            }
+        uint32_t C = gt, nev = gn;
+        for (int d = 32; d > 0; d >>= 1) {
+            C += __shfl_xor(C, d, SAE_WAVE);
+            nev += __shfl_xor(nev, d, SAE_WAVE);
         }
-        __syncthreads();
-    } else {
-        // exact slow path: stream the pool for this queue
+        const uint32_t need = nev < kq ? nev : kq;
+        // a bucket that holds some of the first `need` positions but is too big to sort
+        bool big = false;
+#pragma unroll
+        for (int u = 0; u < SAE_NBUCKET / SAE_WAVE; ++u)
+            big |= (u * SAE_WAVE + lane < NB) && bb[u] < need && bz[u] > SAE_BSORT;
+        const bool anybig = __ballot(big) != 0ull;
+        if (lane == 0) {
+            const bool fb = (a.flags & SAE_SS_FORCE_FALLBACK) || NB < 0 ||
+                            (need > 0 && (NB == 0 || C < need || C > SAE_LCAP || ns > (uint32_t)c.cand_cap ||
+                                          anybig));
+            need_s[q] = need;
+            nev_s[q] = nev;
+            cand_s[q] = C;
+            fb_s[q] = (fb && need > 0) ? 1 : 0;
+            uint32_t *dbg = c.sel_stats + iq * 4;
+            dbg[0] = nev;
+            dbg[1] = C;
+            dbg[2] = ns;
+            dbg[3] = fb_s[q];
+            cnt[q] = (int32_t)need;
+            a.count[iq] = (int32_t)need;
+            c.sel_count[iq] = (int32_t)need;
+        }
+    }
+    __syncthreads();
+    uint32_t dummy = 0;
+    for (int q = 0; q < Q; ++q) {
+        if (!fb_s[q]) continue;  // uniform
+        if (tid == 0) {
+            set_status(c.status, SAE_ST_SELECT_FALLBACK);
+            lcount = 0;
+        }
+        const uint32_t need = need_s[q];
         auto for_each = [&](auto &&fn) {
             for (long long b = tid; b < N; b += blockDim.x) {
                 const uint32_t m = c.meta[base + b];
@@ -967,21 +1522,23 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(DevCtx c, SelectArgs a, 
         };
         uint32_t needv[SAE_MAX_QUEUES], nevv[SAE_MAX_QUEUES];
         needv[0] = need;
-        nevv[0] = nev;
+        nevv[0] = nev_s[q];
         sel_init(st, 1, needv, nevv);
         for (int p = 0; p < 6 && st.any_active; ++p) {
             const int s = (p < 5) ? 53 - 11 * p : 0;
             const int w = (p < 5) ? 11 : 9;
-            for (int i = tid; i < SAE_BINS; i += blockDim.x) bs.hist[i] = 0;
+            uint32_t *hist = reinterpret_cast<uint32_t *>(el);
+            for (int i = tid; i < SAE_BINS; i += blockDim.x) hist[i] = 0;
             __syncthreads();
             const unsigned long long pre = st.prefix[0];
             for_each([&](unsigned long long e) {
-                if (p == 0 || (e >> (s + w)) == pre) atomicAdd(&bs.hist[(uint32_t)(e >> s) & ((1u << w) - 1u)], 1u);
+                if (p == 0 || (e >> (s + w)) == pre) atomicAdd(&hist[(uint32_t)(e >> s) & ((1u << w) - 1u)], 1u);
             });
             __syncthreads();
-            find_crossing(bs.hist, 1, st.rem, st.active, st.cr, st.seg_tot);
+            find_crossing(hist, 1, st.rem, st.active, st.cr, st.seg_tot);
             sel_step(st, 1, s, w, p == 5);
         }
+        __syncthreads();
         for_each([&](unsigned long long e) {
             if (sel_take(st, 0, e)) {
                 const uint32_t pos = atomicAdd(&lcount, 1u);
@@ -989,42 +1546,45 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(DevCtx c, SelectArgs a, 
             }
         });
         __syncthreads();
+        const uint32_t out = need < (uint32_t)P ? need : (uint32_t)P;
+        const int PS = P < 256 ? 256 : P;
+        for (int i = tid + (int)out; i < PS; i += blockDim.x) el[i] = ~0ull;
+        __syncthreads();
+        sort_lds(el, PS);
+        const long long ob = ((long long)inst * Q + q) * c.max_k;
+        for (uint32_t j = tid; j < out; j += blockDim.x) {
+            const unsigned long long e = el[j];
+            a.victims[ob + j] = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
+            if (a.scores) a.scores[ob + j] = __uint_as_float((uint32_t)(e >> 32));
+            c.sel[ob + j] = e;
+        }
+        __syncthreads();
     }
-    // sort the selection and write it out
-    const uint32_t out = min(need, (uint32_t)P);
-    const int PS = P < 256 ? 256 : P;
-    for (int i = tid + (int)out; i < PS; i += blockDim.x) el[i] = ~0ull;
+    if (dummy) atomicOr(&st_s, dummy);
     __syncthreads();
-    sort_lds(el, PS);
-    const long long ob = iq * c.max_k;
-    for (uint32_t j = tid; j < out; j += blockDim.x) {
-        const unsigned long long e = el[j];
-        a.victims[ob + j] = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
-        if (a.scores) a.scores[ob + j] = __uint_as_float((uint32_t)(e >> 32));
-        c.sel[ob + j] = e;
+    // stage 2 searches the sorted lists: from LDS when they fit
+    const unsigned long long *lists = c.sel + (long long)inst * Q * c.max_k;
+    int stride = c.max_k;
+    int n1 = (c.ef_queue >= 0) ? min((int)kq, cnt[c.ef_queue]) : 0;
+    int maxc = 0;
+    for (int q = 0; q < Q; ++q) maxc = max(maxc, (int)cnt[q]);
+    if ((int)kq > n1 && (long long)Q * maxc * 8 <= lds_bytes) {
+        for (int i = tid; i < Q * maxc; i += blockDim.x) {
+            const int q = i / maxc, j = i - q * maxc;
+            if (j < cnt[q]) el[i] = lists[(long long)q * c.max_k + j];
+        }
+        __syncthreads();
+        lists = el;
+        stride = maxc;
     }
+    // stage 1 (the evict-first list) is already in the decision unless that list took the exact path
+    const bool copy1 = c.ef_queue >= 0 && fb_s[c.ef_queue];
+    const int d = merge_decision(lists, stride, cnt, Q, c.ef_queue, (int)kq, a.decision + (long long)inst * c.max_k,
+                                 copy1);
     if (tid == 0) {
-        a.count[iq] = (int32_t)out;
-        c.sel_count[iq] = (int32_t)out;
-        c.spill_n[iq] = 0;
-        set_status(c.status, dummy);
-    }
-}
-
-// Pool-scan engine, step 4: Algorithm 1 decision of each instance.
-__global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a)
-{
-    __shared__ int32_t cnt[SAE_MAX_QUEUES];
-    const int inst = blockIdx.x;
-    const int Q = c.Q;
-    if (threadIdx.x < Q) cnt[threadIdx.x] = c.sel_count[(long long)inst * Q + threadIdx.x];
-    __syncthreads();
-    int kk = inst_k(a, inst, c.max_k);
-    int d = merge_decision(c.sel + (long long)inst * Q * c.max_k, c.max_k, cnt, Q, c.ef_queue, kk,
-                           a.decision + (long long)inst * c.max_k);
-    if (threadIdx.x == 0) {
         a.decision_count[inst] = d;
         commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
+        set_status(c.status, st_s);
     }
 }
 
@@ -1145,11 +1705,24 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
     }
 }
 
-// Kernels whose dynamic LDS may exceed 64 KiB ask for it explicitly.
+// Kernels whose dynamic LDS may exceed 64 KiB ask for it explicitly, once per
+// kernel and size (the attribute call costs host time on every launch otherwise).
 hipError_t allow_lds(const void *fn, size_t bytes)
 {
     if (bytes <= 64 * 1024) return hipSuccess;
-    return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    static thread_local const void *done_fn[16];
+    static thread_local size_t done_bytes[16];
+    for (int i = 0; i < 16; ++i)
+        if (done_fn[i] == fn && done_bytes[i] >= bytes) return hipSuccess;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    for (int i = 0; i < 16; ++i)
+        if (done_fn[i] == nullptr || done_fn[i] == fn) {
+            done_fn[i] = fn;
+            done_bytes[i] = bytes;
+            break;
+        }
+    return hipSuccess;
 }
 
 int pow2_at_least(int x)
@@ -1173,13 +1746,16 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
 {
     hipError_t e;
     // step 1: sample
-    const size_t lds_sample = (size_t)c.Q * SAE_SBINS * sizeof(uint32_t);
-    hipLaunchKernelGGL(k_sample, dim3(SAMPLE_WGS, c.n_inst), dim3(SCAN_THREADS), lds_sample, s, c, a);
+    hipLaunchKernelGGL(k_sample, dim3(SAMPLE_WGS, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 2: candidate bounds
+    // step 2: candidate bounds and bucket upper ends
+    const size_t lds_g = (size_t)GROUP_CAP * sizeof(unsigned long long);
+    if ((e = allow_lds((const void *)k_split1, lds_g)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_split1, dim3(SAE_SPLIT_G, c.Q, c.n_inst), dim3(SEL_THREADS), lds_g, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     const size_t lds_el = (size_t)LCAP * sizeof(unsigned long long);
-    if ((e = allow_lds((const void *)k_threshold, lds_el)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_threshold, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
+    if ((e = allow_lds((const void *)k_split2, lds_el)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_split2, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // step 3: streaming pass
     if (ev0 && (e = hipEventRecord(ev0, s)) != hipSuccess) return e;
@@ -1187,10 +1763,14 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
     e = hipGetLastError();
     if (e == hipSuccess && ev1) e = hipEventRecord(ev1, s);
     if (e != hipSuccess) return e;
-    // step 4: per (queue, instance) exact select
-    const int P = pow2_at_least(c.max_k);
-    if ((e = allow_lds((const void *)k_select, lds_el)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_select, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a, P);
+    // step 4: group the candidates by bucket
+    const size_t lds_c = (size_t)(SAE_LCAP / SAE_GATHER_S + 1) * sizeof(unsigned long long);
+    if ((e = allow_lds((const void *)k_gather, lds_c)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_gather, dim3(SAE_GATHER_S, c.Q, c.n_inst), dim3(GATHER_THREADS), lds_c, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // step 5: sort the buckets
+    const size_t lds_b = (size_t)2 * SAE_BSORT * sizeof(unsigned long long);
+    hipLaunchKernelGGL(k_bucket, dim3(SAE_NBUCKET, c.Q, c.n_inst), dim3(BUCKET_THREADS), lds_b, s, c, a);
     return hipGetLastError();
 }
 
@@ -1211,7 +1791,15 @@ int scan_grid_x(int n_inst, int N)
 
 hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_merge, dim3(c.n_inst), dim3(SEL_THREADS), 0, s, c, a);
+    const int P = pow2_at_least(c.max_k);
+    // the exact path's sort (and histogram), or the sorted lists of stage 2 when they fit
+    size_t lds = (size_t)2 * (P < 256 ? 256 : P) * sizeof(unsigned long long);
+    if (lds < (size_t)SAE_BINS * sizeof(uint32_t)) lds = (size_t)SAE_BINS * sizeof(uint32_t);
+    const size_t lists = (size_t)c.Q * P * sizeof(unsigned long long);
+    if (lists > lds) lds = lists < (size_t)128 * 1024 ? lists : (size_t)128 * 1024;
+    hipError_t e = allow_lds((const void *)k_merge, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_merge, dim3(c.n_inst), dim3(SEL_THREADS), lds, s, c, a, P, (long long)lds);
     return hipGetLastError();
 }
 

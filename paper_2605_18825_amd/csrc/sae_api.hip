@@ -158,6 +158,7 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     c->ghost_slots = 1ll << gl;
     d.index_mask = (uint32_t)(c->index_slots - 1);
     d.ghost_mask = (uint32_t)(c->ghost_slots - 1);
+
     long long cc = 8ll * d.max_k;
     if (cc < 32768) cc = 32768;
     if (cc > d.N) cc = d.N;
@@ -169,10 +170,17 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     bool ok = dev_alloc(c, &d.state, I) && dev_alloc(c, &d.status, 1) &&
               dev_alloc(c, &d.index, I * c->index_slots) && dev_alloc(c, &d.ring, I * d.ring_cap) &&
               dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) &&
-              dev_alloc(c, &d.shist, I * SAE_HIST_STRIPES * Q * SAE_SBINS) &&
               dev_alloc(c, &d.nev_part, I * GX * Q) && dev_alloc(c, &d.creg, I * GX * Q * SAE_CAND_REGION) &&
               dev_alloc(c, &d.creg_n, I * GX * Q) && dev_alloc(c, &d.spill, I * Q * d.cand_cap) &&
-              dev_alloc(c, &d.spill_n, I * Q) && dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
+              dev_alloc(c, &d.spill_n, I * Q) && dev_alloc(c, &d.split, I * Q * SAE_NBUCKET) &&
+              dev_alloc(c, &d.nsplit, I * Q) && dev_alloc(c, &d.bsize, I * Q * SAE_NBUCKET) &&
+              dev_alloc(c, &d.bbelow, I * Q * SAE_NBUCKET) && dev_alloc(c, &d.cand, I * Q * SAE_LCAP) &&
+              dev_alloc(c, &d.g_base, I * Q * SAE_GATHER_S) && dev_alloc(c, &d.g_tot, I * Q * SAE_GATHER_S) &&
+              dev_alloc(c, &d.g_nev, I * Q * SAE_GATHER_S) &&
+              dev_alloc(c, &d.g_rel, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
+              dev_alloc(c, &d.g_cnt, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
+              dev_alloc(c, &d.kept, I * Q * SAE_SPLIT_G * SAE_SPLIT_RCAP) &&
+              dev_alloc(c, &d.kept_n, I * Q * SAE_SPLIT_G) && dev_alloc(c, &d.samp_tot, I * Q * SAE_SPLIT_G) && dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
               dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
               dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
               dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&

@@ -19,9 +19,15 @@
 // Sampling of the pool-scan engine: chunks per instance and blocks per chunk.
 #define SAE_SAMPLE_WGS 256
 #define SAE_SAMPLE_CHUNK 256
-#define SAE_HIST_STRIPES 32  // copies of the sampled histogram (fewer same-address atomics)
-#define SAE_SBINS 512        // sampled histogram bins: top 9 key bits (one bin per octave of P)
+#define SAE_SPLIT_G 8         // groups of sampling chunks, per (instance, queue), in the bound search
+#define SAE_SPLIT_RCAP 2048   // largest sample rank of the candidate bound
+#define SAE_GATHER_S 16       // slices of the scan workgroups, per (instance, queue), in the gather
 #define SAE_CAND_REGION 128  // candidate slots per (scan workgroup, queue)
+// Candidate buckets of the pool-scan engine, per (instance, queue): the bucket
+// upper ends are sampled (key, id) values at or below the candidate bound.
+#define SAE_NBUCKET 256  // buckets
+#define SAE_BSORT 2048   // largest bucket one workgroup sorts
+#define SAE_LCAP 16384   // candidates kept per (instance, queue)
 
 // Feedback counters are added into one of SAE_CSLOTS striped copies (chosen by
 // the adding workgroup) and folded into InstState by the learner kernel:
@@ -86,7 +92,7 @@ struct DevCtx {
     int32_t W;         // ghost window
     int32_t ring_cap;  // W + max_k
     uint32_t index_mask, ghost_mask;
-    int32_t cand_cap;  // candidate capacity per (instance, queue), scan engine
+    int32_t cand_cap;  // spilled candidates per (instance, queue), scan engine
     // pool (caller-owned)
     int32_t *la;
     uint16_t *meta;
@@ -103,15 +109,27 @@ struct DevCtx {
     GhostEntry *ring;     // [n_inst][ring_cap]
     GhostSlot *gtab;      // [n_inst][ghost_mask + 1]
     unsigned long long *thr;   // [n_inst][Q] candidate bound on (key << 32 | id), scan engine
-    uint32_t *shist;      // [n_inst][SAE_HIST_STRIPES][Q][SAE_SBINS] sampled key histogram
     unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
     uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
-    uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, in regions, spilled, slow path
+    unsigned long long *kept;  // [n_inst][Q][SAE_SPLIT_G][SAE_SPLIT_RCAP] smallest sampled elements per group
+    uint32_t *kept_n;          // [n_inst][Q][SAE_SPLIT_G] elements kept (~0u: rank beyond SAE_SPLIT_RCAP)
+    uint32_t *samp_tot;        // [n_inst][Q][SAE_SPLIT_G] sampled elements per group
+    uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, spilled, slow path
     uint32_t *nev_part;        // [n_inst][scan_gx][Q] evictable blocks per scan workgroup
     unsigned long long *creg;  // [n_inst][scan_gx][Q][SAE_CAND_REGION] candidates per scan workgroup
     uint32_t *creg_n;          // [n_inst][scan_gx][Q]
     unsigned long long *spill; // [n_inst][Q][cand_cap] candidates beyond a region
     uint32_t *spill_n;         // [n_inst][Q]
+    unsigned long long *split; // [n_inst][Q][SAE_NBUCKET] bucket upper ends, ascending; the last is thr
+    int32_t *nsplit;           // [n_inst][Q] buckets (0: no candidates; -1: exact path)
+    unsigned long long *cand;  // [n_inst][Q][SAE_LCAP] candidates, per slice grouped by bucket
+    uint32_t *g_base;          // [n_inst][Q][SAE_GATHER_S] where each slice starts in cand
+    uint32_t *g_tot;           // [n_inst][Q][SAE_GATHER_S] candidates per slice (all slices: > SAE_LCAP = too many)
+    uint32_t *g_nev;           // [n_inst][Q][SAE_GATHER_S] evictable blocks per slice
+    uint32_t *g_rel;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket start within its slice
+    uint32_t *g_cnt;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket size within its slice
+    uint32_t *bsize;           // [n_inst][Q][SAE_NBUCKET] candidates per bucket
+    uint32_t *bbelow;          // [n_inst][Q][SAE_NBUCKET] candidates below the bucket
     int32_t scan_gx;           // scan workgroups per instance
     int32_t *cpart;            // [n_inst][SAE_CSLOTS][SAE_CF_STRIDE] feedback counters, striped
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
