@@ -326,10 +326,22 @@ sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream
 sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
 
 /* Diagnostics of the last pool-scan selection of one instance: for each
- * queue q, out[4q..4q+3] = {evictable blocks, candidates under the bound,
- * candidates beyond a scan workgroup's region, 1 if the exact slow path ran}.  out is host memory of
- * 4 * n_queues words; synchronizes `stream`. */
+ * queue q, out[4q..4q+3] = {evictable blocks (0xFFFFFFFF when the selection
+ * did not need the count: the bound admitted only part of the queue and the
+ * exact slow path did not run), candidates under the bound, candidates beyond
+ * a scan workgroup's region, 1 if the exact slow path ran}.  out is host
+ * memory of 4 * n_queues words; synchronizes `stream`. */
 sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_stream_t stream);
+
+/* Device realisation of the fp32 recipe's elementary functions (the ones
+ * Eq. 1 and Eq. 2 are built from), element-wise, for checking it:
+ *  fn = SAE_FN_LN    y = ln x    (x a positive normal float)
+ *       SAE_FN_EXP   y = e^x
+ *       SAE_FN_ERFC  y = erfc x  (x >= 0)
+ *  x[n], y[n] device float.  Returns SAE_ERR_ARG for an unknown fn, n < 0 or
+ *  a NULL array with n > 0 (nothing launched). */
+enum { SAE_FN_LN = 0, SAE_FN_EXP = 1, SAE_FN_ERFC = 2 };
+sae_status sae_recipe_eval(int32_t fn, int64_t n, const float *x, float *y, sae_stream_t stream);
 
 /* Per-kernel timing of the pool-scan engine's scoring pass: when enabled,
  * HIP events bracket every launch of that kernel on the call's stream.

@@ -73,6 +73,7 @@ SIGNATURES = {
     "sae_get_counters": (_I32, [_P, _I32, ctypes.POINTER(SaeCounters), _P]),
     "sae_set_counters": (_I32, [_P, _I32, ctypes.POINTER(SaeCounters), _P]),
     "sae_block_type": (_I32, [_P, _I64, _P, _P]),
+    "sae_recipe_eval": (_I32, [_I32, _I64, _P, _P, _P]),
     "sae_classify_blocks": (_I32, [_P, _I32, _P, _P, ctypes.POINTER(_I32), _P]),
     "sae_index_build": (_I32, [_P, _P]),
     "sae_insert_blocks": (_I32, [_P, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),

@@ -154,6 +154,14 @@ def sae_block_type(counts_u8, tau_u8, stream=None):
     _check(None, _lib.load().sae_block_type(_ptr(counts_u8), n, _ptr(tau_u8), _stream(stream)))
 
 
+FN_LN, FN_EXP, FN_ERFC = 0, 1, 2
+
+
+def sae_recipe_eval(fn, x_f32, y_f32, stream=None):
+    """The device realisation of ln / exp / erfc of the fp32 recipe, element-wise."""
+    _check(None, _lib.load().sae_recipe_eval(int(fn), x_f32.numel(), _ptr(x_f32), _ptr(y_f32), _stream(stream)))
+
+
 def sae_classify_blocks(ctx, hint_u8, meta_u16, roles, stream=None):
     """Algorithm 1 Classify on the device: rewrites the queue bits of meta."""
     r = (ctypes.c_int32 * 4)(*[int(x) for x in roles])

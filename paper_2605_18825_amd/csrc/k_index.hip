@@ -481,7 +481,23 @@ __global__ void k_commit_b(DevCtx c, const int32_t *decision)
 
 inline unsigned grid_for(long long n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
+// The recipe's elementary functions, element-wise (sae_recipe_eval).
+__global__ void k_recipe_eval(int fn, long long n, const float *x, float *y)
+{
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
+        const float v = x[i];
+        y[i] = (fn == SAE_FN_LN) ? dsr::ln(v) : ((fn == SAE_FN_EXP) ? dsr::exp(v) : dsr::erfc(v));
+    }
+}
+
 }  // namespace
+
+hipError_t launch_recipe_eval(int fn, int64_t n, const float *x, float *y, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_recipe_eval, dim3(grid_for(n)), dim3(kThreads), 0, s, fn, (long long)n, x, y);
+    return hipGetLastError();
+}
 
 hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s)
 {

@@ -805,6 +805,76 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split1(DevCtx c, SelectArgs a)
     if (tid == 0) c.samp_tot[iqg] = ng;
 }
 
+// Filter entry of the pool scan for one (type, queue) (see k_scan):
+//  x  log-normal: blocks with dt < x lie above the bound (lognormal_dt_floor);
+//     0 for the other kinds
+//  y  structural / recency: bits of awl = fl(fl(alpha_q w_tau) (1 - 2^-6)) of
+//     the product test, 0 (no pruning) unless 2^-90 <= awl <= 2^100
+//  z  bits of the bound's key T for the product test: +inf (no pruning)
+//     unless T = 0 or 2^-100 <= T < +inf, and for a structural queue gamma = 1
+//  w  bit 0: not the evict-first queue; bit 1: recency (p = 1)
+// Outside those ranges a subnormal or overflowing product could break the
+// test's rounding argument, so nothing is pruned there.
+__device__ uint4 scan_entry(int kind, uint32_t dlo, float aw, uint32_t tk, float gamma)
+{
+    uint4 e = make_uint4(0u, 0u, 0u, 1u);
+    if (kind == SAE_KIND_LOGNORMAL) {
+        e.x = dlo;
+    } else if (kind == SAE_KIND_STRUCTURAL || kind == SAE_KIND_RECENCY) {
+        const float awl = aw * (1.0f - 0x1p-6f);
+        const float T = __uint_as_float(tk);
+        const bool aw_ok = awl >= 0x1p-90f && awl <= 0x1p100f;
+        const bool t_ok = tk < 0x7F800000u && (tk == 0u || T >= 0x1p-100f) &&
+                          (kind == SAE_KIND_RECENCY || gamma == 1.0f);
+        e.y = aw_ok ? __float_as_uint(awl) : 0u;
+        e.z = t_ok ? tk : 0x7F800000u;
+        e.w = (kind == SAE_KIND_RECENCY) ? 3u : 1u;
+    } else {
+        e.w = 0u;  // evict-first: the id limit decides
+    }
+    return e;
+}
+
+// Scan pruning of a log-normal queue q for blocks of type ty: the smallest
+// D in [0, 2^31] such that every block of (q, ty) with dt < D has a key above
+// the bound key tk (IEEE bits of T >= 0), so the scan need not score it.
+// D is the first dt at which key(dt) <= bits(T') holds, T' = max(T (1 + 2^-15),
+// 2^-100), found by a 64-way bisection with the scan's own key function.
+// Why this is safe: for a fixed (q, ty), while P (Eq. 3) stays a normal
+// number, this fp32 recipe never gives a larger dt a P more than a factor
+// 1 + 2^-19 above a smaller dt's -- ln rises monotonically over every float
+// >= 1, the erfc realisation rises by at most one ulp (2^-23 relative) over
+// any interval of [0, 9] (both checked exhaustively), and every other step
+// is a monotone rounding.  The predecessor D - 1 fails the predicate, so
+// P(D - 1) > T' >= 2^-100 (normal) and every dt <= D - 1 has
+// P > T' / (1 + 2^-19) > T.  Returns 0 (nothing pruned) when T is not finite
+// or a parameter is out of range.  Called by a whole wave; the result is
+// wave-uniform.
+__device__ uint32_t lognormal_dt_floor(const ScoreTab &t, int q, int ty, uint32_t tk)
+{
+    const float aw = t.aw[q][ty], mu = t.mu[q], cc = t.c[q];
+    const float inf = __uint_as_float(0x7F800000u);
+    if (tk >= 0x7F800000u || !(aw >= 0.0f && aw < inf) || !(fabsf(mu) < inf) || !(cc > 0.0f && cc < inf)) return 0;
+    const float tp = fmaxf(__uint_as_float(tk) * (1.0f + 0x1p-15f), 0x1p-100f);
+    const uint32_t tpb = __float_as_uint(tp);
+    if (tpb >= 0x7F800000u) return 0;
+    const uint32_t m = (uint32_t)q | ((uint32_t)ty << 3);
+    const uint32_t lane = (uint32_t)lane_id();
+    uint32_t lo = 0, hi = 0x80000000u;  // the predicate fails at lo (dt = 0 gives +inf) and holds at hi
+    uint32_t dummy = 0;
+    while (hi - lo > 1) {
+        const uint32_t p = lo + (uint32_t)(((unsigned long long)(hi - lo) * (lane + 1)) >> 6);  // lane 63: hi
+        const bool ok = (p >= hi) || key_lognormal((int32_t)p, 0, m, t, dummy) <= tpb;
+        const unsigned long long mk = __ballot(ok);
+        const int f = __ffsll((long long)mk) - 1;
+        const uint32_t nhi = __shfl(p, f, SAE_WAVE);
+        const uint32_t prev = __shfl(p, (f + SAE_WAVE - 1) & (SAE_WAVE - 1), SAE_WAVE);
+        lo = (f == 0) ? lo : prev;
+        hi = nhi;
+    }
+    return hi;
+}
+
 // Pool-scan engine, step 2b: per (instance, queue), the candidate bound and the
 // candidate buckets.  The bound is the r-th smallest sampled (key, id); a
 // queue that is estimated small takes every evictable block, and one the
@@ -820,11 +890,13 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
     __shared__ uint32_t kn_s[SAE_SPLIT_G], st_s[SAE_SPLIT_G], kpre[SAE_SPLIT_G + 1], tot_s, nsp_s;
     __shared__ int32_t bad_s, nb_s;
     __shared__ unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s, mx_s;
+    __shared__ ScoreTab tab;
     const int q = blockIdx.x;
     const int inst = blockIdx.y;
     const int Q = c.Q;
     const int tid = threadIdx.x;
     const long long iq = (long long)inst * Q + q;
+    load_score_tab(tab, c.state[inst], c);
     if (tid < SAE_SPLIT_G) kn_s[tid] = c.kept_n[iq * SAE_SPLIT_G + tid];
     if (tid >= SAE_SPLIT_G && tid < 2 * SAE_SPLIT_G) st_s[tid - SAE_SPLIT_G] = c.samp_tot[iq * SAE_SPLIT_G + tid - SAE_SPLIT_G];
     if (tid == SEL_THREADS - 1) {
@@ -923,71 +995,117 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
         c.thr[iq] = bound_s;
         c.nsplit[iq] = nb;
     }
+    // the scan's filter entries of this queue: one wave per token type
+    const int wave = tid / SAE_WAVE;
+    if (wave < 8) {
+        const uint32_t tk = (uint32_t)(bound_s >> 32);
+        uint32_t D = 0;
+        if (c.kind[q] == SAE_KIND_LOGNORMAL && wave < SAE_N_TYPES) D = lognormal_dt_floor(tab, q, wave, tk);
+        if (lane_id() == 0) c.sent[(long long)inst * 64 + wave * 8 + q] = scan_entry(c.kind[q], D, tab.aw[q][wave], tk, tab.gamma);
+        // queue indices >= Q select nothing
+        if (q == 0 && lane_id() < SAE_MAX_QUEUES && lane_id() >= Q)
+            c.sent[(long long)inst * 64 + wave * 8 + lane_id()] = make_uint4(0xFFFFFFFFu, 0u, 0u, 1u);
+    }
+    // the evict-first queue's id limit per num_tokens value: (num_tokens, id) <= bound
+    if ((q == c.ef_queue || (q == 0 && (c.ef_queue < 0 || c.ef_queue >= Q))) && tid < 16) {
+        int32_t lim = -1;
+        if (q == c.ef_queue) {
+            const uint32_t tk = (uint32_t)(bound_s >> 32), ti = (uint32_t)bound_s;
+            const uint32_t kb = __float_as_uint((float)(tid + 1));
+            lim = (kb < tk) ? 0x7FFFFFFF : ((kb == tk) ? (int32_t)(ti > 0x7FFFFFFFu ? 0x7FFFFFFFu : ti) : -1);
+        }
+        c.eflim[(long long)inst * 16 + tid] = lim;
+    }
 }
 
 // Pool-scan engine, step 3: one streaming pass over the whole pool.
-// Each wave takes batches of SCAN_BATCH consecutive blocks: every lane loads
-// 2 x 4 blocks with 16-, 8- and 16-byte loads (last_access, meta, off) into
-// the wave's LDS staging area, the wave sorts the evictable blocks into three
-// lists by queue kind (log-normal, structural, evict-first/recency) with
-// ballots, and then scores each list with all lanes busy on the same code.
-// Non-evictable blocks cost only their load and decode.  Per workgroup:
-// evictable blocks per queue go to a plain store, and blocks with
-// (key, id) <= bound to the workgroup's own candidate region (one LDS atomic
-// per wave and queue); only a region overflow uses the shared spill list.
+// Each wave takes batches of SCAN_BATCH consecutive blocks (4 per lane, read
+// with 16-, 8- and 16-byte loads of last_access, meta and off), with the
+// loads of the next two batches in flight while one is examined.  A cheap
+// exact filter drops almost every evictable block whose (key, id) lies above
+// its queue's bound without evaluating Eq. 1-3; its table (k_split2, one
+// 16-byte entry per (type, queue), see scan_entry) makes every test pass
+// trivially for the other kinds, so a block costs one table read and no
+// branch:
+//  * log-normal: dt below the (queue, type) threshold;
+//  * structural and recency: the product test (product_prunes);
+//  * evict-first: the key is num_tokens, so (key, id) <= bound is an id limit
+//    per num_tokens value.
+// The blocks that remain (about the bound's candidates) are queued per wave in
+// LDS with their features; a wave scores its queue exactly once 64 are queued,
+// and at the end the four waves score what is left together.  Blocks with
+// (key, id) <= bound go to the workgroup's own candidate region (one LDS
+// atomic per wave and queue); only a region overflow uses the shared spill
+// list.  Batches of a pool whose size is not a multiple of 4, and the last
+// partial batch, take a path with per-element loads.
 #define SCAN_BATCH 256  // blocks per wave per batch: 4 per lane
 #define SCAN_WAVES (SCAN_THREADS / SAE_WAVE)
+#define SCAN_LIST (SAE_WAVE + SCAN_BATCH)  // queued blocks per wave
+
+// Structural (pn / pd = 1 - o_b / o_max) and recency (pn = pd = 1) blocks:
+// true only if fl(pn awl) > fl(fl(T dt) pd), which implies P > T.  Proof
+// sketch, for 2^-90 <= awl <= 2^100 and T = 0 or 2^-100 <= T < +inf (the
+// entry disables the test otherwise): the recipe's p = fl(1 - fl(o_b / o_max))
+// is at least (pn / pd)(1 - 2^-8)(1 - 2^-24) because pd < 2^16; P =
+// fl(fl(aw p) / dt) is at least (pn / pd)(aw / dt)(1 - 2^-8)(1 - 2^-13)
+// (1 - 2^-23) even where it is subnormal (it is then above 2^-137); the test's
+// own roundings stay in the normal range, so with the factor 1 - 2^-6 in awl
+// it implies (pn / pd)(aw / dt) > T (1 + 2^-7), hence P > T.  dt = 0 gives a
+// right side of 0 (and P = +inf); T = +inf never prunes.
+__device__ __forceinline__ bool product_prunes(uint32_t pn, uint32_t pd, float awl, float tb, int32_t dt)
+{
+    const float lhs = (float)pn * awl;
+    const float rhs = (tb * (float)dt) * (float)pd;
+    return lhs > rhs;
+}
 
 // Four consecutive blocks of one lane, as loaded from HBM.
 struct Quad {
     int4 la;
     uint4 off;
-    uint32_t m01, m23;
+    uint2 m;
 };
 
-__device__ __forceinline__ Quad load_quad(const DevCtx &c, long long base, long long e0, long long N, bool vec)
+__device__ __forceinline__ Quad load_quad_vec(const DevCtx &c, long long e0)
 {
     Quad r;
-    r.la = make_int4(0, 0, 0, 0);
-    r.off = make_uint4(0, 0, 0, 0);
-    r.m01 = r.m23 = 0;
-    if (vec && e0 + 3 < N) {
-        r.la = *reinterpret_cast<const int4 *>(c.la + base + e0);
-        const uint2 m4 = *reinterpret_cast<const uint2 *>(c.meta + base + e0);
-        r.off = *reinterpret_cast<const uint4 *>(c.off + base + e0);
-        r.m01 = m4.x;
-        r.m23 = m4.y;
-    } else {
-        uint32_t m[4] = {0, 0, 0, 0};
-        int32_t l[4] = {0, 0, 0, 0};
-        uint32_t o[4] = {0, 0, 0, 0};
+    r.la = *reinterpret_cast<const int4 *>(c.la + e0);
+    r.m = *reinterpret_cast<const uint2 *>(c.meta + e0);
+    r.off = *reinterpret_cast<const uint4 *>(c.off + e0);
+    return r;
+}
+
+// Elements e0 .. e0 + 3 of the instance starting at `base`, those below N.
+__device__ __forceinline__ Quad load_quad_safe(const DevCtx &c, long long base, long long e0, long long N)
+{
+    uint32_t m[4] = {0, 0, 0, 0};
+    int32_t l[4] = {0, 0, 0, 0};
+    uint32_t o[4] = {0, 0, 0, 0};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (e0 + j < N) {
-                l[j] = c.la[base + e0 + j];
-                m[j] = c.meta[base + e0 + j];
-                o[j] = c.off[base + e0 + j];
-            }
+    for (int j = 0; j < 4; ++j) {
+        if (e0 + j < N) {
+            l[j] = c.la[base + e0 + j];
+            m[j] = c.meta[base + e0 + j];
+            o[j] = c.off[base + e0 + j];
         }
-        r.la = make_int4(l[0], l[1], l[2], l[3]);
-        r.off = make_uint4(o[0], o[1], o[2], o[3]);
-        r.m01 = m[0] | (m[1] << 16);
-        r.m23 = m[2] | (m[3] << 16);
     }
+    Quad r;
+    r.la = make_int4(l[0], l[1], l[2], l[3]);
+    r.off = make_uint4(o[0], o[1], o[2], o[3]);
+    r.m = make_uint2(m[0] | (m[1] << 16), m[2] | (m[3] << 16));
     return r;
 }
 
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
 {
     __shared__ ScoreTab tab;
+    __shared__ uint4 ent[64];
+    __shared__ int32_t ef_lim[16];
     __shared__ unsigned long long thr_s[SAE_MAX_QUEUES];
-    __shared__ uint32_t nev_s[SAE_MAX_QUEUES];
     __shared__ uint32_t cnt_s[SAE_MAX_QUEUES];
     __shared__ uint32_t st_s;
-    __shared__ int32_t s_la[SCAN_WAVES][SCAN_BATCH];
-    __shared__ uint32_t s_off[SCAN_WAVES][SCAN_BATCH];
-    __shared__ uint16_t s_meta[SCAN_WAVES][SCAN_BATCH];
-    __shared__ uint16_t s_list[SCAN_WAVES][3][SCAN_BATCH];
+    __shared__ uint32_t left_s[SCAN_WAVES + 1];
+    __shared__ int4 s_lst[SCAN_WAVES][SCAN_LIST];  // queued blocks: last_access, off, meta, id
     const int inst = blockIdx.y;
     const int wg = blockIdx.x;
     const int Q = c.Q;
@@ -995,37 +1113,43 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
     const long long base = (long long)inst * N;
     const int lane = lane_id();
     const int wave = threadIdx.x / SAE_WAVE;
-    load_score_tab(tab, c.state[inst], c);
-    if (threadIdx.x < SAE_MAX_QUEUES) {
-        thr_s[threadIdx.x] = (threadIdx.x < Q) ? c.thr[(long long)inst * Q + threadIdx.x] : 0ull;
-        nev_s[threadIdx.x] = 0;
-        cnt_s[threadIdx.x] = 0;
-    }
-    if (threadIdx.x == 0) st_s = 0;
-    __syncthreads();
-
-    // queue kind of every queue, 2 bits each
-    uint32_t kinds = 0;
-    for (int q = 0; q < SAE_MAX_QUEUES; ++q) kinds |= ((uint32_t)tab.kind[q] & 3u) << (2 * q);
-
-    const int now = a.now;
-    unsigned long long cnt_lo = 0, cnt_hi = 0;  // 16-bit evictable counters, queues 0-3 / 4-7
-    uint32_t st = 0;
-    const bool vec = ((N & 3) == 0);
+    const int tid = threadIdx.x;
     const long long nb = (N + SCAN_BATCH - 1) / SCAN_BATCH;
+    const long long nfull = ((N & 3) == 0) ? N / SCAN_BATCH : 0;  // batches read with vector loads
     const long long gw = (long long)wg * SCAN_WAVES + wave;
     const long long tw = (long long)gridDim.x * SCAN_WAVES;
+    // the first two batches' loads go out before the tables are read
+    auto ld = [&](long long bi) {
+        const long long b = bi < nfull ? bi : nfull - 1;
+        return load_quad_vec(c, base + b * SCAN_BATCH + lane * 4);
+    };
+    Quad qa = {}, qb = {}, qc = {};
+    if (nfull > 0) {
+        qa = ld(gw);
+        qb = ld(gw + tw);
+    }
+    load_score_tab(tab, c.state[inst], c);
+    if (tid < 64) ent[tid] = c.sent[(long long)inst * 64 + tid];
+    if (tid >= 64 && tid < 80) ef_lim[tid - 64] = c.eflim[(long long)inst * 16 + tid - 64];
+    if (tid >= 128 && tid < 128 + SAE_MAX_QUEUES) {
+        const int q = tid - 128;
+        thr_s[q] = (q < Q) ? c.thr[(long long)inst * Q + q] : 0ull;
+        cnt_s[q] = 0;
+    }
+    if (tid == 0) st_s = 0;
+    __syncthreads();
+
+    const int now = a.now;
+    uint32_t st = 0;
     const long long rbase = ((long long)inst * c.scan_gx + wg) * Q;
     unsigned long long *reg = c.creg + rbase * SAE_CAND_REGION;
     unsigned long long *spill = c.spill + (long long)inst * Q * c.cand_cap;
     uint32_t *spill_n = c.spill_n + (long long)inst * Q;
-    int32_t *wla = s_la[wave];
-    uint32_t *woff = s_off[wave];
-    uint16_t *wmeta = s_meta[wave];
+    int4 *lst = s_lst[wave];
 
     // append (key, id) of an evictable block if it is within its queue's bound
-    auto emit = [&](bool act, int q, uint32_t key, long long b) {
-        const unsigned long long comp = ((unsigned long long)key << 32) | (uint32_t)b;
+    auto emit = [&](bool act, int q, uint32_t key, uint32_t b) {
+        const unsigned long long comp = ((unsigned long long)key << 32) | b;
         const bool e = act && (comp <= thr_s[q]);
         unsigned long long em = __ballot(e);
         while (em) {
@@ -1053,85 +1177,93 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
             em &= ~mq;
         }
     };
+    // score one queued block per active lane, then emit it
+    auto score = [&](bool act, const int4 v) {
+        const uint32_t m = act ? (uint32_t)v.z : 0u;
+        const uint32_t key = block_key(now, act ? v.x : now, m, act ? (uint32_t)v.y : 0u, tab, st);
+        emit(act, meta_queue(m), key, (uint32_t)v.w);
+    };
 
-    // software pipeline: the next batch's loads are in flight while this one is scored
-    Quad nxt = {};
-    if (gw < nb) nxt = load_quad(c, base, gw * SCAN_BATCH + lane * 4, N, vec);
-    for (long long bi = gw; bi < nb; bi += tw) {  // wave-uniform
-        const long long b0 = bi * SCAN_BATCH;
-        const Quad cur = nxt;
-        *reinterpret_cast<int4 *>(wla + lane * 4) = cur.la;
-        *reinterpret_cast<uint4 *>(woff + lane * 4) = cur.off;
-        *reinterpret_cast<uint2 *>(wmeta + lane * 4) = make_uint2(cur.m01, cur.m23);
-        if (bi + tw < nb) nxt = load_quad(c, base, (bi + tw) * SCAN_BATCH + lane * 4, N, vec);
-        // kind lists (block indices within the batch)
-        uint32_t n0 = 0, n1 = 0, n2 = 0;
-        const uint32_t mreg[4] = {cur.m01 & 0xFFFFu, cur.m01 >> 16, cur.m23 & 0xFFFFu, cur.m23 >> 16};
-        const unsigned long long lt = lanemask_lt();
+    const unsigned long long lt = lanemask_lt();
+    uint32_t nl = 0;  // queued blocks of this wave (wave-uniform)
+    auto process = [&](const Quad &cur, long long bi) {
+        const int32_t lav[4] = {cur.la.x, cur.la.y, cur.la.z, cur.la.w};
+        const uint32_t offv[4] = {cur.off.x, cur.off.y, cur.off.z, cur.off.w};
+        const uint32_t mv[4] = {cur.m.x & 0xFFFFu, cur.m.x >> 16, cur.m.y & 0xFFFFu, cur.m.y >> 16};
+        const uint32_t b0 = (uint32_t)(bi * SCAN_BATCH) + (uint32_t)lane * 4u;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint32_t m = mreg[j];
-            const int idx = lane * 4 + j;
-            const int q = meta_queue(m);
-            const bool ev = meta_evictable(m) && q < Q;
-            const int kind = (int)((kinds >> (2 * q)) & 3u);
-            const int cls = !ev ? 3 : (kind == SAE_KIND_LOGNORMAL ? 0 : (kind == SAE_KIND_STRUCTURAL ? 1 : 2));
-            if (ev) {
-                const unsigned long long inc = 1ull << (16 * (q & 3));
-                if (q < 4) cnt_lo += inc;
-                else cnt_hi += inc;
-            }
-            const unsigned long long b0m = __ballot(cls == 0);
-            const unsigned long long b1m = __ballot(cls == 1);
-            const unsigned long long b2m = __ballot(cls == 2);
-            if (cls == 0) s_list[wave][0][n0 + __popcll(b0m & lt)] = (uint16_t)idx;
-            if (cls == 1) s_list[wave][1][n1 + __popcll(b1m & lt)] = (uint16_t)idx;
-            if (cls == 2) s_list[wave][2][n2 + __popcll(b2m & lt)] = (uint16_t)idx;
-            n0 += (uint32_t)__popcll(b0m);
-            n1 += (uint32_t)__popcll(b1m);
-            n2 += (uint32_t)__popcll(b2m);
+            const uint32_t m = mv[j];
+            const uint4 e = ent[m & 63u];
+            const bool ev = (m & (SAE_META_VALID | SAE_META_LEAF | SAE_META_REF)) == (SAE_META_VALID | SAE_META_LEAF);
+            const int32_t dtr = now - lav[j];
+            st |= (ev & (dtr < 0)) ? (uint32_t)SAE_ST_FUTURE_ACCESS : 0u;
+            const int32_t dt = dtr < 0 ? 0 : dtr;
+            const uint32_t ob = offv[j] & 0xFFFFu, om = offv[j] >> 16;
+            const bool one = ((e.w & 2u) != 0u) | (om == 0u);
+            const uint32_t pn = one ? 1u : (om > ob ? om - ob : 0u);
+            const uint32_t pd = one ? 1u : om;
+            // every test evaluated (no short-circuit branches)
+            const int32_t lim = ef_lim[(m >> SAE_META_NTOK_SHIFT) & 15u];
+            const bool k_ef = ((e.w & 1u) != 0u) | ((int32_t)(b0 + j) <= lim);
+            const bool k_pr = !product_prunes(pn, pd, __uint_as_float(e.y), __uint_as_float(e.z), dt);
+            const bool keep = ev & ((uint32_t)dt >= e.x) & k_pr & k_ef;
+            const unsigned long long km = __ballot(keep);
+            if (keep) lst[nl + (uint32_t)__popcll(km & lt)] = make_int4(lav[j], (int32_t)offv[j], (int32_t)m, (int32_t)(b0 + j));
+            nl += (uint32_t)__popcll(km);
         }
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        // log-normal queues
-        for (uint32_t i0 = 0; i0 < n0; i0 += SAE_WAVE) {
-            const bool act = i0 + lane < n0;
-            const int idx = act ? s_list[wave][0][i0 + lane] : 0;
-            const uint32_t m = wmeta[idx];
-            const uint32_t key = key_lognormal(now, wla[idx], m, tab, st);
-            emit(act, meta_queue(m), key, b0 + idx);
+        if (nl >= SAE_WAVE) {  // wave-uniform, rare
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            do {
+                nl -= SAE_WAVE;
+                score(true, lst[nl + lane]);
+            } while (nl >= SAE_WAVE);
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            __builtin_amdgcn_wave_barrier();
         }
-        // structural queues
-        for (uint32_t i0 = 0; i0 < n1; i0 += SAE_WAVE) {
-            const bool act = i0 + lane < n1;
-            const int idx = act ? s_list[wave][1][i0 + lane] : 0;
-            const uint32_t m = wmeta[idx];
-            const uint32_t key = key_structural(now, wla[idx], m, woff[idx], tab, st);
-            emit(act, meta_queue(m), key, b0 + idx);
-        }
-        // evict-first and recency queues
-        for (uint32_t i0 = 0; i0 < n2; i0 += SAE_WAVE) {
-            const bool act = i0 + lane < n2;
-            const int idx = act ? s_list[wave][2][i0 + lane] : 0;
-            const uint32_t m = wmeta[idx];
-            const int kind = (int)((kinds >> (2 * meta_queue(m))) & 3u);
-            const uint32_t key = key_cheap(kind, now, wla[idx], m, tab, st);
-            emit(act, meta_queue(m), key, b0 + idx);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        __builtin_amdgcn_wave_barrier();
+    };
+
+    // full batches: unconditional vector loads, two batches ahead
+    for (long long bi = gw; bi < nfull; bi += 3 * tw) {  // wave-uniform
+        qc = ld(bi + 2 * tw);
+        process(qa, bi);
+        if (bi + tw >= nfull) break;
+        qa = ld(bi + 3 * tw);
+        process(qb, bi + tw);
+        if (bi + 2 * tw >= nfull) break;
+        qb = ld(bi + 4 * tw);
+        process(qc, bi + 2 * tw);
     }
-    for (int q = 0; q < Q; ++q) {
-        const uint32_t v = (uint32_t)(((q < 4 ? cnt_lo : cnt_hi) >> (16 * (q & 3))) & 0xFFFFull);
-        if (v) atomicAdd(&nev_s[q], v);
+    // the rest: per-element loads
+    for (long long bi = nfull + gw; bi < nb; bi += tw)
+        process(load_quad_safe(c, base, bi * SCAN_BATCH + lane * 4, N), bi);
+
+    // what the waves left queued, scored by the four waves together
+    if (lane == 0) left_s[wave] = nl;
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t o = 0;
+        for (int w = 0; w < SCAN_WAVES; ++w) {
+            const uint32_t v = left_s[w];
+            left_s[w] = o;
+            o += v;
+        }
+        left_s[SCAN_WAVES] = o;
+    }
+    __syncthreads();
+    const uint32_t total = left_s[SCAN_WAVES];
+    for (uint32_t i0 = (uint32_t)wave * SAE_WAVE; i0 < total; i0 += SCAN_THREADS) {  // wave-uniform
+        const uint32_t i = i0 + (uint32_t)lane;
+        int w = 0;
+        while (w + 1 < SCAN_WAVES && left_s[w + 1] <= i) ++w;
+        const bool act = i < total;
+        score(act, act ? s_lst[w][i - left_s[w]] : make_int4(0, 0, 0, 0));
     }
     if (st) atomicOr(&st_s, st);
     __syncthreads();
-    if (threadIdx.x < Q) {
-        c.nev_part[rbase + threadIdx.x] = nev_s[threadIdx.x];
-        c.creg_n[rbase + threadIdx.x] = min(cnt_s[threadIdx.x], (uint32_t)SAE_CAND_REGION);
-    }
-    if (threadIdx.x == 0) set_status(c.status, st_s);
+    if (tid < Q) c.creg_n[rbase + tid] = min(cnt_s[tid], (uint32_t)SAE_CAND_REGION);
+    if (tid == 0) set_status(c.status, st_s);
 }
 
 // Sum over a wave of n words p[0], p[stride], ... (n <= 32 * SAE_WAVE): every
@@ -1166,7 +1298,6 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
     __shared__ unsigned long long spl[SAE_NBUCKET];
     __shared__ uint32_t offs[2048 + 1];
     __shared__ uint32_t hist[SAE_NBUCKET], boff[SAE_NBUCKET], wsum[GATHER_THREADS / SAE_WAVE];
-    __shared__ uint32_t nev_s;
     const int s = blockIdx.x;
     const int q = blockIdx.y;
     const int inst = blockIdx.z;
@@ -1176,9 +1307,7 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
     const int lane = lane_id();
     const long long iq = (long long)inst * Q + q;
     const long long iqs = iq * SAE_GATHER_S + s;
-    const int w0 = (s * gx) / SAE_GATHER_S, w1 = ((s + 1) * gx) / SAE_GATHER_S;  // evictable-count share
-    // one round of loads: every workgroup's candidate count, this share's evictable
-    // counts, the bucket upper ends
+    // one round of loads: every workgroup's candidate count, the bucket upper ends
     const int NB = c.nsplit[iq];
     const uint32_t ns = c.spill_n[iq];
     uint32_t cv[GATHER_RPT];
@@ -1187,9 +1316,7 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
         const int w = tid * GATHER_RPT + u;
         cv[u] = (w < gx) ? c.creg_n[((long long)inst * gx + w) * Q + q] : 0u;
     }
-    const uint32_t nv = (w0 + tid < w1) ? c.nev_part[((long long)inst * gx + w0 + tid) * Q + q] : 0u;
     const unsigned long long sv = c.split[iq * SAE_NBUCKET + tid];
-    if (tid == 0) nev_s = 0;
     hist[tid] = 0;
     spl[tid] = (tid < NB) ? sv : ~0ull;
     uint32_t loc = 0;
@@ -1197,10 +1324,7 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
     for (int u = 0; u < GATHER_RPT; ++u) loc += cv[u];
     const uint32_t inc = wave_incl_scan(loc);
     if (lane == 63) wsum[tid >> 6] = inc;
-    uint32_t nvs = nv;
-    for (int d = 32; d > 0; d >>= 1) nvs += __shfl_xor(nvs, d, SAE_WAVE);
     __syncthreads();
-    if (lane == 0 && nvs) atomicAdd(&nev_s, nvs);
     {
         uint32_t o = inc - loc;
         for (int w = 0; w < (tid >> 6); ++w) o += wsum[w];
@@ -1220,7 +1344,6 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
     const uint32_t hi = (uint32_t)(((unsigned long long)(s + 1) * C) / SAE_GATHER_S);
     const uint32_t n = hi - lo;
     if (tid == 0) {
-        c.g_nev[iqs] = nev_s;
         c.g_base[iqs] = lo;
         c.g_tot[iqs] = (NB <= 0) ? 0u : (C > SAE_LCAP ? (uint32_t)SAE_LCAP + 1u : n);
     }
@@ -1280,7 +1403,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
 {
     extern __shared__ unsigned long long bel[];  // [2 * SAE_BSORT]
     __shared__ uint32_t base_v[SAE_GATHER_S], rel_v[SAE_GATHER_S], pre_v[SAE_GATHER_S + 1];
-    __shared__ uint32_t C_s, nev_s, off_s;
+    __shared__ uint32_t C_s, off_s;
     const int j = blockIdx.x;
     const int q = blockIdx.y;
     const int inst = blockIdx.z;
@@ -1290,11 +1413,11 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
     // one round of loads; the first wave sums the slices
     const int NB = c.nsplit[iq];
     const uint32_t ns = c.spill_n[iq];
+    const bool all = c.thr[iq] == ~0ull;
     if (tid < SAE_WAVE) {
         const bool in = tid < SAE_GATHER_S;
         const long long iqs = iq * SAE_GATHER_S + tid;
         uint32_t tv = in ? c.g_tot[iqs] : 0u;
-        uint32_t nv = in ? c.g_nev[iqs] : 0u;
         const uint32_t bv = in ? c.g_base[iqs] : 0u;
         uint32_t rv = in ? c.g_rel[iqs * SAE_NBUCKET + j] : 0u;
         const uint32_t cv = in ? c.g_cnt[iqs * SAE_NBUCKET + j] : 0u;
@@ -1307,12 +1430,10 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
         if (tid == SAE_GATHER_S - 1) pre_v[SAE_GATHER_S] = inc;
         for (int d = 32; d > 0; d >>= 1) {
             tv += __shfl_xor(tv, d, SAE_WAVE);
-            nv += __shfl_xor(nv, d, SAE_WAVE);
             rv += __shfl_xor(rv, d, SAE_WAVE);
         }
         if (tid == 0) {
             C_s = tv;
-            nev_s = nv;
             off_s = rv;
         }
     }
@@ -1324,7 +1445,8 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
         c.bbelow[iq * SAE_NBUCKET + j] = off;
     }
     const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
-    const uint32_t need = nev_s < kq ? nev_s : kq;
+    // a bound that admits every block makes the candidates the evictable blocks
+    const uint32_t need = (all && C < kq) ? C : kq;
     if ((a.flags & SAE_SS_FORCE_FALLBACK) || C > SAE_LCAP || ns > (uint32_t)c.cand_cap || C < need) return;
     if (off >= need || n == 0 || n > SAE_BSORT) return;
     const unsigned long long *cand = c.cand + iq * SAE_LCAP;
@@ -1458,27 +1580,27 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
     const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
     load_score_tab(tab, c.state[inst], c);
     if (tid == 0) st_s = 0;
-    // one wave per queue: candidates, evictable blocks, whether the buckets suffice
+    // one wave per queue: candidates, list size, whether the buckets suffice
     if (wave < Q) {
         const int q = wave;
         const long long iq = (long long)inst * Q + q;
         // every load of this wave in one round
         const int NB = c.nsplit[iq];
         const uint32_t ns = c.spill_n[iq];
+        const bool all = c.thr[iq] == ~0ull;
         const uint32_t gt = (lane < SAE_GATHER_S) ? c.g_tot[iq * SAE_GATHER_S + lane] : 0u;
-        const uint32_t gn = (lane < SAE_GATHER_S) ? c.g_nev[iq * SAE_GATHER_S + lane] : 0u;
         uint32_t bb[SAE_NBUCKET / SAE_WAVE], bz[SAE_NBUCKET / SAE_WAVE];
 #pragma unroll
         for (int u = 0; u < SAE_NBUCKET / SAE_WAVE; ++u) {
             bb[u] = c.bbelow[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
             bz[u] = c.bsize[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
         }
-        uint32_t C = gt, nev = gn;
-        for (int d = 32; d > 0; d >>= 1) {
-            C += __shfl_xor(C, d, SAE_WAVE);
-            nev += __shfl_xor(nev, d, SAE_WAVE);
-        }
-        const uint32_t need = nev < kq ? nev : kq;
+        uint32_t C = gt;
+        for (int d = 32; d > 0; d >>= 1) C += __shfl_xor(C, d, SAE_WAVE);
+        // a bound that admits every block makes the candidates the evictable
+        // blocks; otherwise fewer than k candidates send the queue to the exact path
+        const uint32_t need = (all && C < kq) ? C : kq;
+        const uint32_t nev = all ? C : 0xFFFFFFFFu;
         // a bucket that holds some of the first `need` positions but is too big to sort
         bool big = false;
 #pragma unroll
@@ -1511,7 +1633,33 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
             set_status(c.status, SAE_ST_SELECT_FALLBACK);
             lcount = 0;
         }
+        // the exact path counts the queue's evictable blocks itself
+        __syncthreads();
+        {
+            uint32_t n = 0;
+            for (long long b = tid; b < N; b += blockDim.x) {
+                const uint32_t m = c.meta[base + b];
+                n += (meta_evictable(m) && meta_queue(m) == q) ? 1u : 0u;
+            }
+            for (int d = 32; d > 0; d >>= 1) n += __shfl_xor(n, d, SAE_WAVE);
+            if (lane == 0 && n) atomicAdd(&lcount, n);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            const uint32_t nev = lcount;
+            const uint32_t nd = nev < kq ? nev : kq;
+            const long long iq = (long long)inst * Q + q;
+            nev_s[q] = nev;
+            need_s[q] = nd;
+            cnt[q] = (int32_t)nd;
+            a.count[iq] = (int32_t)nd;
+            c.sel_count[iq] = (int32_t)nd;
+            c.sel_stats[iq * 4] = nev;
+            lcount = 0;
+        }
+        __syncthreads();
         const uint32_t need = need_s[q];
+        if (need == 0) continue;  // uniform
         auto for_each = [&](auto &&fn) {
             for (long long b = tid; b < N; b += blockDim.x) {
                 const uint32_t m = c.meta[base + b];

@@ -169,14 +169,13 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     const long long GX = d.scan_gx;
     bool ok = dev_alloc(c, &d.state, I) && dev_alloc(c, &d.status, 1) &&
               dev_alloc(c, &d.index, I * c->index_slots) && dev_alloc(c, &d.ring, I * d.ring_cap) &&
-              dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) &&
-              dev_alloc(c, &d.nev_part, I * GX * Q) && dev_alloc(c, &d.creg, I * GX * Q * SAE_CAND_REGION) &&
+              dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) && dev_alloc(c, &d.sent, I * 64) && dev_alloc(c, &d.eflim, I * 16) &&
+              dev_alloc(c, &d.creg, I * GX * Q * SAE_CAND_REGION) &&
               dev_alloc(c, &d.creg_n, I * GX * Q) && dev_alloc(c, &d.spill, I * Q * d.cand_cap) &&
               dev_alloc(c, &d.spill_n, I * Q) && dev_alloc(c, &d.split, I * Q * SAE_NBUCKET) &&
               dev_alloc(c, &d.nsplit, I * Q) && dev_alloc(c, &d.bsize, I * Q * SAE_NBUCKET) &&
               dev_alloc(c, &d.bbelow, I * Q * SAE_NBUCKET) && dev_alloc(c, &d.cand, I * Q * SAE_LCAP) &&
               dev_alloc(c, &d.g_base, I * Q * SAE_GATHER_S) && dev_alloc(c, &d.g_tot, I * Q * SAE_GATHER_S) &&
-              dev_alloc(c, &d.g_nev, I * Q * SAE_GATHER_S) &&
               dev_alloc(c, &d.g_rel, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
               dev_alloc(c, &d.g_cnt, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
               dev_alloc(c, &d.kept, I * Q * SAE_SPLIT_G * SAE_SPLIT_RCAP) &&
@@ -342,6 +341,15 @@ sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_st
     if (n < 0 || (n > 0 && (!counts || !tau))) return fail(nullptr, SAE_ERR_ARG, "counts/tau must be non-NULL, n >= 0");
     hipError_t e = launch_block_type(counts, n, tau, S(stream));
     if (e != hipSuccess) return hip_fail(nullptr, e, "sae_block_type");
+    return SAE_OK;
+}
+
+sae_status sae_recipe_eval(int32_t fn, int64_t n, const float *x, float *y, sae_stream_t stream)
+{
+    if (fn != SAE_FN_LN && fn != SAE_FN_EXP && fn != SAE_FN_ERFC) return fail(nullptr, SAE_ERR_ARG, "unknown recipe function");
+    if (n < 0 || (n > 0 && (!x || !y))) return fail(nullptr, SAE_ERR_ARG, "x/y must be non-NULL, n >= 0");
+    hipError_t e = launch_recipe_eval(fn, n, x, y, S(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "sae_recipe_eval");
     return SAE_OK;
 }
 

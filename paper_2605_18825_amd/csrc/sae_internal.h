@@ -109,13 +109,14 @@ struct DevCtx {
     GhostEntry *ring;     // [n_inst][ring_cap]
     GhostSlot *gtab;      // [n_inst][ghost_mask + 1]
     unsigned long long *thr;   // [n_inst][Q] candidate bound on (key << 32 | id), scan engine
+    uint4 *sent;               // [n_inst][64] scan filter entry of each (type, queue), index type << 3 | queue
+    int32_t *eflim;            // [n_inst][16] evict-first queue: largest candidate id per num_tokens - 1 (-1: none)
     unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
     uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
     unsigned long long *kept;  // [n_inst][Q][SAE_SPLIT_G][SAE_SPLIT_RCAP] smallest sampled elements per group
     uint32_t *kept_n;          // [n_inst][Q][SAE_SPLIT_G] elements kept (~0u: rank beyond SAE_SPLIT_RCAP)
     uint32_t *samp_tot;        // [n_inst][Q][SAE_SPLIT_G] sampled elements per group
     uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, spilled, slow path
-    uint32_t *nev_part;        // [n_inst][scan_gx][Q] evictable blocks per scan workgroup
     unsigned long long *creg;  // [n_inst][scan_gx][Q][SAE_CAND_REGION] candidates per scan workgroup
     uint32_t *creg_n;          // [n_inst][scan_gx][Q]
     unsigned long long *spill; // [n_inst][Q][cand_cap] candidates beyond a region
@@ -125,7 +126,6 @@ struct DevCtx {
     unsigned long long *cand;  // [n_inst][Q][SAE_LCAP] candidates, per slice grouped by bucket
     uint32_t *g_base;          // [n_inst][Q][SAE_GATHER_S] where each slice starts in cand
     uint32_t *g_tot;           // [n_inst][Q][SAE_GATHER_S] candidates per slice (all slices: > SAE_LCAP = too many)
-    uint32_t *g_nev;           // [n_inst][Q][SAE_GATHER_S] evictable blocks per slice
     uint32_t *g_rel;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket start within its slice
     uint32_t *g_cnt;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket size within its slice
     uint32_t *bsize;           // [n_inst][Q][SAE_NBUCKET] candidates per bucket
@@ -394,6 +394,7 @@ struct SelectArgs {
 };
 
 hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s);
+hipError_t launch_recipe_eval(int fn, int64_t n, const float *x, float *y, hipStream_t s);
 hipError_t launch_classify(int n, const uint8_t *hint, uint16_t *meta, const int32_t *roles, hipStream_t s);
 hipError_t launch_index_build(const DevCtx &c, hipStream_t s);
 hipError_t launch_insert(const DevCtx &c, int32_t n, const int32_t *inst, const int32_t *ids,

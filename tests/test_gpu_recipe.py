@@ -90,3 +90,71 @@ def test_division_and_subnormal_scores():
             pair.select(now, NB)
     finally:
         pair.close()
+
+
+def _dev_eval(fn, x):
+    xd = torch.as_tensor(x).cuda()
+    yd = torch.empty_like(xd)
+    api.sae_recipe_eval(fn, xd, yd)
+    torch.cuda.synchronize()
+    return yd.cpu().numpy()
+
+
+def test_elementary_functions_bit_identical():
+    """Device ln / exp / erfc against the oracle's transcription of the same
+    recipe, on dense grids of float bit patterns."""
+    from oracle import _native as dsr
+    rng = np.random.default_rng(11)
+    lo, hi = np.float32(1.0).view(np.uint32), np.float32(2.0 ** 31).view(np.uint32)
+    xs_ln = np.concatenate([np.arange(lo, lo + (1 << 20), dtype=np.uint32),
+                            rng.integers(np.float32(1e-30).view(np.uint32), hi, 1 << 21, dtype=np.uint32)]).view(np.float32)
+    xs_exp = np.concatenate([np.linspace(-90, 90, 1 << 20, dtype=np.float32),
+                             rng.uniform(-87, 88, 1 << 20).astype(np.float32)])
+    xs_erfc = np.concatenate([np.arange(0, 1 << 20, dtype=np.uint32).view(np.float32),
+                              rng.integers(0, np.float32(9.5).view(np.uint32), 1 << 21, dtype=np.uint32).view(np.float32)])
+    for fn, xs, ref in ((api.FN_LN, xs_ln, dsr.ln), (api.FN_EXP, xs_exp, dsr.exp), (api.FN_ERFC, xs_erfc, dsr.erfc)):
+        d = _dev_eval(fn, xs)
+        o = ref(xs)
+        bad = np.flatnonzero(d.view(np.uint32) != o.view(np.uint32))
+        assert bad.size == 0, (fn, xs[bad[:5]], d[bad[:5]], o[bad[:5]])
+    say("elementary functions: %d inputs bit-identical" % (xs_ln.size + xs_exp.size + xs_erfc.size))
+
+
+def test_monotonicity_exhaustive():
+    """What the scan's pruning of log-normal queues relies on, over EVERY float
+    input: ln is non-decreasing on [1, 2^31], and erfc never rises above its
+    value at a smaller argument by more than a relative 2^-20 on [0, 9]."""
+    chunk = 1 << 25
+    # ln, ascending
+    lo, hi = int(np.float32(1.0).view(np.uint32)), int(np.float32(2.0 ** 31).view(np.uint32))
+    prev = None
+    y = torch.empty(chunk, dtype=torch.float32, device="cuda")
+    for a in range(lo, hi + 1, chunk):
+        b = min(a + chunk, hi + 1)
+        x = torch.arange(a, b, dtype=torch.int64, device="cuda").to(torch.int32).view(torch.float32)
+        yy = y[:b - a]
+        api.sae_recipe_eval(api.FN_LN, x, yy)
+        assert bool((yy[1:] >= yy[:-1]).all()), "ln decreases inside [%d, %d)" % (a, b)
+        if prev is not None:
+            assert float(yy[0]) >= prev, "ln decreases at bits %d" % a
+        prev = float(yy[-1])
+    # erfc, descending, carrying the largest value at larger arguments
+    top = int(np.float32(9.0).view(np.uint32))
+    run = 0.0
+    worst = 1.0
+    b = top + 1
+    while b > 0:
+        a = max(0, b - chunk)
+        x = torch.arange(a, b, dtype=torch.int64, device="cuda").to(torch.int32).view(torch.float32)
+        yy = y[:b - a]
+        api.sae_recipe_eval(api.FN_ERFC, x, yy)
+        suf = torch.flip(torch.cummax(torch.flip(yy, [0]), 0).values, [0])
+        suf = torch.clamp(suf, min=run)
+        pos = yy > 0
+        r = float((suf[pos].double() / yy[pos].double()).max()) if bool(pos.any()) else 1.0
+        worst = max(worst, r)
+        run = max(run, float(yy.max()))
+        b = a
+    torch.cuda.synchronize()
+    say("monotonicity: ln non-decreasing on [1, 2^31]; erfc worst relative rise %.3e" % (worst - 1.0))
+    assert worst - 1.0 <= 2.0 ** -20
