@@ -344,7 +344,8 @@ enum { SAE_FN_LN = 0, SAE_FN_EXP = 1, SAE_FN_ERFC = 2 };
 sae_status sae_recipe_eval(int32_t fn, int64_t n, const float *x, float *y, sae_stream_t stream);
 
 /* Per-kernel timing of the pool-scan engine's scoring pass: when enabled,
- * HIP events bracket every launch of that kernel on the call's stream.
+ * every launch of that kernel carries a pair of HIP events that record the
+ * dispatch's own start and end on the call's stream.
  * sae_profile_read returns the summed milliseconds and launch count since the
  * last read (synchronizes) and resets them. */
 sae_status sae_profile_enable(sae_ctx *ctx, int32_t enable);

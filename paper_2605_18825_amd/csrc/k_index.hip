@@ -17,14 +17,32 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// Lookup by linear probing from the home slot.  The probe order is the plain
+// one (home, home + 1, ...), but slots are fetched a whole aligned group of
+// IDX_GROUP (one 128-byte line) at a time, with every load of the group in
+// flight together, so a lookup usually costs one memory round trip.  Tables
+// hold at least 64 slots, a multiple of IDX_GROUP.
+#define IDX_GROUP 8
 __device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h)
 {
+    const uint4 *t4 = reinterpret_cast<const uint4 *>(tab);
+    const int lim = (int)(mask + 1 < (uint32_t)SAE_MAX_PROBES ? mask + 1 : (uint32_t)SAE_MAX_PROBES);
     uint32_t s = hash_home(h, mask);
-    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        unsigned long long v = tab[s].hash;
-        if (v == h) return tab[s].id;
-        if (v == SAE_EMPTY_HASH) return -1;
-        s = (s + 1) & mask;
+    int seen = 0;
+    while (seen < lim) {
+        const uint32_t g = s & ~(uint32_t)(IDX_GROUP - 1);
+        uint4 v[IDX_GROUP];
+#pragma unroll
+        for (int t = 0; t < IDX_GROUP; ++t) v[t] = t4[g + t];
+#pragma unroll
+        for (int t = 0; t < IDX_GROUP; ++t) {
+            if ((uint32_t)t < s - g || seen >= lim) continue;
+            ++seen;
+            const unsigned long long vh = (unsigned long long)v[t].x | ((unsigned long long)v[t].y << 32);
+            if (vh == h) return (int32_t)v[t].z;
+            if (vh == SAE_EMPTY_HASH) return -1;
+        }
+        s = (g + IDX_GROUP) & mask;
     }
     return -1;
 }

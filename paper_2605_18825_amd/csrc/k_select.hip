@@ -14,6 +14,8 @@
 //  * batched (pools of <= 65,536 blocks): one workgroup of 1024 threads per
 //    instance keeps every key in registers and does scoring, the radix select
 //    of all queues, the sort and the merge in one launch.
+#include <hip/hip_ext.h>
+
 #include "sae_internal.h"
 
 #define SCAN_THREADS 256
@@ -1905,12 +1907,12 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
     if ((e = allow_lds((const void *)k_split2, lds_el)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_split2, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 3: streaming pass
-    if (ev0 && (e = hipEventRecord(ev0, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_scan, dim3(c.scan_gx, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
-    e = hipGetLastError();
-    if (e == hipSuccess && ev1) e = hipEventRecord(ev1, s);
-    if (e != hipSuccess) return e;
+    // step 3: streaming pass (with profiling, the events carry the dispatch's own start and end)
+    if (ev0 && ev1)
+        hipExtLaunchKernelGGL(k_scan, dim3(c.scan_gx, c.n_inst), dim3(SCAN_THREADS), 0, s, ev0, ev1, 0, c, a);
+    else
+        hipLaunchKernelGGL(k_scan, dim3(c.scan_gx, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     // step 4: group the candidates by bucket
     const size_t lds_c = (size_t)(SAE_LCAP / SAE_GATHER_S + 1) * sizeof(unsigned long long);
     if ((e = allow_lds((const void *)k_gather, lds_c)) != hipSuccess) return e;
