@@ -28,6 +28,15 @@ namespace {
 
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
+// Workgroup barrier that orders LDS accesses only: global loads and stores
+// still in flight stay in flight (__syncthreads waits for them too).
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ unsigned long long lanemask_lt()
 {
     int l = lane_id();
@@ -73,7 +82,7 @@ __device__ void find_crossing(const uint32_t *hist, int nq, const uint32_t *rem,
     uint32_t incl = wave_incl_scan(s);
     const int w = tid >> 6;
     if (lane_id() == 63) seg_tot[w] = incl;
-    __syncthreads();
+    lds_barrier();
     if ((w & 1) == 1) incl += seg_tot[w - 1];
     uint32_t excl = incl - s;
     if (q < nq && active[q]) {
@@ -93,7 +102,7 @@ __device__ void find_crossing(const uint32_t *hist, int nq, const uint32_t *rem,
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Per-queue radix-select state (LDS).
@@ -140,13 +149,13 @@ __device__ void sel_init(SelState &st, int nq, const uint32_t *need, const uint3
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     if (tid == 0) {
         int a = 0;
         for (int q = 0; q < nq; ++q) a |= st.active[q];
         st.any_active = a;
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // One refinement step after the histogram of digit (shift, width) was built.
@@ -166,13 +175,13 @@ __device__ void sel_step(SelState &st, int nq, int shift, int width, bool last)
             st.rem[tid] -= c.below;
         }
     }
-    __syncthreads();
+    lds_barrier();
     if (tid == 0) {
         int a = 0;
         for (int q = 0; q < nq; ++q) a |= st.active[q];
         st.any_active = a;
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Bitonic sort, ascending, of nseg independent segments of length P (a power
@@ -198,7 +207,7 @@ __device__ void bitonic_sort_segments(unsigned long long *a, int nseg, int P)
                     sg[hi] = x;
                 }
             }
-            __syncthreads();
+            lds_barrier();
         }
     }
 }
@@ -265,7 +274,7 @@ __device__ void sort_lds(unsigned long long *a, int P)
     const int wave = tid / SAE_WAVE;
     const int nwaves = blockDim.x / SAE_WAVE;
     for (int rI = wave; rI < P / 256; rI += nwaves) wave_sort256(a + rI * 256);
-    __syncthreads();
+    lds_barrier();
     unsigned long long *src = a, *dst = a + P;
     const int E = P / (int)blockDim.x > 0 ? P / (int)blockDim.x : 1;
     for (int run = 256; run < P; run <<= 1) {
@@ -288,14 +297,14 @@ __device__ void sort_lds(unsigned long long *a, int P)
                 D[e] = takeA ? A[i++] : B[jb++];
             }
         }
-        __syncthreads();
+        lds_barrier();
         unsigned long long *t = src;
         src = dst;
         dst = t;
     }
     if (src != a) {
         for (int i = tid; i < P; i += blockDim.x) a[i] = src[i];
-        __syncthreads();
+        lds_barrier();
     }
 }
 
@@ -405,7 +414,7 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
         b.mn = ~0ull;
         b.mx = 0;
     }
-    __syncthreads();
+    lds_barrier();
     unsigned long long mn = ~0ull, mx = 0;
     for (int i = tid; i < n; i += nt) {
         const unsigned long long e = el[i];
@@ -421,7 +430,7 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
         atomicMin(&b.mn, mn);
         atomicMax(&b.mx, mx);
     }
-    __syncthreads();
+    lds_barrier();
     mn = b.mn;
     mx = b.mx;
     if (mn == mx) return mn;
@@ -433,12 +442,12 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
         sh -= w;
         const int nb = 1 << w;
         for (int i = tid; i < nb; i += nt) b.hist[i] = 0;
-        __syncthreads();
+        lds_barrier();
         for (int i = tid; i < n; i += nt) {
             const unsigned long long e = el[i];
             if ((sh + w >= 64) || (e >> (sh + w)) == prefix) atomicAdd(&b.hist[(uint32_t)(e >> sh) & (nb - 1)], 1u);
         }
-        __syncthreads();
+        lds_barrier();
         // the bin holding the rem-th element: block scan, each thread owning `per` bins
         const int per = (nb + nt - 1) / nt;
         uint32_t s = 0;
@@ -448,7 +457,7 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
         }
         const uint32_t inc = wave_incl_scan(s);
         if (lane == 63) b.wsum[wave] = inc;
-        __syncthreads();
+        lds_barrier();
         uint32_t run = inc - s;
         for (int w2 = 0; w2 < wave; ++w2) run += b.wsum[w2];
         if (run < rem && rem <= run + s) {
@@ -463,9 +472,9 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
                 run += v;
             }
         }
-        __syncthreads();
+        lds_barrier();
         const uint32_t bin = b.bin, below = b.below, cnt = b.cnt;
-        __syncthreads();
+        lds_barrier();
         prefix = (prefix << w) | (unsigned long long)bin;
         rem -= below;
         if (cnt == rem || sh == 0) break;
@@ -491,7 +500,7 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
             for (int i = 0; i < n; ++i) rk += (el[i] < e) ? 1u : 0u;
             if (rk == r - 1) b.res = e;
         }
-        __syncthreads();
+        lds_barrier();
         return b.res;
     }
     if (tid < SAE_WAVE) {
@@ -507,17 +516,30 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
     }
     if (tid < SEL_PIVOTS + 1) b.pcnt[tid] = 0;
     if (tid == 0) b.fill = 0;
-    __syncthreads();
-    for (int i = tid; i < n; i += nt) {
-        const unsigned long long e = el[i];
-        int k = 0;  // pivots below e
+    lds_barrier();
+    // four elements per thread per round, their searches interleaved
+    for (int i0 = tid; i0 < n; i0 += 4 * nt) {
+        unsigned long long e[4];
+        int k[4];  // pivots below e
 #pragma unroll
-        for (int st = 32; st > 0; st >>= 1)
-            if (b.piv[k + st - 1] < e) k += st;
-        k += (b.piv[SEL_PIVOTS - 1] < e && k == SEL_PIVOTS - 1) ? 1 : 0;
-        atomicAdd(&b.pcnt[k], 1u);
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * nt;
+            e[u] = (i < n) ? el[i] : 0ull;
+            k[u] = 0;
+        }
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (b.piv[k[u] + st - 1] < e[u]) k[u] += st;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            k[u] += (b.piv[SEL_PIVOTS - 1] < e[u] && k[u] == SEL_PIVOTS - 1) ? 1 : 0;
+            if (i0 + u * nt < n) atomicAdd(&b.pcnt[k[u]], 1u);
+        }
     }
-    __syncthreads();
+    lds_barrier();
     if (tid < SAE_WAVE) {
         // the interval holding the r-th element (interval SEL_PIVOTS counted by lane 63)
         const uint32_t v = b.pcnt[tid] + ((tid == SAE_WAVE - 1) ? b.pcnt[SEL_PIVOTS] : 0u);
@@ -536,14 +558,14 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     const uint32_t kb = b.kb, kbelow = b.kbelow, kn = b.kn;
     if (kn > SEL_TMP) {
-        __syncthreads();
+        lds_barrier();
         const unsigned long long B = lds_select_bound(el, n, r, b);  // exactly r elements <= B
         // the r-th smallest is the largest element <= B
         if (tid == 0) b.mx = 0;
-        __syncthreads();
+        lds_barrier();
         unsigned long long mx = 0;
         for (int i = tid; i < n; i += nt) mx = (el[i] <= B && el[i] > mx) ? el[i] : mx;
         for (int d = 32; d > 0; d >>= 1) {
@@ -551,16 +573,22 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
             mx = o > mx ? o : mx;
         }
         if (lane == 0) atomicMax(&b.mx, mx);
-        __syncthreads();
+        lds_barrier();
         return b.mx;
     }
-    for (int i = tid; i < n; i += nt) {
-        const unsigned long long e = el[i];
-        const bool lo_ok = (kb == 0) || (b.piv[kb - 1] < e);
-        const bool hi_ok = (kb == SEL_PIVOTS) || (e <= b.piv[kb]);
-        if (lo_ok && hi_ok) b.tmp[atomicAdd(&b.fill, 1u)] = e;
+    const unsigned long long plo = (kb == 0) ? 0ull : b.piv[kb - 1];
+    const unsigned long long phi = (kb == SEL_PIVOTS) ? ~0ull : b.piv[kb];
+    for (int i0 = tid; i0 < n; i0 += 4 * nt) {
+        unsigned long long e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = (i0 + u * nt < n) ? el[i0 + u * nt] : 0ull;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool in = i0 + u * nt < n && (kb == 0 || plo < e[u]) && e[u] <= phi;
+            if (in) b.tmp[atomicAdd(&b.fill, 1u)] = e[u];
+        }
     }
-    __syncthreads();
+    lds_barrier();
     const uint32_t want = r - kbelow - 1;
     for (int t = tid; t < (int)kn; t += nt) {
         const unsigned long long e = b.tmp[t];
@@ -572,7 +600,7 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
         for (; i < kn; ++i) rk += (b.tmp[i] < e) ? 1u : 0u;
         if (rk == want) b.res = e;
     }
-    __syncthreads();
+    lds_barrier();
     return b.res;
 }
 
@@ -585,7 +613,6 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
 // evenly over it: a sample without long runs of consecutive ids keeps the
 // buckets of an id-ordered queue (equal keys) small.
 static_assert(SCAN_THREADS == SAMPLE_CHUNK, "one sampled block per thread");
-static_assert(SAMPLE_WGS / SAE_SPLIT_G <= SAE_WAVE, "a group's chunks fit one wave");
 __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
 {
     __shared__ ScoreTab tab;
@@ -624,7 +651,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
         pos_s = 0;
         st_s = 0;
     }
-    __syncthreads();
+    lds_barrier();
     uint32_t st = 0;
     const int q = meta_queue(m);
     if (b >= 0 && meta_evictable(m) && q < Q) {
@@ -635,7 +662,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
         tq[p] = (uint8_t)q;
     }
     if (st) atomicOr(&st_s, st);
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x == 0) {
         uint32_t o = 0;
         for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
@@ -645,7 +672,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
     }
     if (threadIdx.x < SAE_MAX_QUEUES)
         c.samp_qn[((long long)inst * SAMPLE_WGS + chunk) * SAE_MAX_QUEUES + threadIdx.x] = qcnt[threadIdx.x];
-    __syncthreads();
+    lds_barrier();
     // the chunk's region holds queue 0's elements, then queue 1's, ...
     const long long reg = ((long long)inst * SAMPLE_WGS + chunk) * SAMPLE_CHUNK;
     const uint32_t n = pos_s;
@@ -660,22 +687,6 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
 __device__ __forceinline__ int pow2_ge(int x)
 {
     return x <= 1 ? 1 : 1 << (32 - __clz(x - 1));
-}
-
-// Largest of n elements in LDS (all threads call; n >= 1).
-__device__ unsigned long long lds_max(const unsigned long long *el, int n, unsigned long long *slot)
-{
-    if (threadIdx.x == 0) *slot = 0;
-    __syncthreads();
-    unsigned long long mx = 0;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) mx = el[i] > mx ? el[i] : mx;
-    for (int d = 32; d > 0; d >>= 1) {
-        const unsigned long long o = __shfl_xor(mx, d, SAE_WAVE);
-        mx = o > mx ? o : mx;
-    }
-    if (lane_id() == 0) atomicMax(slot, mx);
-    __syncthreads();
-    return *slot;
 }
 
 // Fixed-step binary searches: every step is unrolled, so that the searches of
@@ -717,7 +728,7 @@ __device__ void rank_sort(const unsigned long long *src, int n, unsigned long lo
         for (; i < n; ++i) rank += (src[i] < e) ? 1 : 0;
         dst[rank] = e;
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Sample rank r of the candidate bound: with f the sampled fraction and need
@@ -734,77 +745,6 @@ __device__ __forceinline__ double sample_fraction(long long N)
 {
     const long long S = (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) ? N : (long long)SAMPLE_WGS * SAMPLE_CHUNK;
     return (double)S / (double)N;
-}
-
-// Pool-scan engine, step 2a: per (instance, queue) and group of
-// SAMPLE_WGS / SAE_SPLIT_G chunks, keep the group's r_max smallest sampled
-// elements (r_max: the bound rank for need = k), unordered.  The bound's
-// r-th smallest sampled element is then among the kept ones.
-#define GROUP_CHUNKS (SAMPLE_WGS / SAE_SPLIT_G)
-#define GROUP_CAP (GROUP_CHUNKS * SAMPLE_CHUNK)
-__global__ void __launch_bounds__(SEL_THREADS) k_split1(DevCtx c, SelectArgs a)
-{
-    extern __shared__ unsigned long long el[];  // [GROUP_CAP]
-    __shared__ BoundScratch bs;
-    __shared__ uint32_t cbase[GROUP_CHUNKS], cpre[GROUP_CHUNKS + 1];
-    __shared__ uint32_t kept_s;
-    const int g = blockIdx.x;
-    const int q = blockIdx.y;
-    const int inst = blockIdx.z;
-    const int Q = c.Q;
-    const int tid = threadIdx.x;
-    const long long iqg = ((long long)inst * Q + q) * SAE_SPLIT_G + g;
-    const int chunk0 = g * GROUP_CHUNKS;
-    if (tid == 0) kept_s = 0;
-    if (tid < GROUP_CHUNKS) {
-        // chunk tid: where queue q's elements start in its region, and how many (a scan over one wave)
-        const uint32_t *qn = c.samp_qn + ((long long)inst * SAMPLE_WGS + chunk0 + tid) * SAE_MAX_QUEUES;
-        uint32_t v[SAE_MAX_QUEUES];
-#pragma unroll
-        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) v[qq] = qn[qq];
-        uint32_t o = 0, cnt = 0;
-#pragma unroll
-        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
-            o += (qq < q) ? v[qq] : 0u;
-            cnt = (qq == q) ? v[qq] : cnt;
-        }
-        cbase[tid] = o;
-        const uint32_t inc = wave_incl_scan(cnt);
-        cpre[tid] = inc - cnt;
-        if (tid == GROUP_CHUNKS - 1) cpre[GROUP_CHUNKS] = inc;
-    }
-    __syncthreads();
-    const uint32_t ng = cpre[GROUP_CHUNKS];
-    const unsigned long long *sp = c.samp + ((long long)inst * SAMPLE_WGS + chunk0) * SAMPLE_CHUNK;
-    unsigned long long ev[GROUP_CAP / SEL_THREADS];
-#pragma unroll
-    for (int m = 0; m < GROUP_CAP / SEL_THREADS; ++m) {
-        const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
-        const int ch = last_le<5>(cpre, GROUP_CHUNKS, i);  // the chunk holding element i
-        ev[m] = (i < ng) ? sp[(long long)ch * SAMPLE_CHUNK + cbase[ch] + (i - cpre[ch])] : ~0ull;
-    }
-#pragma unroll
-    for (int m = 0; m < GROUP_CAP / SEL_THREADS; ++m) {
-        const uint32_t i = tid + (uint32_t)m * SEL_THREADS;
-        if (i < ng) el[i] = ev[m];
-    }
-    __syncthreads();
-    const uint32_t rmax = bound_rank((double)inst_k(a, inst, c.max_k), sample_fraction(c.N));
-    unsigned long long *out = c.kept + iqg * SAE_SPLIT_RCAP;
-    if (rmax > SAE_SPLIT_RCAP) {
-        if (tid == 0) c.kept_n[iqg] = ~0u;  // beyond this engine's bound search: exact path
-    } else if (ng <= rmax) {
-        for (uint32_t i = tid; i < ng; i += blockDim.x) out[i] = el[i];
-        if (tid == 0) c.kept_n[iqg] = ng;
-    } else {
-        const unsigned long long B = lds_select_rank(el, (int)ng, rmax, bs);  // exactly rmax elements <= B
-        for (uint32_t i = tid; i < ng; i += blockDim.x) {
-            const unsigned long long e = el[i];
-            if (e <= B) out[atomicAdd(&kept_s, 1u)] = e;
-        }
-        if (tid == 0) c.kept_n[iqg] = rmax;
-    }
-    if (tid == 0) c.samp_tot[iqg] = ng;
 }
 
 // Filter entry of the pool scan for one (type, queue) (see k_scan):
@@ -877,62 +817,67 @@ __device__ uint32_t lognormal_dt_floor(const ScoreTab &t, int q, int ty, uint32_
     return hi;
 }
 
-// Pool-scan engine, step 2b: per (instance, queue), the candidate bound and the
-// candidate buckets.  The bound is the r-th smallest sampled (key, id); a
-// queue that is estimated small takes every evictable block, and one the
-// sample missed gets a single bucket for all of them.  Bucket upper ends are
-// the sampled elements at or below the bound -- all of them up to
-// SAE_NBUCKET - 1, else an evenly spread subset -- and the last one is the
-// bound.  Resets the scan's spill list.
+// Pool-scan engine, step 2: per (instance, queue), the candidate bound and the
+// candidate buckets.  The workgroup stages every sampled element of its queue
+// in LDS; the bound is their r-th smallest (key, id); a queue that is
+// estimated small takes every evictable block, and one the sample missed gets
+// a single bucket for all of them.  Bucket upper ends are the sampled elements
+// at or below the bound -- all of them up to SAE_NBUCKET - 1, else an evenly
+// spread subset -- and the last one is the bound.  Also writes the scan's
+// filter entries and resets its spill list.
 #define ALL_EST 2048.0
-__global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
+static_assert(SAMPLE_WGS <= SAE_WAVE, "the chunks' counts fit one wave");
+static_assert(SAMPLE_WGS * SAMPLE_CHUNK <= LCAP, "a queue's sampled elements fit the LDS staging area");
+__global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
 {
     extern __shared__ unsigned long long el[];  // [LCAP]
     __shared__ BoundScratch bs;
-    __shared__ uint32_t kn_s[SAE_SPLIT_G], st_s[SAE_SPLIT_G], kpre[SAE_SPLIT_G + 1], tot_s, nsp_s;
-    __shared__ int32_t bad_s, nb_s;
-    __shared__ unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s, mx_s;
+    __shared__ uint32_t cbase[SAMPLE_WGS], cpre[SAMPLE_WGS + 1], nsp_s;
+    __shared__ int32_t nb_s;
+    __shared__ unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s;
     __shared__ ScoreTab tab;
     const int q = blockIdx.x;
     const int inst = blockIdx.y;
     const int Q = c.Q;
     const int tid = threadIdx.x;
+    const int wave = tid / SAE_WAVE;
     const long long iq = (long long)inst * Q + q;
     load_score_tab(tab, c.state[inst], c);
-    if (tid < SAE_SPLIT_G) kn_s[tid] = c.kept_n[iq * SAE_SPLIT_G + tid];
-    if (tid >= SAE_SPLIT_G && tid < 2 * SAE_SPLIT_G) st_s[tid - SAE_SPLIT_G] = c.samp_tot[iq * SAE_SPLIT_G + tid - SAE_SPLIT_G];
+    if (tid < SAE_WAVE) {
+        // chunk tid: where queue q's elements start in its region, and how many
+        const bool in = tid < SAMPLE_WGS;
+        uint32_t v[SAE_MAX_QUEUES];
+        const uint32_t *qn = c.samp_qn + ((long long)inst * SAMPLE_WGS + (in ? tid : 0)) * SAE_MAX_QUEUES;
+#pragma unroll
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) v[qq] = qn[qq];
+        uint32_t o = 0, cnt = 0;
+#pragma unroll
+        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+            o += (qq < q) ? v[qq] : 0u;
+            cnt = (qq == q) ? v[qq] : cnt;
+        }
+        cnt = in ? cnt : 0u;
+        const uint32_t inc = wave_incl_scan(cnt);
+        if (in) {
+            cbase[tid] = o;
+            cpre[tid] = inc - cnt;
+        }
+        if (tid == SAMPLE_WGS - 1) cpre[SAMPLE_WGS] = inc;
+    }
     if (tid == SEL_THREADS - 1) {
         c.spill_n[iq] = 0;  // this call's spill list starts empty
         nsp_s = 0;
         nb_s = 0;
         bound_s = 0;
     }
-    __syncthreads();
-    if (tid < SAE_WAVE) {
-        const bool in = tid < SAE_SPLIT_G;
-        const uint32_t kn = in ? kn_s[tid] : 0u;
-        const uint32_t kv = (kn == ~0u) ? 0u : kn;
-        const uint32_t inc = wave_incl_scan(kv);
-        uint32_t t = in ? st_s[tid] : 0u;
-        for (int d = 32; d > 0; d >>= 1) t += __shfl_xor(t, d, SAE_WAVE);
-        const bool bad = __ballot(kn == ~0u) != 0ull;
-        if (in) kpre[tid] = inc - kv;
-        if (tid == SAE_SPLIT_G - 1) kpre[SAE_SPLIT_G] = inc;
-        if (tid == 0) {
-            tot_s = t;
-            bad_s = bad ? 1 : 0;
-        }
-    }
-    __syncthreads();
-    const uint32_t tot = tot_s;
+    lds_barrier();
+    const uint32_t tot = cpre[SAMPLE_WGS];  // sampled elements of this queue
     const int kq = inst_k(a, inst, c.max_k);
     const double f = sample_fraction(c.N);
     const double est = (double)tot / f;
     const uint32_t r = bound_rank(fmin((double)kq, est), f);
     if (kq == 0) {
         // nothing to select: no candidates
-    } else if (bad_s) {
-        if (tid == 0) nb_s = -1;  // exact path
     } else if (tot == 0) {
         // the sample holds no block of this queue: all its evictable blocks, one bucket
         if (tid == 0) {
@@ -942,15 +887,15 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
         }
     } else {
         const bool all = (r >= tot) || (est <= ALL_EST);
-        const uint32_t K = kpre[SAE_SPLIT_G];  // kept elements, <= SAE_SPLIT_G * SAE_SPLIT_RCAP = LCAP
-        const unsigned long long *kp = c.kept + iq * SAE_SPLIT_G * SAE_SPLIT_RCAP;
+        const uint32_t K = tot;  // <= SAMPLE_WGS * SAMPLE_CHUNK <= LCAP
+        const unsigned long long *sp = c.samp + (long long)inst * SAMPLE_WGS * SAMPLE_CHUNK;
         for (uint32_t i0 = 0; i0 < K; i0 += 4 * SEL_THREADS) {
             unsigned long long ev[4];
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 const uint32_t i = i0 + tid + (uint32_t)m * SEL_THREADS;
-                const int g = last_le<3>(kpre, SAE_SPLIT_G, i);
-                ev[m] = (i < K) ? kp[(long long)g * SAE_SPLIT_RCAP + (i - kpre[g])] : ~0ull;
+                const int ch = last_le<6>(cpre, SAMPLE_WGS, i);  // the chunk holding element i
+                ev[m] = (i < K) ? sp[(long long)ch * SAMPLE_CHUNK + cbase[ch] + (i - cpre[ch])] : ~0ull;
             }
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
@@ -958,20 +903,17 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
                 if (i < K) el[i] = ev[m];
             }
         }
-        __syncthreads();
+        lds_barrier();
         unsigned long long bound;
-        uint32_t rr;  // kept elements at or below the bound
+        uint32_t rr;  // staged elements at or below the bound
         if (all) {
             bound = ~0ull;
             rr = K;
-        } else if (r < K) {
+        } else {  // r < K
             bound = lds_select_rank(el, (int)K, r, bs);
             rr = r;
-        } else {
-            bound = lds_max(el, (int)K, &mx_s);
-            rr = K;
         }
-        // upper ends: the elements <= bound, or every stride-th kept one of them
+        // upper ends: the elements <= bound, or every stride-th staged one of them
         const uint32_t stride = rr <= SAE_NBUCKET - 1 ? 1u : (rr + SAE_NBUCKET - 3) / (SAE_NBUCKET - 2);
         for (uint32_t i = tid; i < K; i += blockDim.x) {
             const unsigned long long e = el[i];
@@ -980,7 +922,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
                 if (p < SAE_NBUCKET - 1) spl_raw[p] = e;
             }
         }
-        __syncthreads();
+        lds_barrier();
         const int np = nsp_s < SAE_NBUCKET - 1 ? (int)nsp_s : SAE_NBUCKET - 1;
         rank_sort(spl_raw, np, spl);
         if (tid == 0) {
@@ -989,8 +931,35 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
             bound_s = bound;
             nb_s = nb;
         }
+        lds_barrier();
+        // Few sampled upper ends (small k against the sample): each gap
+        // between consecutive ones (the first taken as wide as the second) is
+        // cut into F = 4 or 2 equal ranges of (key << 32 | id) values, with
+        // F * ends <= 255, so that buckets stay small.  Any ascending ends
+        // ending at the bound are valid; these only balance the work.
+        const int nb0 = nb_s;
+        const int LF = (4 * nb0 <= SAE_NBUCKET - 1) ? 2 : ((2 * nb0 <= SAE_NBUCKET - 1) ? 1 : 0);
+        const int F = 1 << LF;
+        if (F >= 2) {
+            if (tid < nb0) {
+                const unsigned long long hi = spl[tid];
+                unsigned long long lo;
+                if (tid > 0) {
+                    lo = spl[tid - 1];
+                } else {
+                    const unsigned long long w = (nb0 >= 2) ? spl[1] - spl[0] : 0ull;
+                    lo = (spl[0] >= w) ? spl[0] - w : 0ull;
+                }
+                const unsigned long long d = (hi - lo) >> LF;
+                for (int j = 1; j < F; ++j) spl_raw[tid * F + j - 1] = lo + d * (unsigned long long)j;
+                spl_raw[tid * F + F - 1] = hi;
+            }
+            lds_barrier();
+            if (tid < nb0 * F) spl[tid] = spl_raw[tid];
+            if (tid == 0) nb_s = nb0 * F;
+        }
     }
-    __syncthreads();
+    lds_barrier();
     const int nb = nb_s;
     if (tid < nb) c.split[iq * SAE_NBUCKET + tid] = spl[tid];
     if (tid == 0) {
@@ -998,7 +967,6 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
         c.nsplit[iq] = nb;
     }
     // the scan's filter entries of this queue: one wave per token type
-    const int wave = tid / SAE_WAVE;
     if (wave < 8) {
         const uint32_t tk = (uint32_t)(bound_s >> 32);
         uint32_t D = 0;
@@ -1025,7 +993,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split2(DevCtx c, SelectArgs a)
 // with 16-, 8- and 16-byte loads of last_access, meta and off), with the
 // loads of the next two batches in flight while one is examined.  A cheap
 // exact filter drops almost every evictable block whose (key, id) lies above
-// its queue's bound without evaluating Eq. 1-3; its table (k_split2, one
+// its queue's bound without evaluating Eq. 1-3; its table (k_split, one
 // 16-byte entry per (type, queue), see scan_entry) makes every test pass
 // trivially for the other kinds, so a block costs one table read and no
 // branch:
@@ -1243,7 +1211,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
 
     // what the waves left queued, scored by the four waves together
     if (lane == 0) left_s[wave] = nl;
-    __syncthreads();
+    lds_barrier();
     if (tid == 0) {
         uint32_t o = 0;
         for (int w = 0; w < SCAN_WAVES; ++w) {
@@ -1253,7 +1221,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
         }
         left_s[SCAN_WAVES] = o;
     }
-    __syncthreads();
+    lds_barrier();
     const uint32_t total = left_s[SCAN_WAVES];
     for (uint32_t i0 = (uint32_t)wave * SAE_WAVE; i0 < total; i0 += SCAN_THREADS) {  // wave-uniform
         const uint32_t i = i0 + (uint32_t)lane;
@@ -1263,7 +1231,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
         score(act, act ? s_lst[w][i - left_s[w]] : make_int4(0, 0, 0, 0));
     }
     if (st) atomicOr(&st_s, st);
-    __syncthreads();
+    lds_barrier();
     if (tid < Q) c.creg_n[rbase + tid] = min(cnt_s[tid], (uint32_t)SAE_CAND_REGION);
     if (tid == 0) set_status(c.status, st_s);
 }
@@ -1326,7 +1294,7 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
     for (int u = 0; u < GATHER_RPT; ++u) loc += cv[u];
     const uint32_t inc = wave_incl_scan(loc);
     if (lane == 63) wsum[tid >> 6] = inc;
-    __syncthreads();
+    lds_barrier();
     {
         uint32_t o = inc - loc;
         for (int w = 0; w < (tid >> 6); ++w) o += wsum[w];
@@ -1338,7 +1306,7 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
         }
         if (tid == GATHER_THREADS - 1) offs[gx] = o;  // cv is 0 beyond gx
     }
-    __syncthreads();
+    lds_barrier();
     const uint32_t total_r = offs[gx];
     const uint32_t nsp = ns < (uint32_t)c.cand_cap ? ns : (uint32_t)c.cand_cap;
     const uint32_t C = total_r + nsp;
@@ -1371,19 +1339,19 @@ __global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs 
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     {
         const uint32_t v = hist[tid];
         const uint32_t inc2 = wave_incl_scan(v);
         if (lane == 63) wsum[tid >> 6] = inc2;
-        __syncthreads();
+        lds_barrier();
         uint32_t pre = 0;
         for (int w = 0; w < (tid >> 6); ++w) pre += wsum[w];
         boff[tid] = pre + inc2 - v;
         c.g_rel[iqs * SAE_NBUCKET + tid] = pre + inc2 - v;
         c.g_cnt[iqs * SAE_NBUCKET + tid] = v;
     }
-    __syncthreads();
+    lds_barrier();
     unsigned long long *out = c.cand + iq * SAE_LCAP + lo;
     for (uint32_t i = tid; i < n; i += GATHER_THREADS) {
         const unsigned long long e = el[i];
@@ -1439,7 +1407,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
             off_s = rv;
         }
     }
-    __syncthreads();
+    lds_barrier();
     if (j >= NB) return;  // uniform per workgroup
     const uint32_t C = C_s, off = off_s, n = pre_v[SAE_GATHER_S];
     if (tid == 0) {
@@ -1462,7 +1430,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
     if (n <= BUCKET_THREADS) {
         const unsigned long long e0 = (tid < (int)n) ? elem((uint32_t)tid) : ~0ull;
         if (tid < (int)n) bel[tid] = e0;
-        __syncthreads();
+        lds_barrier();
         if (tid < (int)n) {
             uint32_t rank = 0, i = 0;
             for (; i + 8 <= n; i += 8) {
@@ -1491,7 +1459,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
         sh[tid] = 0;
         sfill[tid] = 0;
     }
-    __syncthreads();
+    lds_barrier();
     __shared__ unsigned long long praw[SEL_PIVOTS];
     if (tid < SAE_WAVE) {
         const unsigned long long p = bel[(uint32_t)(((unsigned long long)tid * n) / SEL_PIVOTS)];
@@ -1503,7 +1471,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
         for (int i = 0; i < SEL_PIVOTS; ++i) rk += (praw[i] < p) ? 1u : 0u;
         piv[rk] = p;
     }
-    __syncthreads();
+    lds_barrier();
     for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
         const unsigned long long e = bel[t];
         int k = 0;  // pivots below e
@@ -1514,7 +1482,7 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
         sk[t] = (uint8_t)k;
         atomicAdd(&sh[k], 1u);
     }
-    __syncthreads();
+    lds_barrier();
     if (tid < SAE_WAVE) {
         // exclusive offsets of the SEL_PIVOTS + 1 sub-buckets (lane 63 also owns the last one)
         const uint32_t v = sh[tid] + ((tid == SAE_WAVE - 1) ? sh[SEL_PIVOTS] : 0u);
@@ -1528,12 +1496,12 @@ __global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs 
             sh[SEL_PIVOTS + 1] = inc;
         }
     }
-    __syncthreads();
+    lds_barrier();
     for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
         const int k = sk[t];
         bel2[sh[k] + atomicAdd(&sfill[k], 1u)] = bel[t];
     }
-    __syncthreads();
+    lds_barrier();
     for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
         // position t of the sub-bucket order: rank within its sub-bucket
         const unsigned long long e = bel2[t];
@@ -1898,14 +1866,10 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
     // step 1: sample
     hipLaunchKernelGGL(k_sample, dim3(SAMPLE_WGS, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 2: candidate bounds and bucket upper ends
-    const size_t lds_g = (size_t)GROUP_CAP * sizeof(unsigned long long);
-    if ((e = allow_lds((const void *)k_split1, lds_g)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_split1, dim3(SAE_SPLIT_G, c.Q, c.n_inst), dim3(SEL_THREADS), lds_g, s, c, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // step 2: candidate bounds, bucket upper ends, the scan's filter entries
     const size_t lds_el = (size_t)LCAP * sizeof(unsigned long long);
-    if ((e = allow_lds((const void *)k_split2, lds_el)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_split2, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
+    if ((e = allow_lds((const void *)k_split, lds_el)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_split, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // step 3: streaming pass (with profiling, the events carry the dispatch's own start and end)
     if (ev0 && ev1)

@@ -178,11 +178,10 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.g_base, I * Q * SAE_GATHER_S) && dev_alloc(c, &d.g_tot, I * Q * SAE_GATHER_S) &&
               dev_alloc(c, &d.g_rel, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
               dev_alloc(c, &d.g_cnt, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
-              dev_alloc(c, &d.kept, I * Q * SAE_SPLIT_G * SAE_SPLIT_RCAP) &&
-              dev_alloc(c, &d.kept_n, I * Q * SAE_SPLIT_G) && dev_alloc(c, &d.samp_tot, I * Q * SAE_SPLIT_G) && dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
-              dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
+              dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
               dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
               dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&
+              dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
               dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);

@@ -17,10 +17,8 @@
 #define SAE_BINS (1 << SAE_DIGIT_BITS)
 
 // Sampling of the pool-scan engine: chunks per instance and blocks per chunk.
-#define SAE_SAMPLE_WGS 256
+#define SAE_SAMPLE_WGS 64
 #define SAE_SAMPLE_CHUNK 256
-#define SAE_SPLIT_G 8         // groups of sampling chunks, per (instance, queue), in the bound search
-#define SAE_SPLIT_RCAP 2048   // largest sample rank of the candidate bound
 #define SAE_GATHER_S 16       // slices of the scan workgroups, per (instance, queue), in the gather
 #define SAE_CAND_REGION 128  // candidate slots per (scan workgroup, queue)
 // Candidate buckets of the pool-scan engine, per (instance, queue): the bucket
@@ -113,9 +111,6 @@ struct DevCtx {
     int32_t *eflim;            // [n_inst][16] evict-first queue: largest candidate id per num_tokens - 1 (-1: none)
     unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
     uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
-    unsigned long long *kept;  // [n_inst][Q][SAE_SPLIT_G][SAE_SPLIT_RCAP] smallest sampled elements per group
-    uint32_t *kept_n;          // [n_inst][Q][SAE_SPLIT_G] elements kept (~0u: rank beyond SAE_SPLIT_RCAP)
-    uint32_t *samp_tot;        // [n_inst][Q][SAE_SPLIT_G] sampled elements per group
     uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, spilled, slow path
     unsigned long long *creg;  // [n_inst][scan_gx][Q][SAE_CAND_REGION] candidates per scan workgroup
     uint32_t *creg_n;          // [n_inst][scan_gx][Q]
