@@ -8,9 +8,12 @@
 // recently_evicted (Algorithm 1): victims are appended to a ring of
 // W + max_k entries in eviction order, each stamped with the eviction count
 // right after its decision; an entry is live while fewer than W evictions
-// followed it.  A hash table maps a content hash to its ring entry.  When a
-// ring slot is reused, its old entry (always expired) leaves the table first;
-// removals and inserts run in separate kernels.
+// followed it.  A hash table maps a content hash to its ring position; a
+// lookup follows a slot only if the ring entry there still holds that hash,
+// is live and not consumed.  A reused ring slot's old table slot is therefore
+// left in place (stale, like a deleted one) and the table is rebuilt from the
+// ring once stale and deleted slots reach a quarter of it, so a commit only
+// inserts.
 #include "sae_internal.h"
 
 namespace {
@@ -98,20 +101,6 @@ __device__ __forceinline__ int ghost_find(const GhostSlot *tab, uint32_t mask, c
         s = (s + 1) & mask;
     }
     return -1;
-}
-
-__device__ __forceinline__ void ghost_remove(GhostSlot *tab, uint32_t mask, unsigned long long h, uint32_t ring_pos)
-{
-    uint32_t s = hash_home(h, mask);
-    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        unsigned long long v = tab[s].hash;
-        if (v == SAE_EMPTY_HASH) return;
-        if (v == h && tab[s].ring == ring_pos) {
-            tab[s].hash = SAE_TOMB_HASH;
-            return;
-        }
-        s = (s + 1) & mask;
-    }
 }
 
 __device__ __forceinline__ bool ghost_insert(GhostSlot *tab, uint32_t mask, unsigned long long h, uint32_t ring_pos)
@@ -430,10 +419,10 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
 }
 
 // ---------------------------------------------------------------------------
-// Commit, phase 1: per victim, free the block, erase its index entry, count
-// it (Algorithm 3 evicted[tau], Algorithm 2 queue_evictions[q]), update its
-// parent, and drop the expired ring entry its ring slot will take.
-__global__ void k_commit_a(DevCtx c, const int32_t *decision)
+// Commit, per victim: free the block, erase its index entry, count it
+// (Algorithm 3 evicted[tau], Algorithm 2 queue_evictions[q]), update its
+// parent and record it in recently_evicted.
+__global__ void k_commit(DevCtx c, const int32_t *decision)
 {
     __shared__ int32_t sums[SAE_CF_N];
     const int inst = blockIdx.y;
@@ -449,52 +438,33 @@ __global__ void k_commit_a(DevCtx c, const int32_t *decision)
     }
     if (v >= 0) {
         const long long g = (long long)inst * c.N + v;
-        GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
-        GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-        const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
-        const GhostEntry old = ring[rp];
-        if (old.hash != 0 && !(old.tq & 0x100u)) ghost_remove(gt, c.ghost_mask, old.hash, rp);
         const uint32_t m = c.meta[g];
+        const unsigned long long h = c.hash[g];
+        const int32_t p = c.parent[g];
         atomicAdd(&sums[SAE_CF_EVICTED + meta_type(m) % SAE_N_TYPES], 1);
         atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
         meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
         IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-        index_erase(tab, c.index_mask, c.hash[g]);
-        const int32_t p = c.parent[g];
+        index_erase(tab, c.index_mask, h);
         if (p >= 0 && p < c.N) {
             const long long gp = (long long)inst * c.N + p;
             const int before = atomicSub(&c.child_count[gp], 1);
             if (before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
         }
+        GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+        GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+        const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
+        GhostEntry e;
+        e.hash = h;
+        e.stamp = s.ev_before + d;
+        e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3);
+        e.pad_ = 0;
+        ring[rp] = e;
+        if (!ghost_insert(gt, c.ghost_mask, h, rp)) set_status(c.status, SAE_ST_GHOST_FULL);
     }
     __syncthreads();
     if (threadIdx.x < SAE_CF_N && sums[threadIdx.x])
         atomicAdd(counter_slot(c, inst, blockIdx.x) + threadIdx.x, sums[threadIdx.x]);
-}
-
-// Commit, phase 2: record the victims in recently_evicted.
-__global__ void k_commit_b(DevCtx c, const int32_t *decision)
-{
-    const int inst = blockIdx.y;
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
-    const InstState &s = c.state[inst];
-    const int d = s.last_d;
-    if (j >= d) return;
-    int32_t v = decision[(long long)inst * c.max_k + j];
-    if (v < 0 || v >= c.N) return;
-    const long long g = (long long)inst * c.N + v;
-    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
-    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-    const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
-    uint32_t m = c.meta[g];
-    unsigned long long h = c.hash[g];
-    GhostEntry e;
-    e.hash = h;
-    e.stamp = s.ev_before + d;
-    e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3);
-    e.pad_ = 0;
-    ring[rp] = e;
-    if (!ghost_insert(gt, c.ghost_mask, h, rp)) set_status(c.status, SAE_ST_GHOST_FULL);
 }
 
 inline unsigned grid_for(long long n) { return (unsigned)((n + kThreads - 1) / kThreads); }
@@ -607,9 +577,6 @@ hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, 
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s)
 {
     dim3 grid((unsigned)((c.max_k + kThreads - 1) / kThreads), (unsigned)c.n_inst);
-    hipLaunchKernelGGL(k_commit_a, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_commit_b, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
+    hipLaunchKernelGGL(k_commit, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
     return hipGetLastError();
 }
