@@ -32,6 +32,23 @@ Readings of points where the paper is silent (each listed in the design doc):
 * The learners run once per decision in which floor(evictions / K) grew
   (Algorithm 1's "every K evictions").  lambda = 0.99 decays a counter x to
   floor(99 x / 100) exactly.
+* Algorithm 4 (online log-normal MLE) keeps one interval buffer per
+  log-normal queue.  A prefix match that records intervals adds, for every
+  request and every log-normal queue among its matched blocks, the elapsed
+  time now - last_access of its deepest matched block of that queue, as it was
+  before the call, when that is >= 1 tick; a call's intervals join the buffer
+  in request order.  The buffer keeps at most IVL_CAP intervals (the oldest
+  leave first).  An update needs more than 20 intervals and then keeps the
+  last 200 (Algorithm 4); mean and std are the population moments of the fp32
+  ln of the intervals, summed exactly and rounded once (`sample_moments`).
+* The decay-power learner (App. B) bins structural blocks by o_b / o_max into
+  8 positional bins.  A bin's hit rate is hits / (hits + misses after
+  eviction): prefix-match hits of blocks in the bin, and Add() calls that find
+  a recently evicted block of the bin.  front = mean rate of bins 0-3, back =
+  of bins 4-7 (bins without events left out); gamma moves by the EMA factor
+  beta toward 1 / (back / front + 0.1) and is clipped to [0.3, 3.0].  It needs
+  more than 20 events, events in both halves and front > 0; its counters
+  restart after an update.
 """
 import math
 
@@ -41,6 +58,8 @@ from . import _native
 
 EVICT_FIRST, STRUCTURAL, LOGNORMAL, RECENCY = 0, 1, 2, 3
 N_TYPES = 5  # system, user, tool, response, cot — the order of Algorithm 3
+N_BINS = 8   # positional bins of the decay-power learner
+IVL_CAP = 4096  # intervals an Algorithm 4 buffer holds at most
 F32 = np.float32
 
 
@@ -95,7 +114,8 @@ class Params:
     """Learned parameters and learner settings (Sec. 3.1, App. B)."""
 
     def __init__(self, n_queues, w=1.0, alpha=1.0, mu=0.0, sigma=1.0, gamma=1.0,
-                 eta=0.01, T=1.0, beta=0.1, K=32, learn_w=True, learn_alpha=True):
+                 eta=0.01, T=1.0, beta=0.1, K=32, learn_w=True, learn_alpha=True,
+                 beta_ln=0.1, learn_ln=False, learn_gamma=False):
         def vec(v, n):
             a = np.zeros(n, F32)
             a[:] = np.resize(np.asarray(v, F32), n)
@@ -111,6 +131,9 @@ class Params:
         self.K = int(K)
         self.learn_w = bool(learn_w)
         self.learn_alpha = bool(learn_alpha)
+        self.beta_ln = F32(beta_ln)
+        self.learn_ln = bool(learn_ln)
+        self.learn_gamma = bool(learn_gamma)
 
 
 class OracleCache:
@@ -143,6 +166,9 @@ class OracleCache:
         self.ev_count = 0
         self.pending = False
         self.n_updates = 0
+        self.ivl = [[] for _ in range(self.Q)]   # Algorithm 4 buffers (log-normal queues)
+        self.bin_hits = [0] * N_BINS
+        self.bin_missed = [0] * N_BINS
 
     # ------------------------------------------------------------------ state
     def bind(self, last_access, queue, tau, ntok, ob, omax, valid, ref_count,
@@ -170,6 +196,15 @@ class OracleCache:
 
     def ghost_live(self, entry):
         return self.ev_count - entry[2] < self.W
+
+    def pos_bin(self, b):
+        """Positional bin of block b: floor(8 o_b / o_max), o_b taken as at most
+        o_max, bin 7 at the end and bin 0 for a one-block template (o_max = 0)."""
+        omax = int(self.omax[b])
+        if omax == 0:
+            return 0
+        o = min(int(self.ob[b]), omax)
+        return min(N_BINS - 1, (N_BINS * o) // omax)
 
     # ---------------------------------------------------------- Eq. 1-3 keys
     def keys(self, now):
@@ -254,7 +289,7 @@ class OracleCache:
             self.valid[b] = False
             h = int(self.hash[b])
             del self.index[h]
-            self.ghost[h] = (int(self.tau[b]), int(self.queue[b]), stamp)
+            self.ghost[h] = (int(self.tau[b]), int(self.queue[b]), stamp, self.pos_bin(b))
             self.evicted[self.tau[b]] += 1
             self.evictions[self.queue[b]] += 1
             par = int(self.parent[b])
@@ -266,11 +301,14 @@ class OracleCache:
             self.pending = True
 
     # ------------------------------------------------------------ prefix match
-    def prefix_match(self, hashes, lens, now, touch=True, stats=True):
+    def prefix_match(self, hashes, lens, now, touch=True, stats=True, intervals=False):
         """Strict prefix matching (Sec. 2.1): match_len = number of leading
         hashes found in the index.  All requests see the same snapshot; touches
         (last_access = now, access_count += 1 per request hit) apply afterwards.
-        With stats, every hit block counts for queue_hits[queue(b)]."""
+        With stats, every hit block counts for queue_hits[queue(b)] and, in a
+        structural queue, for the hits of its positional bin.  With intervals,
+        each request records Algorithm 4's reuse interval of each log-normal
+        queue it hit: now - last_access of its deepest matched block there."""
         hashes = np.asarray(hashes, np.uint64)
         n = len(lens)
         mlen = np.zeros(n, np.int32)
@@ -285,12 +323,26 @@ class OracleCache:
                 matched[r, m] = b
                 m += 1
             mlen[r] = m
+            deepest = {}
             for j in range(m):
                 b = matched[r, j]
+                q = int(self.queue[b])
                 if stats:
-                    self.hits[self.queue[b]] += 1
+                    self.hits[q] += 1
+                    if self.kind[q] == STRUCTURAL:
+                        self.bin_hits[self.pos_bin(b)] += 1
                 if touch:
                     touched.append(b)
+                if self.kind[q] == LOGNORMAL:
+                    deepest[q] = b
+            if intervals:
+                for q in sorted(deepest):
+                    dt = int(now) - int(self.la[deepest[q]])
+                    if dt >= 1:
+                        buf = self.ivl[q]
+                        buf.append(dt)
+                        if len(buf) > IVL_CAP:
+                            del buf[0]
         for b in touched:
             self.la[b] = now
             self.access_count[b] += 1
@@ -321,6 +373,8 @@ class OracleCache:
             g = self.ghost.pop(h, None)
             if g is not None and self.ghost_live(g):
                 self.missed[g[0]] += 1
+                if self.kind[g[1]] == STRUCTURAL:
+                    self.bin_missed[g[3]] += 1
         for i in range(len(ids)):
             if parent[i] >= 0:
                 self.child_count[parent[i]] += 1
@@ -354,6 +408,48 @@ class OracleCache:
             self.hits[q] = 0
             self.evictions[q] = 0
 
+    def lognormal_params(self):
+        """Algorithm 4 for every log-normal queue (one estimator per queue)."""
+        p = self.prm
+        for q in range(self.Q):
+            if self.kind[q] != LOGNORMAL:
+                continue
+            buf = self.ivl[q]
+            if len(buf) > 20:
+                mu_s, sigma_s = sample_moments(buf)
+                p.mu[q] = p.mu[q] + p.beta_ln * (mu_s - p.mu[q])
+                s = p.sigma[q] + p.beta_ln * (sigma_s - p.sigma[q])
+                p.sigma[q] = max(s, F32(0.1))
+                self.ivl[q] = buf[-200:]
+
+    def decay_power(self):
+        """Decay-power learner (App. B) over the 8 positional bins."""
+        p = self.prm
+        events = [self.bin_hits[i] + self.bin_missed[i] for i in range(N_BINS)]
+        if sum(events) <= 20:
+            return
+        rates = [F32(self.bin_hits[i]) / F32(events[i]) if events[i] else None for i in range(N_BINS)]
+        half = N_BINS // 2
+        front = [r for r in rates[:half] if r is not None]
+        back = [r for r in rates[half:] if r is not None]
+        if not front or not back:
+            return
+        f_avg = F32(0.0)
+        for r in front:
+            f_avg = f_avg + r
+        f_avg = f_avg / F32(len(front))
+        b_avg = F32(0.0)
+        for r in back:
+            b_avg = b_avg + r
+        b_avg = b_avg / F32(len(back))
+        if not f_avg > 0:
+            return
+        ratio = b_avg / f_avg
+        est = F32(1.0) / (ratio + F32(0.1))
+        p.gamma = clamp(p.gamma + p.beta * (est - p.gamma), 0.3, 3.0)
+        self.bin_hits = [0] * N_BINS
+        self.bin_missed = [0] * N_BINS
+
     def feedback(self, force=False):
         if not (self.pending or force):
             return False
@@ -361,6 +457,10 @@ class OracleCache:
             self.token_weights()
         if self.prm.learn_alpha:
             self.queue_weights()
+        if self.prm.learn_ln:
+            self.lognormal_params()
+        if self.prm.learn_gamma:
+            self.decay_power()
         self.pending = False
         self.n_updates += 1
         return True
@@ -368,4 +468,27 @@ class OracleCache:
     def counters(self):
         return dict(evicted=list(self.evicted), missed=list(self.missed),
                     hits=list(self.hits), evictions=list(self.evictions),
-                    ev_count=self.ev_count, pending=self.pending)
+                    ev_count=self.ev_count, pending=self.pending,
+                    bin_hits=list(self.bin_hits), bin_missed=list(self.bin_missed))
+
+
+def sample_moments(intervals):
+    """Algorithm 4's mu_sample, sigma_sample: mean and population std of
+    ln(dt) over the buffer.  ln is the fp32 recipe's ln of fl32(dt).  Every
+    x = ln(dt) is 0 or at least ln 2, so X = x * 2^24 is an integer and the
+    sums S1 = sum X, S2 = sum X^2 are exact; then, in IEEE double,
+    m = S1 / n * 2^-24, v = max(S2 / n * 2^-48 - m * m, 0), with S2 converted
+    as hi * 2^64 + lo (hi, lo its 64-bit halves), and the results rounded to
+    fp32: mu = fl32(m), sigma = fl32(sqrt(v))."""
+    x = _native.ln(np.asarray(intervals, np.float64).astype(F32))
+    n = len(x)
+    X = [int(F32(v).astype(np.float64) * 2.0 ** 24) for v in x]
+    assert all(float(Xi) == float(v) * 2.0 ** 24 for Xi, v in zip(X, x))
+    S1 = sum(X)
+    S2 = sum(Xi * Xi for Xi in X)
+    m = (float(S1) / float(n)) * 2.0 ** -24
+    s2 = float(S2 >> 64) * 2.0 ** 64 + float(S2 & (2 ** 64 - 1))
+    v = (s2 / float(n)) * 2.0 ** -48 - m * m
+    if v < 0.0:
+        v = 0.0
+    return F32(m), F32(math.sqrt(v))
