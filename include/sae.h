@@ -88,6 +88,8 @@ enum {
 };
 
 #define SAE_MAX_QUEUES 8
+#define SAE_N_BINS 8        /* positional bins of the decay-power learner (App. B)      */
+#define SAE_IVL_CAP 4096    /* intervals an Algorithm 4 buffer holds between updates    */
 
 #define SAE_META_QUEUE_SHIFT 0
 #define SAE_META_TYPE_SHIFT 3
@@ -116,6 +118,8 @@ typedef struct {
     int32_t ghost_window;              /* W of recently_evicted (>= 1; 0 = blocks)     */
     int32_t index_log2;                /* index slots per instance = 2^index_log2
                                           (0 = smallest power of two >= 2 blocks)      */
+    int32_t max_requests;              /* largest n_req of a sae_prefix_match call with
+                                          SAE_PM_INTERVALS, 0 .. 2^24 (0: none)         */
 } sae_config;
 
 /* Learned parameters and learner settings (Sec. 3.1, App. B). */
@@ -127,12 +131,18 @@ typedef struct {
     float gamma;                   /* position decay power > 0 (Eq. 2)              */
     float eta;                     /* token-weight learning rate (Algorithm 3)      */
     float temperature;             /* T of Algorithm 2, > 0                         */
-    float beta;                    /* EMA factor of Algorithm 2                     */
+    float beta;                    /* EMA factor of Algorithm 2 and of gamma        */
+    float beta_ln;                 /* EMA factor of Algorithm 4 (beta_ln)           */
     int32_t K;                     /* learners run every K evictions (Algorithm 1)  */
     uint32_t learn;                /* SAE_LEARN_* bits                              */
 } sae_params;
 
-enum { SAE_LEARN_TOKEN_WEIGHTS = 1u << 0, SAE_LEARN_QUEUE_WEIGHTS = 1u << 1 };
+enum {
+    SAE_LEARN_TOKEN_WEIGHTS = 1u << 0, /* Algorithm 3                              */
+    SAE_LEARN_QUEUE_WEIGHTS = 1u << 1, /* Algorithm 2                              */
+    SAE_LEARN_LOGNORMAL = 1u << 2,     /* Algorithm 4: mu_q, sigma_q              */
+    SAE_LEARN_DECAY_POWER = 1u << 3    /* gamma from positional hit rates (App. B) */
+};
 
 /* Feedback counters of one instance (Algorithms 1-3). */
 typedef struct {
@@ -143,6 +153,10 @@ typedef struct {
     int64_t eviction_count;           /* all evictions so far                     */
     int32_t pending;                  /* learners due (eviction_count crossed K)  */
     int32_t n_updates;                /* learner runs so far                      */
+    int32_t bin_hits[SAE_N_BINS];     /* decay-power learner: prefix-match hits of
+                                         structural blocks per positional bin     */
+    int32_t bin_missed[SAE_N_BINS];   /* ... and misses after their eviction
+                                         (both only while SAE_LEARN_DECAY_POWER) */
 } sae_counters;
 
 /* Caller-owned device arrays of the block pool (layout above). */
@@ -245,7 +259,7 @@ sae_status sae_ref_blocks(sae_ctx *ctx, int32_t n, const int32_t *inst, const in
                           int32_t delta, sae_stream_t stream);
 
 /* Flags of sae_prefix_match */
-enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1 };
+enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1, SAE_PM_INTERVALS = 1u << 2 };
 
 /*
  * HOT 1 — batched strict prefix matching (Sec. 2.1: a later block is reusable
@@ -260,7 +274,16 @@ enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1 };
  * Every request sees the index as it was before the call.  SAE_PM_TOUCH sets
  * last_access = now and adds 1 to access_count for every (request, matched
  * block); SAE_PM_STATS adds every matched block to queue_hits[its queue]
- * (Algorithm 2).  Without both flags the call is read-only.
+ * (Algorithm 2) and, in a structural queue of an instance whose
+ * SAE_LEARN_DECAY_POWER bit is set, to the hits of its positional bin
+ * floor(8 o_b / o_max) (decay-power learner, App. B).
+ * SAE_PM_INTERVALS records Algorithm 4's reuse intervals: for every request
+ * and every log-normal queue among its matched blocks, dt = now - last_access
+ * of its deepest matched block of that queue, as it was before the call,
+ * if 1 <= dt < 2^31; a call's intervals join that queue's buffer in request
+ * order (the buffer keeps the newest SAE_IVL_CAP).  It needs matched_ids
+ * (the touch pass reads it) and n_req <= sae_config.max_requests.
+ * Without TOUCH, STATS and INTERVALS the call is read-only.
  */
 sae_status sae_prefix_match(sae_ctx *ctx, int32_t n_req, int32_t max_len, const uint64_t *hashes,
                             const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
@@ -317,9 +340,27 @@ enum { SAE_FB_FORCE = 1u << 0 };
  *  Algorithm 2 (queue weights): for each queue but the evict-first one with
  *    evictions > 5, alpha_q <- clamp(alpha_q + beta (1 + (hits/evictions)/T
  *    - alpha_q), 0.1, 3.0); then hits and evictions reset to 0.
+ *  Algorithm 4 (log-normal parameters): for each log-normal queue whose
+ *    interval buffer holds n > 20 intervals: with x = ln dt (the fp32 recipe's
+ *    ln), mu_s = mean x, sigma_s = population std of x (exact integer sums of
+ *    x * 2^24, then rounded in double and to fp32),
+ *    mu_q <- mu_q + beta_ln (mu_s - mu_q), sigma_q <- max(sigma_q +
+ *    beta_ln (sigma_s - sigma_q), 0.1); the buffer keeps its last 200.
+ *  Decay power (App. B): with rate_i = hits_i / (hits_i + missed_i) over the
+ *    bins that had events, front = mean rate of bins 0-3, back = of bins 4-7;
+ *    if there were more than 20 events, both halves had some and front > 0:
+ *    gamma <- clamp(gamma + beta (1 / (back / front + 0.1) - gamma), 0.3, 3.0)
+ *    and the bin counters restart.
  * Each algorithm runs only if its SAE_LEARN_* bit is set.
  */
 sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream);
+
+/* Algorithm 4's interval buffer of one (instance, log-normal queue), oldest
+ * first: out (host int32, cap entries) receives the first min(n, cap)
+ * intervals in ticks and *n (host) the number held.  Synchronizes `stream`.
+ * SAE_ERR_ARG for a queue that is not log-normal. */
+sae_status sae_get_intervals(sae_ctx *ctx, int32_t inst, int32_t queue, int32_t *out, int32_t cap, int32_t *n,
+                             sae_stream_t stream);
 
 /* OR of the device status bits since the last poll (then cleared);
  * synchronizes `stream`. */

@@ -36,7 +36,7 @@ Readings of points where the paper is silent (each listed in the design doc):
   log-normal queue.  A prefix match that records intervals adds, for every
   request and every log-normal queue among its matched blocks, the elapsed
   time now - last_access of its deepest matched block of that queue, as it was
-  before the call, when that is >= 1 tick; a call's intervals join the buffer
+  before the call, when 1 <= dt < 2^31 ticks; a call's intervals join the buffer
   in request order.  The buffer keeps at most IVL_CAP intervals (the oldest
   leave first).  An update needs more than 20 intervals and then keeps the
   last 200 (Algorithm 4); mean and std are the population moments of the fp32
@@ -48,7 +48,8 @@ Readings of points where the paper is silent (each listed in the design doc):
   of bins 4-7 (bins without events left out); gamma moves by the EMA factor
   beta toward 1 / (back / front + 0.1) and is clipped to [0.3, 3.0].  It needs
   more than 20 events, events in both halves and front > 0; its counters
-  restart after an update.
+  restart after an update.  They are gathered only while the learner is on
+  (the bin of an evicted block is always kept with its entry).
 """
 import math
 
@@ -306,7 +307,8 @@ class OracleCache:
         hashes found in the index.  All requests see the same snapshot; touches
         (last_access = now, access_count += 1 per request hit) apply afterwards.
         With stats, every hit block counts for queue_hits[queue(b)] and, in a
-        structural queue, for the hits of its positional bin.  With intervals,
+        structural queue with the decay-power learner on, for the hits of its
+        positional bin.  With intervals,
         each request records Algorithm 4's reuse interval of each log-normal
         queue it hit: now - last_access of its deepest matched block there."""
         hashes = np.asarray(hashes, np.uint64)
@@ -329,7 +331,7 @@ class OracleCache:
                 q = int(self.queue[b])
                 if stats:
                     self.hits[q] += 1
-                    if self.kind[q] == STRUCTURAL:
+                    if self.kind[q] == STRUCTURAL and self.prm.learn_gamma:
                         self.bin_hits[self.pos_bin(b)] += 1
                 if touch:
                     touched.append(b)
@@ -338,7 +340,7 @@ class OracleCache:
             if intervals:
                 for q in sorted(deepest):
                     dt = int(now) - int(self.la[deepest[q]])
-                    if dt >= 1:
+                    if 1 <= dt < 2 ** 31:
                         buf = self.ivl[q]
                         buf.append(dt)
                         if len(buf) > IVL_CAP:
@@ -373,7 +375,7 @@ class OracleCache:
             g = self.ghost.pop(h, None)
             if g is not None and self.ghost_live(g):
                 self.missed[g[0]] += 1
-                if self.kind[g[1]] == STRUCTURAL:
+                if self.kind[g[1]] == STRUCTURAL and self.prm.learn_gamma:
                     self.bin_missed[g[3]] += 1
         for i in range(len(ids)):
             if parent[i] >= 0:

@@ -11,6 +11,8 @@ LIB_PATH = os.path.join(HERE, "libsae.so")
 
 MAX_QUEUES = 8
 N_TYPES = 5
+N_BINS = 8
+IVL_CAP = 4096
 
 
 class SaeConfig(ctypes.Structure):
@@ -22,6 +24,7 @@ class SaeConfig(ctypes.Structure):
         ("max_k", ctypes.c_int32),
         ("ghost_window", ctypes.c_int32),
         ("index_log2", ctypes.c_int32),
+        ("max_requests", ctypes.c_int32),
     ]
 
 
@@ -35,6 +38,7 @@ class SaeParams(ctypes.Structure):
         ("eta", ctypes.c_float),
         ("temperature", ctypes.c_float),
         ("beta", ctypes.c_float),
+        ("beta_ln", ctypes.c_float),
         ("K", ctypes.c_int32),
         ("learn", ctypes.c_uint32),
     ]
@@ -49,6 +53,8 @@ class SaeCounters(ctypes.Structure):
         ("eviction_count", ctypes.c_int64),
         ("pending", ctypes.c_int32),
         ("n_updates", ctypes.c_int32),
+        ("bin_hits", ctypes.c_int32 * N_BINS),
+        ("bin_missed", ctypes.c_int32 * N_BINS),
     ]
 
 
@@ -82,6 +88,7 @@ SIGNATURES = {
     "sae_score_select": (_I32, [_P, _I32, _I32, _P, _U32, _P, _P, _P, _P, _P, _P]),
     "sae_feedback_update": (_I32, [_P, _U32, _P]),
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
+    "sae_get_intervals": (_I32, [_P, _I32, _I32, _P, _I32, ctypes.POINTER(_I32), _P]),
     "sae_select_stats": (_I32, [_P, _I32, _P, _P]),
     "sae_profile_enable": (_I32, [_P, _I32]),
     "sae_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),

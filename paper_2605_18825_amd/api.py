@@ -9,16 +9,16 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import SaeConfig, SaeCounters, SaeError, SaeParams, SaePool
+from ._lib import IVL_CAP, N_BINS, SaeConfig, SaeCounters, SaeError, SaeParams, SaePool  # noqa: F401
 
 KIND_EVICT_FIRST, KIND_STRUCTURAL, KIND_LOGNORMAL, KIND_RECENCY = 0, 1, 2, 3
 META_VALID, META_LEAF, META_REF = 0x40, 0x80, 0x100
-PM_TOUCH, PM_STATS = 1, 2
+PM_TOUCH, PM_STATS, PM_INTERVALS = 1, 2, 4
 SS_COMMIT, SS_ENGINE_SCAN, SS_ENGINE_BATCHED, SS_FORCE_FALLBACK = 1, 2, 4, 8
 FB_FORCE = 1
 HINT_DECODE, HINT_UNTEMPLATED, HINT_MULTI_TURN, HINT_AGENTIC, HINT_CONVERSATION, HINT_SHARED_PREFIX = 1, 2, 4, 8, 16, 32
 ROLE_EVICT, ROLE_STRUCT, ROLE_CHAT, ROLE_AGENT = 0, 1, 2, 3
-LEARN_TOKEN_WEIGHTS, LEARN_QUEUE_WEIGHTS = 1, 2
+LEARN_TOKEN_WEIGHTS, LEARN_QUEUE_WEIGHTS, LEARN_LOGNORMAL, LEARN_DECAY_POWER = 1, 2, 4, 8
 ST_NAMES = {1: "INDEX_FULL", 2: "GHOST_FULL", 4: "BAD_OFFSET", 8: "FUTURE_ACCESS",
             16: "SLOT_BUSY", 32: "SELECT_FALLBACK", 64: "BAD_BLOCK"}
 
@@ -78,7 +78,7 @@ def off_to_u32(off):
 
 
 # ----------------------------------------------------------------- the C ABI
-def sae_create(n_instances, blocks_per_instance, queue_kinds, max_k, ghost_window=0, index_log2=0):
+def sae_create(n_instances, blocks_per_instance, queue_kinds, max_k, ghost_window=0, index_log2=0, max_requests=0):
     L = _lib.load()
     cfg = SaeConfig()
     cfg.n_instances = n_instances
@@ -89,6 +89,7 @@ def sae_create(n_instances, blocks_per_instance, queue_kinds, max_k, ghost_windo
     cfg.max_k = max_k
     cfg.ghost_window = ghost_window
     cfg.index_log2 = index_log2
+    cfg.max_requests = max_requests
     out = ctypes.c_void_p()
     st = L.sae_create(ctypes.byref(cfg), ctypes.byref(out))
     if st != 0:
@@ -110,7 +111,7 @@ def sae_bind_pool(ctx, last_access, meta, off, hash, parent, child_count, ref_co
 
 
 def make_params(n_queues, w=1.0, alpha=1.0, mu=0.0, sigma=1.0, gamma=1.0, eta=0.01, temperature=1.0,
-                beta=0.1, K=32, learn=LEARN_TOKEN_WEIGHTS | LEARN_QUEUE_WEIGHTS):
+                beta=0.1, K=32, learn=LEARN_TOKEN_WEIGHTS | LEARN_QUEUE_WEIGHTS, beta_ln=0.1):
     p = SaeParams()
 
     def fill(arr, v, n):
@@ -124,7 +125,7 @@ def make_params(n_queues, w=1.0, alpha=1.0, mu=0.0, sigma=1.0, gamma=1.0, eta=0.
     for i in range(n_queues, 8):
         p.alpha[i] = 1.0
         p.sigma[i] = 1.0
-    p.gamma, p.eta, p.temperature, p.beta = gamma, eta, temperature, beta
+    p.gamma, p.eta, p.temperature, p.beta, p.beta_ln = gamma, eta, temperature, beta, beta_ln
     p.K, p.learn = int(K), int(learn)
     return p
 
@@ -221,6 +222,15 @@ def sae_profile_read(ctx):
     n = ctypes.c_int64()
     _check(ctx, _lib.load().sae_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n)))
     return ms.value, n.value
+
+
+def sae_get_intervals(ctx, inst, queue, cap=IVL_CAP, stream=None):
+    """Algorithm 4's interval buffer of (inst, queue), oldest first (host list)."""
+    buf = (ctypes.c_int32 * max(cap, 1))()
+    n = ctypes.c_int32()
+    _check(ctx, _lib.load().sae_get_intervals(ctx, inst, queue, ctypes.cast(buf, ctypes.c_void_p), cap,
+                                              ctypes.byref(n), _stream(stream)))
+    return list(buf[:min(n.value, cap)])
 
 
 def status_names(bits):

@@ -93,7 +93,7 @@ __device__ __forceinline__ int ghost_find(const GhostSlot *tab, uint32_t mask, c
         if (v == h) {
             uint32_t r = tab[s].ring;
             const GhostEntry &g = ring[r];
-            if (g.hash == h && !(g.tq & 0x100u) && ev_now - g.stamp < (long long)W) {
+            if (g.hash == h && !(g.tq & SAE_TQ_CONSUMED) && ev_now - g.stamp < (long long)W) {
                 *ring_pos = r;
                 return (int)s;
             }
@@ -192,6 +192,8 @@ __global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
         s.pending = 0;
         s.n_updates = 0;
         s.last_d = 0;
+        for (int b = 0; b < SAE_N_BINS; ++b) s.bin_hits[b] = s.bin_missed[b] = 0;
+        for (int q = 0; q < SAE_MAX_QUEUES; ++q) s.ivl_n[q] = s.ivl_start[q] = 0;
     }
 }
 
@@ -223,7 +225,7 @@ __global__ void k_ghost_fill(DevCtx c)
     int inst = (int)(i / c.ring_cap);
     uint32_t r = (uint32_t)(i - (long long)inst * c.ring_cap);
     GhostEntry g = c.ring[i];
-    if (g.hash == 0 || (g.tq & 0x100u)) return;
+    if (g.hash == 0 || (g.tq & SAE_TQ_CONSUMED)) return;
     if (c.state[inst].ev_count - g.stamp >= (long long)c.W) return;
     GhostSlot *tab = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
     if (!ghost_insert(tab, c.ghost_mask, g.hash, r)) set_status(c.status, SAE_ST_GHOST_FULL);
@@ -270,8 +272,13 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     int s = ghost_find(gt, c.ghost_mask, ring, h, c.state[inst].ev_count, c.W, &rp);
     if (s >= 0) {
         if (atomicCAS(&gt[s].hash, h, SAE_TOMB_HASH) == h) {
-            uint32_t old = atomicOr(&ring[rp].tq, 0x100u);
-            if (!(old & 0x100u)) atomicAdd(counter_slot(c, inst, i) + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
+            uint32_t old = atomicOr(&ring[rp].tq, SAE_TQ_CONSUMED);
+            if (!(old & SAE_TQ_CONSUMED)) {
+                int32_t *cs = counter_slot(c, inst, i);
+                atomicAdd(cs + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
+                if (((c.struct_mask >> ((old >> 3) & 7u)) & 1u) && (c.state[inst].learn & SAE_LEARN_DECAY_POWER))
+                    atomicAdd(cs + SAE_CF_BMISS + ((old >> SAE_TQ_BIN_SHIFT) & (SAE_N_BINS - 1)), 1);
+            }
         }
     }
 }
@@ -320,25 +327,40 @@ __global__ void k_ref_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *i
 // ---------------------------------------------------------------------------
 // Strict prefix matching, one wave per request.  Lanes probe 64 consecutive
 // hashes; the lowest missing lane ends the match and no later chunk is probed.
-// queue_hits are summed per workgroup in LDS (when its requests share an
-// instance) and added into one striped counter copy.
+// queue_hits (and the positional-bin hits of structural blocks) are summed per
+// workgroup in LDS (when its requests share an instance) and added into one
+// striped counter copy.
+// With SAE_PM_INTERVALS the request also finds, per log-normal queue, its
+// deepest matched block and stores now - last_access of it (Algorithm 4's
+// reuse interval, 0 when none) in pm_rec[r]; no block is touched here, so
+// every last_access read is the one from before the call, and k_pm_place
+// touches afterwards.
 __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, int max_len, const uint64_t *hashes,
                                                           const int32_t *lens, const int32_t *inst_a, int32_t now,
                                                           uint32_t flags, int32_t *match_len, int32_t *matched_ids)
 {
+    constexpr int NC = SAE_MAX_QUEUES + SAE_N_BINS;
     __shared__ int32_t winst[kThreads / SAE_WAVE];
-    __shared__ uint32_t wg_hits[SAE_MAX_QUEUES];
+    __shared__ uint32_t wg_hits[NC];
     const int lane = (int)__lane_id();
     const int wave = threadIdx.x / SAE_WAVE;
     const int r = (blockIdx.x * blockDim.x + threadIdx.x) / SAE_WAVE;
     const bool active = r < n_req;
+    const bool intervals = (flags & SAE_PM_INTERVALS) != 0;
+    const bool touch = (flags & SAE_PM_TOUCH) && !intervals;
     int inst = (active && inst_a) ? inst_a[r] : 0;
     const bool inst_ok = inst >= 0 && inst < c.n_inst;
-    if (threadIdx.x < SAE_MAX_QUEUES) wg_hits[threadIdx.x] = 0;
+    // positional-bin hits are gathered only while the decay-power learner is on
+    const bool bins = (flags & SAE_PM_STATS) && c.struct_mask && active && inst_ok &&
+                      (c.state[inst].learn & SAE_LEARN_DECAY_POWER);
+    if (threadIdx.x < NC) wg_hits[threadIdx.x] = 0;
     if (lane == 0) winst[wave] = (active && inst_ok) ? inst : -1;
-    uint32_t qcount[SAE_MAX_QUEUES];
+    uint32_t qcount[NC];
 #pragma unroll
-    for (int q = 0; q < SAE_MAX_QUEUES; ++q) qcount[q] = 0;
+    for (int q = 0; q < NC; ++q) qcount[q] = 0;
+    int32_t deep[SAE_MAX_QUEUES];  // deepest matched block per log-normal queue (-1: none)
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) deep[q] = -1;
     if (active) {
         int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
         int len = lens[r];
@@ -366,10 +388,13 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                 const int lim = min(first, len - j0);
                 const bool hit = lane < lim;
                 int q = 0;
+                uint32_t bin = 0;
                 if (hit) {
                     const long long g = base + id;
+                    const uint32_t off = bins ? c.off[g] : 0u;  // loaded beside meta, not after it
                     q = meta_queue(c.meta[g]);
-                    if (flags & SAE_PM_TOUCH) {
+                    if (bins && ((c.struct_mask >> q) & 1u)) bin = pos_bin(off);
+                    if (touch) {
                         c.la[g] = now;
                         atomicAdd(&c.access_count[g], 1);
                     }
@@ -381,6 +406,20 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
 #pragma unroll
                     for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
                         qcount[qq] += (uint32_t)__popcll(__ballot(hit && q == qq));
+                    if (bins) {
+                        const bool sh = hit && ((c.struct_mask >> q) & 1u);
+#pragma unroll
+                        for (int bb = 0; bb < SAE_N_BINS; ++bb)
+                            qcount[SAE_MAX_QUEUES + bb] += (uint32_t)__popcll(__ballot(sh && bin == (uint32_t)bb));
+                    }
+                }
+                if (intervals) {
+#pragma unroll
+                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+                        if (!((c.ln_mask >> qq) & 1u)) continue;
+                        const unsigned long long bm = __ballot(hit && q == qq);
+                        if (bm) deep[qq] = __shfl(id, 63 - __clzll((long long)bm));
+                    }
                 }
                 m = j0 + lim;
                 if (mm) {
@@ -391,7 +430,20 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
             if (mid)
                 for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
             if (lane == 0) match_len[r] = m;
+            if (intervals && lane < SAE_MAX_QUEUES) {
+                int32_t b = -1;
+#pragma unroll
+                for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
+                    if (lane == qq) b = deep[qq];
+                int32_t rec = 0;
+                if (b >= 0) {
+                    const long long dt = (long long)now - (long long)c.la[base + b];
+                    if (dt >= 1 && dt <= 0x7FFFFFFFll) rec = (int32_t)dt;
+                }
+                c.pm_rec[(long long)r * SAE_MAX_QUEUES + lane] = rec;
+            }
         }
+        if (intervals && !inst_ok && lane < SAE_MAX_QUEUES) c.pm_rec[(long long)r * SAE_MAX_QUEUES + lane] = 0;
     }
     __syncthreads();
     if (!(flags & SAE_PM_STATS)) return;
@@ -407,14 +459,102 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
     if (i0 < 0) return;
     if (uniform) {
         if (lane == 0 && active && inst_ok)
-            for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
+            for (int qq = 0; qq < NC; ++qq)
                 if (qcount[qq]) atomicAdd(&wg_hits[qq], qcount[qq]);
         __syncthreads();
-        if (threadIdx.x < c.Q && wg_hits[threadIdx.x])
-            atomicAdd(counter_slot(c, i0, blockIdx.x) + SAE_CF_HITS + threadIdx.x, (int)wg_hits[threadIdx.x]);
+        const int f = threadIdx.x;
+        if (f < NC && wg_hits[f] && (f >= SAE_MAX_QUEUES || f < c.Q)) {
+            const int field = f < SAE_MAX_QUEUES ? SAE_CF_HITS + f : SAE_CF_BHITS + (f - SAE_MAX_QUEUES);
+            atomicAdd(counter_slot(c, i0, blockIdx.x) + field, (int)wg_hits[f]);
+        }
     } else if (lane == 0 && active && inst_ok) {
+        int32_t *cs = counter_slot(c, inst, blockIdx.x);
         for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
-            if (qq < c.Q && qcount[qq]) atomicAdd(counter_slot(c, inst, blockIdx.x) + SAE_CF_HITS + qq, (int)qcount[qq]);
+            if (qq < c.Q && qcount[qq]) atomicAdd(cs + SAE_CF_HITS + qq, (int)qcount[qq]);
+        for (int bb = 0; bb < SAE_N_BINS; ++bb)
+            if (qcount[SAE_MAX_QUEUES + bb]) atomicAdd(cs + SAE_CF_BHITS + bb, (int)qcount[SAE_MAX_QUEUES + bb]);
+    }
+}
+
+// Second pass of a prefix match with SAE_PM_INTERVALS.  Workgroups
+// 0 .. n_inst-1 append instance i's intervals to its rings in request order
+// (an exclusive scan over the requests, per log-normal queue; only the newest
+// SAE_IVL_CAP of the call are written); the other workgroups touch every
+// matched block (SAE_PM_TOUCH).  Neither reads what the other writes.
+__global__ void __launch_bounds__(kThreads) k_pm_place(DevCtx c, int n_req, int max_len, const int32_t *inst_a,
+                                                      int32_t now, uint32_t flags, const int32_t *matched_ids)
+{
+    __shared__ uint32_t wsum[kThreads / SAE_WAVE];
+    __shared__ uint32_t tot;
+    const int lane = (int)__lane_id();
+    const int wave = threadIdx.x / SAE_WAVE;
+    if ((int)blockIdx.x >= c.n_inst) {
+        if (!(flags & SAE_PM_TOUCH)) return;
+        const long long total = (long long)n_req * max_len;
+        const long long stride = (long long)(gridDim.x - c.n_inst) * kThreads;
+        for (long long e = (long long)(blockIdx.x - c.n_inst) * kThreads + threadIdx.x; e < total; e += stride) {
+            const int32_t id = matched_ids[e];
+            if (id < 0) continue;
+            const int r = (int)(e / max_len);
+            const int inst = inst_a ? inst_a[r] : 0;
+            const long long g = (long long)inst * c.N + id;
+            c.la[g] = now;
+            atomicAdd(&c.access_count[g], 1);
+        }
+        return;
+    }
+    const int i = blockIdx.x;
+    InstState &s = c.state[i];
+    int32_t *ring_base = c.ivl + (long long)i * c.Q * SAE_IVL_CAP;
+    for (int q = 0; q < c.Q; ++q) {
+        if (!((c.ln_mask >> q) & 1u)) continue;
+        // pass 1: intervals of this call for (i, q)
+        uint32_t cnt = 0;
+        for (int r = threadIdx.x; r < n_req; r += kThreads) {
+            const int ri = inst_a ? inst_a[r] : 0;
+            cnt += (ri == i && c.pm_rec[(long long)r * SAE_MAX_QUEUES + q] > 0) ? 1u : 0u;
+        }
+        for (int o = SAE_WAVE / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+        if (lane == 0) wsum[wave] = cnt;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t t = 0;
+            for (int w = 0; w < kThreads / SAE_WAVE; ++w) t += wsum[w];
+            tot = t;
+        }
+        __syncthreads();
+        const long long total = tot;
+        const long long n0 = s.ivl_n[q];
+        const long long keep_from = total - SAE_IVL_CAP;  // call-local ranks below this are overwritten anyway
+        int32_t *ring = ring_base + (long long)q * SAE_IVL_CAP;
+        // pass 2: request-order ranks by a workgroup scan per chunk
+        long long run = 0;
+        for (int base = 0; base < n_req; base += kThreads) {
+            const int r = base + threadIdx.x;
+            int32_t v = 0;
+            if (r < n_req) {
+                const int ri = inst_a ? inst_a[r] : 0;
+                if (ri == i) v = c.pm_rec[(long long)r * SAE_MAX_QUEUES + q];
+            }
+            const bool f = v > 0;
+            const unsigned long long bm = __ballot(f);
+            const uint32_t below = (uint32_t)__popcll(bm & ((1ull << lane) - 1ull));
+            __syncthreads();  // wsum of the previous chunk has been read
+            if (lane == 0) wsum[wave] = (uint32_t)__popcll(bm);
+            __syncthreads();
+            uint32_t before = 0, chunk = 0;
+            for (int w = 0; w < kThreads / SAE_WAVE; ++w) {
+                const uint32_t x = wsum[w];
+                before += (w < wave) ? x : 0u;
+                chunk += x;
+            }
+            const long long rank = run + before + below;
+            if (f && rank >= keep_from) ring[(n0 + rank) % SAE_IVL_CAP] = v;
+            run += chunk;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) s.ivl_n[q] = n0 + total;
+        __syncthreads();
     }
 }
 
@@ -457,7 +597,8 @@ __global__ void k_commit(DevCtx c, const int32_t *decision)
         GhostEntry e;
         e.hash = h;
         e.stamp = s.ev_before + d;
-        e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3);
+        e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
+               (pos_bin(c.off[g]) << SAE_TQ_BIN_SHIFT);
         e.pad_ = 0;
         ring[rp] = e;
         if (!ghost_insert(gt, c.ghost_mask, h, rp)) set_status(c.status, SAE_ST_GHOST_FULL);
@@ -571,6 +712,12 @@ hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, 
     long long threads = (long long)n_req * SAE_WAVE;
     hipLaunchKernelGGL(k_prefix_match, dim3(grid_for(threads)), dim3(kThreads), 0, s, c, n_req, max_len, hashes, lens,
                        inst, now, flags, match_len, matched_ids);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !(flags & SAE_PM_INTERVALS)) return e;
+    long long tg = (flags & SAE_PM_TOUCH) ? (long long)grid_for((long long)n_req * max_len) : 0;
+    if (tg > 2048) tg = 2048;
+    hipLaunchKernelGGL(k_pm_place, dim3((unsigned)(c.n_inst + tg)), dim3(kThreads), 0, s, c, n_req, max_len, inst,
+                       now, flags, (const int32_t *)matched_ids);
     return hipGetLastError();
 }
 

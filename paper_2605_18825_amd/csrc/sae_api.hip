@@ -81,6 +81,7 @@ void default_params(InstState &s, int max_k)
     s.eta = 0.01f;
     s.T = 1.0f;
     s.beta = 0.1f;
+    s.beta_ln = 0.1f;
     s.K = max_k;
     s.learn = SAE_LEARN_TOKEN_WEIGHTS | SAE_LEARN_QUEUE_WEIGHTS;
 }
@@ -123,6 +124,8 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     if (k.max_k < 1 || k.max_k > 8192) return fail(nullptr, SAE_ERR_ARG, "max_k must be in 1..8192");
     if (k.ghost_window < 0) return fail(nullptr, SAE_ERR_ARG, "ghost_window must be >= 0");
     if (k.index_log2 < 0 || k.index_log2 > 30) return fail(nullptr, SAE_ERR_ARG, "index_log2 must be in 0..30");
+    if (k.max_requests < 0 || k.max_requests > (1 << 24))
+        return fail(nullptr, SAE_ERR_ARG, "max_requests must be in 0..2^24");
     int n_ef = 0;
     for (int q = 0; q < k.n_queues; ++q) {
         if (k.queue_kind[q] < SAE_KIND_EVICT_FIRST || k.queue_kind[q] > SAE_KIND_RECENCY)
@@ -142,8 +145,12 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     d.max_k = k.max_k;
     d.ef_queue = -1;
     for (int q = 0; q < SAE_MAX_QUEUES; ++q) d.kind[q] = (q < k.n_queues) ? k.queue_kind[q] : SAE_KIND_RECENCY;
-    for (int q = 0; q < k.n_queues; ++q)
+    for (int q = 0; q < k.n_queues; ++q) {
         if (k.queue_kind[q] == SAE_KIND_EVICT_FIRST) d.ef_queue = q;
+        if (k.queue_kind[q] == SAE_KIND_LOGNORMAL) d.ln_mask |= 1u << q;
+        if (k.queue_kind[q] == SAE_KIND_STRUCTURAL) d.struct_mask |= 1u << q;
+    }
+    d.max_req = k.max_requests;
     d.W = k.ghost_window ? k.ghost_window : k.blocks_per_instance;
     d.ring_cap = d.W + d.max_k;
     int il = k.index_log2 ? k.index_log2 : log2_ceil(2ll * d.N);
@@ -182,7 +189,9 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
               dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&
               dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
-              dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N);
+              dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N) &&
+              dev_alloc(c, &d.ivl, d.ln_mask ? I * Q * SAE_IVL_CAP : 0) &&
+              dev_alloc(c, &d.pm_rec, (long long)d.max_req * SAE_MAX_QUEUES);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);
         delete c;
@@ -260,6 +269,7 @@ sae_status sae_set_params(sae_ctx *c, int32_t inst, const sae_params *p, sae_str
     h.eta = p->eta;
     h.T = p->temperature;
     h.beta = p->beta;
+    h.beta_ln = p->beta_ln;
     h.K = p->K;
     h.learn = p->learn;
     const size_t nbytes = offsetof(InstState, evicted);
@@ -289,6 +299,7 @@ sae_status sae_get_params(sae_ctx *c, int32_t inst, sae_params *out, sae_stream_
     out->eta = h.eta;
     out->temperature = h.T;
     out->beta = h.beta;
+    out->beta_ln = h.beta_ln;
     out->K = h.K;
     out->learn = h.learn;
     return SAE_OK;
@@ -310,6 +321,8 @@ sae_status sae_get_counters(sae_ctx *c, int32_t inst, sae_counters *out, sae_str
     out->eviction_count = h.ev_count;
     out->pending = h.pending;
     out->n_updates = h.n_updates;
+    memcpy(out->bin_hits, h.bin_hits, sizeof(out->bin_hits));
+    memcpy(out->bin_missed, h.bin_missed, sizeof(out->bin_missed));
     return SAE_OK;
 }
 
@@ -329,9 +342,41 @@ sae_status sae_set_counters(sae_ctx *c, int32_t inst, const sae_counters *in, sa
     h.ev_count = in->eviction_count;
     h.pending = in->pending;
     h.n_updates = in->n_updates;
+    memcpy(h.bin_hits, in->bin_hits, sizeof(h.bin_hits));
+    memcpy(h.bin_missed, in->bin_missed, sizeof(h.bin_missed));
     e = hipMemcpyAsync(c->dc.state + inst, &h, sizeof(h), hipMemcpyHostToDevice, S(stream));
     if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_set_counters write");
+    return SAE_OK;
+}
+
+sae_status sae_get_intervals(sae_ctx *c, int32_t inst, int32_t queue, int32_t *out, int32_t cap, int32_t *n,
+                             sae_stream_t stream)
+{
+    if (!c || !n || cap < 0 || (cap > 0 && !out)) return fail(c, SAE_ERR_ARG, "ctx, n (and out if cap > 0) needed");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    if (queue < 0 || queue >= c->dc.Q || c->dc.kind[queue] != SAE_KIND_LOGNORMAL)
+        return fail(c, SAE_ERR_ARG, "queue is not a log-normal queue");
+    InstState h;
+    hipError_t e = hipMemcpyAsync(&h, c->dc.state + inst, sizeof(h), hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_get_intervals");
+    const long long total = h.ivl_n[queue];
+    long long lo = total - SAE_IVL_CAP;
+    if (lo < h.ivl_start[queue]) lo = h.ivl_start[queue];
+    const long long cnt = total - lo;
+    *n = (int32_t)cnt;
+    const long long want = cnt < cap ? cnt : cap;
+    const int32_t *ring = c->dc.ivl + ((long long)inst * c->dc.Q + queue) * SAE_IVL_CAP;
+    for (long long done = 0; done < want && e == hipSuccess;) {
+        const long long pos = (lo + done) % SAE_IVL_CAP;
+        long long len = SAE_IVL_CAP - pos;
+        if (len > want - done) len = want - done;
+        e = hipMemcpyAsync(out + done, ring + pos, (size_t)len * sizeof(int32_t), hipMemcpyDeviceToHost, S(stream));
+        done += len;
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_get_intervals copy");
     return SAE_OK;
 }
 
@@ -419,10 +464,15 @@ sae_status sae_prefix_match(sae_ctx *c, int32_t n_req, int32_t max_len, const ui
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
     if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
     if (n_req < 0 || max_len < 0) return fail(c, SAE_ERR_ARG, "n_req and max_len must be >= 0");
-    if (flags & ~(uint32_t)(SAE_PM_TOUCH | SAE_PM_STATS)) return fail(c, SAE_ERR_ARG, "unknown prefix-match flag");
+    if (flags & ~(uint32_t)(SAE_PM_TOUCH | SAE_PM_STATS | SAE_PM_INTERVALS))
+        return fail(c, SAE_ERR_ARG, "unknown prefix-match flag");
     if (n_req == 0) return SAE_OK;
     if (max_len < 1 || !hashes || !lens || !match_len)
         return fail(c, SAE_ERR_ARG, "hashes, lens, match_len must be non-NULL and max_len >= 1");
+    if (flags & SAE_PM_INTERVALS) {
+        if (!matched_ids) return fail(c, SAE_ERR_ARG, "SAE_PM_INTERVALS needs matched_ids");
+        if (n_req > c->dc.max_req) return fail(c, SAE_ERR_ARG, "SAE_PM_INTERVALS: n_req exceeds max_requests");
+    }
     if ((long long)n_req * SAE_WAVE > 0x7FFFFFFFll) return fail(c, SAE_ERR_ARG, "n_req too large");
     hipError_t e = launch_prefix_match(c->dc, n_req, max_len, hashes, lens, inst, now, flags, match_len,
                                        matched_ids, S(stream));

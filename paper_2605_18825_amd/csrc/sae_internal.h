@@ -36,8 +36,14 @@
 #define SAE_CF_MISSED 5      // 5 fields, token_stats[tau].miss_after_evict
 #define SAE_CF_HITS 10       // 8 fields, queue_hits[q]
 #define SAE_CF_EVICTIONS 18  // 8 fields, queue_evictions[q]
-#define SAE_CF_N 26
-#define SAE_CF_STRIDE 32
+#define SAE_CF_BHITS 26      // 8 fields, hits of structural blocks per positional bin
+#define SAE_CF_BMISS 34      // 8 fields, misses after eviction per positional bin
+#define SAE_CF_N 42
+#define SAE_CF_STRIDE 64
+
+// recently_evicted entry bits: tau | queue << 3 | consumed | positional bin << 9
+#define SAE_TQ_CONSUMED 0x100u
+#define SAE_TQ_BIN_SHIFT 9
 
 // ----------------------------------------------------------------------------
 // Per-instance device state: learned parameters, learner settings and the
@@ -47,7 +53,7 @@ struct InstState {
     float alpha[SAE_MAX_QUEUES];
     float mu[SAE_MAX_QUEUES];
     float sigma[SAE_MAX_QUEUES];
-    float gamma, eta, T, beta;
+    float gamma, eta, T, beta, beta_ln;
     int32_t K;
     uint32_t learn;
     int32_t evicted[SAE_N_TYPES];
@@ -59,7 +65,10 @@ struct InstState {
     int32_t pending;      // learners due
     int32_t n_updates;
     int32_t last_d;       // size of the last committed decision
-    int32_t pad_;
+    int32_t bin_hits[SAE_N_BINS];    // decay-power learner counters
+    int32_t bin_missed[SAE_N_BINS];
+    long long ivl_n[SAE_MAX_QUEUES];      // Algorithm 4: intervals recorded so far, per queue
+    long long ivl_start[SAE_MAX_QUEUES];  // first interval still in the buffer (before the cap)
 };
 
 // Open-addressing slot of the block index: content hash -> block id.
@@ -129,7 +138,22 @@ struct DevCtx {
     int32_t *cpart;            // [n_inst][SAE_CSLOTS][SAE_CF_STRIDE] feedback counters, striped
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
     int32_t *sel_count;        // [n_inst][Q]
+    int32_t *ivl;              // [n_inst][Q][SAE_IVL_CAP] Algorithm 4 interval rings (dt in ticks)
+    int32_t *pm_rec;           // [max_requests][SAE_MAX_QUEUES] intervals of one prefix-match call
+    int32_t max_req;
+    uint32_t ln_mask;          // bit q: queue q is log-normal
+    uint32_t struct_mask;      // bit q: queue q is structural
 };
+
+// Positional bin of a block (decay-power learner): floor(8 o_b / o_max) with
+// o_b capped at o_max, 7 at the end, 0 for a one-block template (o_max = 0).
+__device__ __forceinline__ uint32_t pos_bin(uint32_t off)
+{
+    const uint32_t ob = off & 0xFFFFu, omax = off >> 16;
+    if (omax == 0) return 0;
+    const uint32_t b = (SAE_N_BINS * (ob < omax ? ob : omax)) / omax;
+    return b < SAE_N_BINS - 1 ? b : SAE_N_BINS - 1;
+}
 
 // ----------------------------------------------------------------------------
 // Meta field access.

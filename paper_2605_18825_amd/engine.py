@@ -22,7 +22,9 @@ class DeviceBackend:
         self.n_inst, self.N, self.Q = n_inst, capacity, len(kinds)
         self.roles = list(roles)
         self.max_k = max_k
-        self.ctx = api.sae_create(n_inst, capacity, kinds, max_k=max_k, ghost_window=ghost_window)
+        self.intervals = bool(learn & api.LEARN_LOGNORMAL)
+        self.ctx = api.sae_create(n_inst, capacity, kinds, max_k=max_k, ghost_window=ghost_window,
+                                  max_requests=n_inst if self.intervals else 0)
         self.pool = DevicePool(n_inst, capacity)
         self.pool.bind(self.ctx)
         api.sae_index_build(self.ctx)
@@ -46,8 +48,9 @@ class DeviceBackend:
             lens[j] = len(p)
         ml = torch.zeros(n, dtype=torch.int32, device="cuda")
         mid = torch.empty((n, L), dtype=torch.int32, device="cuda")
+        flags = api.PM_TOUCH | api.PM_STATS | (api.PM_INTERVALS if self.intervals else 0)
         api.sae_prefix_match(self.ctx, _dev(h.view(np.int64), torch.int64), _dev(lens, torch.int32), now,
-                             api.PM_TOUCH | api.PM_STATS, ml, matched_ids=mid, inst=_dev(insts, torch.int32))
+                             flags, ml, matched_ids=mid, inst=_dev(insts, torch.int32))
         ml = ml.cpu().numpy()
         mid = mid.cpu().numpy()
         return ml, [mid[j, :ml[j]] for j in range(n)]
@@ -87,11 +90,16 @@ class DeviceBackend:
         c = api.sae_get_counters(self.ctx, i)
         return dict(evicted=list(c.evicted), missed=list(c.missed), hits=list(c.hits[:self.Q]),
                     evictions=list(c.evictions[:self.Q]), ev_count=int(c.eviction_count), pending=bool(c.pending),
-                    n_updates=int(c.n_updates))
+                    n_updates=int(c.n_updates), bin_hits=list(c.bin_hits), bin_missed=list(c.bin_missed))
 
     def params(self, i):
         p = api.sae_get_params(self.ctx, i)
         return np.array(p.w[:5], np.float32), np.array(p.alpha[:self.Q], np.float32)
+
+    def timing_params(self, i):
+        """mu, sigma per queue and gamma of instance i."""
+        p = api.sae_get_params(self.ctx, i)
+        return np.array(p.mu[:self.Q], np.float32), np.array(p.sigma[:self.Q], np.float32), np.float32(p.gamma)
 
     def status(self):
         return api.status_names(api.sae_poll_status(self.ctx))

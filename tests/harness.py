@@ -26,7 +26,7 @@ class Pair:
     """One instance held by both the oracle and a libsae context."""
 
     def __init__(self, kinds, pool, max_k, mu=None, sigma=None, gamma=1.0, w=1.0, alpha=1.0, K=None,
-                 ghost_window=0, learn=3, eta=0.01, T=1.0, beta=0.1):
+                 ghost_window=0, learn=3, eta=0.01, T=1.0, beta=0.1, beta_ln=0.1, max_requests=0):
         N = pool["n_blocks"]
         Q = len(kinds)
         self.N, self.Q, self.max_k, self.kinds = N, Q, max_k, list(kinds)
@@ -34,12 +34,13 @@ class Pair:
         sigma = [1.0] * Q if sigma is None else list(sigma)
         K = max_k if K is None else K
         self.prm = oracle.Params(Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma, eta=eta, T=T, beta=beta, K=K,
-                                 learn_w=bool(learn & 1), learn_alpha=bool(learn & 2))
+                                 learn_w=bool(learn & 1), learn_alpha=bool(learn & 2), beta_ln=beta_ln,
+                                 learn_ln=bool(learn & 4), learn_gamma=bool(learn & 8))
         self.oc = oracle.OracleCache(N, kinds, self.prm, ghost_window=ghost_window or None)
         self.tau_oracle = oracle.block_type(pool["counts"])
         self.oc.bind(pool["last_access"], pool["queue"], self.tau_oracle, pool["ntok"], pool["ob"], pool["omax"],
                      pool["valid"], pool["ref_count"], pool["parent"], pool["hash"], pool.get("access_count"))
-        self.ctx = api.sae_create(1, N, kinds, max_k=max_k, ghost_window=ghost_window)
+        self.ctx = api.sae_create(1, N, kinds, max_k=max_k, ghost_window=ghost_window, max_requests=max_requests)
         self.dp = DevicePool(1, N)
         self.tau_gpu = self.dp.fill_instance(0, pool)
         self.dp.bind(self.ctx)
@@ -47,7 +48,8 @@ class Pair:
         wv = list(w) if hasattr(w, "__len__") else w
         av = list(alpha) if hasattr(alpha, "__len__") else alpha
         api.sae_set_params(self.ctx, -1, api.make_params(Q, w=wv, alpha=av, mu=mu, sigma=sigma, gamma=gamma, eta=eta,
-                                                         temperature=T, beta=beta, K=K, learn=learn))
+                                                         temperature=T, beta=beta, K=K, learn=learn,
+                                                         beta_ln=beta_ln))
         self.out = SelectBuffers(1, Q, max_k)
 
     def close(self):
@@ -92,7 +94,7 @@ class Pair:
         mid = torch.zeros(R.shape, dtype=torch.int32, device="cuda")
         api.sae_prefix_match(self.ctx, R, L, now, flags, ml, matched_ids=mid)
         om, omid = self.oc.prefix_match(hashes, lens, now, touch=bool(flags & api.PM_TOUCH),
-                                        stats=bool(flags & api.PM_STATS))
+                                        stats=bool(flags & api.PM_STATS), intervals=bool(flags & api.PM_INTERVALS))
         if check:
             torch.cuda.synchronize()
             g = ml.cpu().numpy()
@@ -128,6 +130,22 @@ class Pair:
         ga = np.array(gp.alpha[:self.Q], np.float32)
         assert np.array_equal(gw.view(np.uint32), self.prm.w.view(np.uint32)), "w: %s vs %s" % (gw, self.prm.w)
         assert np.array_equal(ga.view(np.uint32), self.prm.alpha.view(np.uint32)), "alpha: %s vs %s" % (ga, self.prm.alpha)
+        gm = np.array(gp.mu[:self.Q], np.float32)
+        gs = np.array(gp.sigma[:self.Q], np.float32)
+        assert np.array_equal(gm.view(np.uint32), self.prm.mu.view(np.uint32)), "mu: %s vs %s" % (gm, self.prm.mu)
+        assert np.array_equal(gs.view(np.uint32), self.prm.sigma.view(np.uint32)), \
+            "sigma: %s vs %s" % (gs, self.prm.sigma)
+        gg = np.float32(gp.gamma)
+        assert gg.view(np.uint32) == np.float32(self.prm.gamma).view(np.uint32), \
+            "gamma: %r vs %r" % (gg, self.prm.gamma)
+
+    def check_intervals(self):
+        for q in range(self.Q):
+            if self.kinds[q] == api.KIND_LOGNORMAL:
+                got = api.sae_get_intervals(self.ctx, 0, q)
+                want = self.oc.ivl[q]
+                assert got == want, "queue %d intervals: %d held vs oracle %d; first %s vs %s" % (
+                    q, len(got), len(want), got[:5], want[:5])
 
     def check_counters(self):
         c = api.sae_get_counters(self.ctx, 0)
@@ -138,6 +156,8 @@ class Pair:
         assert list(c.evictions[:self.Q]) == o.evictions, ("evictions", list(c.evictions[:self.Q]), o.evictions)
         assert c.eviction_count == o.ev_count
         assert bool(c.pending) == o.pending
+        assert list(c.bin_hits) == o.bin_hits, ("bin_hits", list(c.bin_hits), o.bin_hits)
+        assert list(c.bin_missed) == o.bin_missed, ("bin_missed", list(c.bin_missed), o.bin_missed)
 
     def check_pool(self):
         torch.cuda.synchronize()

@@ -9,19 +9,22 @@ class OracleBackend:
     def __init__(self, insts, capacity, kinds, roles, mu, sigma, K, learn, w=1.0, alpha=1.0, gamma=1.0, eta=0.01,
                  T=1.0, beta=0.1, ghost_window=None):
         self.insts = list(insts)
+        self.intervals = bool(learn & 4)
         self.roles = list(roles)
         self.Q = len(kinds)
         self.c = {}
         for i in self.insts:
             prm = oracle.Params(self.Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma, eta=eta, T=T, beta=beta,
-                                K=K, learn_w=bool(learn & 1), learn_alpha=bool(learn & 2))
+                                K=K, learn_w=bool(learn & 1), learn_alpha=bool(learn & 2), learn_ln=bool(learn & 4),
+                                learn_gamma=bool(learn & 8))
             self.c[i] = oracle.OracleCache(capacity, kinds, prm, ghost_window=ghost_window)
 
     def prefix_match(self, now, insts, prompts):
         ml = np.zeros(len(insts), np.int32)
         mids = []
         for j, (i, p) in enumerate(zip(insts, prompts)):
-            m, ids = self.c[i].prefix_match(np.asarray(p, np.uint64)[None, :], [len(p)], now, touch=True, stats=True)
+            m, ids = self.c[i].prefix_match(np.asarray(p, np.uint64)[None, :], [len(p)], now, touch=True, stats=True,
+                                            intervals=self.intervals)
             ml[j] = m[0]
             mids.append(ids[0, :m[0]].astype(np.int32))
         return ml, mids
@@ -67,3 +70,7 @@ class OracleBackend:
     def params(self, i):
         p = self.c[i].prm
         return p.w.copy(), p.alpha.copy()
+
+    def timing_params(self, i):
+        p = self.c[i].prm
+        return p.mu.copy(), p.sigma.copy(), np.float32(p.gamma)

@@ -63,6 +63,10 @@ def test_create_rejects_bad_config_without_gpu(lib):
     assert L.sae_create(ctypes.byref(cfg), ctypes.byref(out)) == -1
     assert b"evict-first" in L.sae_last_error(None)
     cfg.queue_kind[1] = 2
+    cfg.max_requests = -1
+    assert L.sae_create(ctypes.byref(cfg), ctypes.byref(out)) == -1
+    assert b"max_requests" in L.sae_last_error(None)
+    cfg.max_requests = 0
     cfg.max_k = 0
     assert L.sae_create(ctypes.byref(cfg), ctypes.byref(out)) == -1
 
@@ -73,3 +77,5 @@ def test_hot_calls_reject_null_context(lib):
     assert L.sae_score_select(None, 0, 1, None, 0, None, None, None, None, None, None) == -1
     assert L.sae_prefix_match(None, 1, 1, None, None, None, 0, 0, None, None, None) == -1
     assert L.sae_feedback_update(None, 0, None) == -1
+    n = ctypes.c_int32()
+    assert L.sae_get_intervals(None, 0, 0, None, 0, ctypes.byref(n), None) == -1

@@ -25,6 +25,21 @@ def test_trace_balanced_fixed_weights():
     assert rd.summary()["evicted"] > 0
 
 
+def test_trace_balanced_all_learners():
+    """Algorithms 2, 3 and 4 and the decay-power learner together: every
+    step's matches and decisions, and mu / sigma / gamma, agree bit for bit."""
+    rd, ro, _ = run_pair("trace_balanced", 1200, [0], learn=15, check_every=200)
+    o = ro.be.c[0]
+    assert o.n_updates > 0 and len(o.ivl[2]) + len(o.ivl[3]) > 0
+
+
+def test_batched_sweep_all_learners():
+    """Interval placement across 256 instances of one context."""
+    rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], learn=15, check_every=300)
+    assert rd.summary()["evicted"] > 0
+    assert all(len(ro.be.c[i].ivl[2]) + len(ro.be.c[i].ivl[3]) > 0 for i in (5, 200))
+
+
 def test_batched_sweep_sampled_instances():
     rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], check_every=150)
     s = rd.summary()

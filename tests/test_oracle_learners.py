@@ -273,3 +273,14 @@ def test_decay_power_counts_structural_hits_and_misses():
         c.insert([b], [h[b]], [b - 1], [20], [queue[b]], [0], [16], [ob[b]], [omax[b]])
     assert c.bin_missed == [0, 0, 0, 0, 0, 0, 0, 2]
     assert c.missed[0] == 3
+
+
+def test_bins_only_while_the_learner_is_on():
+    c = _ln_cache(n=16, kinds=(STRUCTURAL, RECENCY), learn_ln=False, learn_gamma=False)
+    h = _bind_chains(c, [list(range(8))], np.zeros(16, np.int32), np.zeros(16, np.int32),
+                     np.arange(16, dtype=np.int32), np.full(16, 7, np.int32))
+    c.prefix_match(h[None, :8], [8], now=10)
+    assert c.bin_hits == [0] * N_BINS and sum(c.hits) == 8
+    c.commit(np.array([7], np.int32))
+    c.insert([7], [h[7]], [6], [20], [0], [0], [16], [7], [7])
+    assert c.bin_missed == [0] * N_BINS and c.missed[0] == 1

@@ -55,11 +55,15 @@ def check_pool(dev, orc, i):
 
 def check_state(dev, orc, i):
     cd, co = dev.counters(i), orc.counters(i)
-    for key in ("evicted", "missed", "hits", "evictions", "ev_count", "pending", "n_updates"):
+    for key in ("evicted", "missed", "hits", "evictions", "ev_count", "pending", "n_updates", "bin_hits", "bin_missed"):
         assert cd[key] == co[key], "instance %d: %s %s vs oracle %s" % (i, key, cd[key], co[key])
     (wd, ad), (wo, ao) = dev.params(i), orc.params(i)
     assert np.array_equal(wd.view(np.uint32), wo.view(np.uint32)), "instance %d: w %s vs %s" % (i, wd, wo)
     assert np.array_equal(ad.view(np.uint32), ao.view(np.uint32)), "instance %d: alpha %s vs %s" % (i, ad, ao)
+    (md, sd, gd), (mo, so, go) = dev.timing_params(i), orc.timing_params(i)
+    assert np.array_equal(md.view(np.uint32), mo.view(np.uint32)), "instance %d: mu %s vs %s" % (i, md, mo)
+    assert np.array_equal(sd.view(np.uint32), so.view(np.uint32)), "instance %d: sigma %s vs %s" % (i, sd, so)
+    assert gd.view(np.uint32) == go.view(np.uint32), "instance %d: gamma %r vs %r" % (i, gd, go)
 
 
 def run_pair(name, steps, oracle_insts, n_inst=None, capacity=None, learn=3, check_every=100, **gen_over):
