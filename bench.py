@@ -110,7 +110,7 @@ def main():
     R = max(1, args.replicas)
     caches = []
     for r in range(R):
-        ctx = api.sae_create(1, N, cfg["kinds"], max_k=k)
+        ctx = api.sae_create(1, N, cfg["kinds"], max_k=k, max_requests=int(len(lens)))
         dp = DevicePool(1, N)
         dp.fill_instance(0, pool)
         dp.bind(ctx)
@@ -120,6 +120,7 @@ def main():
     d_reqs = torch.as_tensor(np.asarray(reqs, np.uint64).view(np.int64)).cuda()
     d_lens = torch.as_tensor(lens).cuda()
     d_ml = torch.zeros(len(lens), dtype=torch.int32, device="cuda")
+    d_mid = torch.empty((len(lens), reqs.shape[1]), dtype=torch.int32, device="cuda")
     stream = torch.cuda.Stream()  # default priority
     torch.cuda.synchronize()
 
@@ -133,6 +134,14 @@ def main():
     def select_only(i):
         c = caches[i % R]
         c["out"].run(c["ctx"], c["now"], k, 0, stream=stream)
+
+    def step_all_learners(i):
+        c = caches[i % R]
+        api.sae_prefix_match(c["ctx"], d_reqs, d_lens, c["now"], api.PM_TOUCH | api.PM_STATS | api.PM_INTERVALS,
+                             d_ml, matched_ids=d_mid, stream=stream)
+        c["out"].run(c["ctx"], c["now"], k, api.SS_COMMIT, stream=stream)
+        api.sae_feedback_update(c["ctx"], 0, stream=stream)
+        c["now"] += 1000
 
     with torch.cuda.stream(stream):
         # --- full steps
@@ -162,6 +171,19 @@ def main():
             select_only(i)
         torch.cuda.synchronize()
         s1 = time.perf_counter()
+        # --- the same step with every learner on: Algorithms 2, 3, 4 and the
+        # decay power, the prefix match recording reuse intervals
+        for c in caches:
+            api.sae_set_params(c["ctx"], -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k, learn=15),
+                               stream=stream)
+        for i in range(args.warmup):
+            step_all_learners(i)
+        torch.cuda.synchronize()
+        a0 = time.perf_counter()
+        for i in range(args.steps):
+            step_all_learners(i)
+        torch.cuda.synchronize()
+        a1 = time.perf_counter()
     st = 0
     for c in caches:
         st |= api.sae_poll_status(c["ctx"])
@@ -171,6 +193,7 @@ def main():
 
     ms_step = (t1 - t0) * 1e3 / args.steps
     ms_sel = (s1 - s0) * 1e3 / args.steps
+    ms_all = (a1 - a0) * 1e3 / args.steps
     scan_avg_ms = scan_ms / max(scan_n, 1)
     alg_bytes = BYTES_PER_BLOCK * N
     achieved = alg_bytes / (scan_avg_ms * 1e-3) / 1e9
@@ -197,6 +220,11 @@ def main():
         "score_select": {
             "value": N / (ms_sel * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_sel,
             "hbm_frac_at_10B_per_block": BYTES_PER_BLOCK * N / (ms_sel * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        },
+        "all_learners": {
+            "value": N / (ms_all * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_all,
+            "step": "the same step with Algorithms 2, 3, 4 and the decay-power learner on "
+                    "(prefix match records reuse intervals)",
         },
         "roofline": {
             "kernel": "k_scan", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -476,23 +476,28 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
     }
 }
 
-// Second pass of a prefix match with SAE_PM_INTERVALS.  Workgroups
-// 0 .. n_inst-1 append instance i's intervals to its rings in request order
-// (an exclusive scan over the requests, per log-normal queue; only the newest
-// SAE_IVL_CAP of the call are written); the other workgroups touch every
-// matched block (SAE_PM_TOUCH).  Neither reads what the other writes.
-__global__ void __launch_bounds__(kThreads) k_pm_place(DevCtx c, int n_req, int max_len, const int32_t *inst_a,
-                                                      int32_t now, uint32_t flags, const int32_t *matched_ids)
+// Second pass of a prefix match with SAE_PM_INTERVALS, 1024 threads per
+// workgroup.  Workgroups 0 .. n_inst-1 append instance i's intervals to its
+// rings in request order: each round gives thread t the PLACE_R requests
+// t*PLACE_R .. t*PLACE_R+PLACE_R-1 of the round (one round trip for all of
+// their records), a workgroup scan per log-normal queue ranks them, and a
+// later round overwrites the ring slots of an earlier one in rank order (the
+// barrier between rounds orders the stores).  The other workgroups touch every
+// matched block (SAE_PM_TOUCH).  Neither part reads what the other writes.
+constexpr int kPlaceThreads = 1024;
+constexpr int PLACE_R = 4;
+__global__ void __launch_bounds__(kPlaceThreads) k_pm_place(DevCtx c, int n_req, int max_len, const int32_t *inst_a,
+                                                           int32_t now, uint32_t flags, const int32_t *matched_ids)
 {
-    __shared__ uint32_t wsum[kThreads / SAE_WAVE];
-    __shared__ uint32_t tot;
+    constexpr int NW = kPlaceThreads / SAE_WAVE;
+    __shared__ uint32_t wsum[NW];
     const int lane = (int)__lane_id();
     const int wave = threadIdx.x / SAE_WAVE;
     if ((int)blockIdx.x >= c.n_inst) {
         if (!(flags & SAE_PM_TOUCH)) return;
         const long long total = (long long)n_req * max_len;
-        const long long stride = (long long)(gridDim.x - c.n_inst) * kThreads;
-        for (long long e = (long long)(blockIdx.x - c.n_inst) * kThreads + threadIdx.x; e < total; e += stride) {
+        const long long stride = (long long)(gridDim.x - c.n_inst) * kPlaceThreads;
+        for (long long e = (long long)(blockIdx.x - c.n_inst) * kPlaceThreads + threadIdx.x; e < total; e += stride) {
             const int32_t id = matched_ids[e];
             if (id < 0) continue;
             const int r = (int)(e / max_len);
@@ -505,56 +510,68 @@ __global__ void __launch_bounds__(kThreads) k_pm_place(DevCtx c, int n_req, int 
     }
     const int i = blockIdx.x;
     InstState &s = c.state[i];
-    int32_t *ring_base = c.ivl + (long long)i * c.Q * SAE_IVL_CAP;
-    for (int q = 0; q < c.Q; ++q) {
-        if (!((c.ln_mask >> q) & 1u)) continue;
-        // pass 1: intervals of this call for (i, q)
-        uint32_t cnt = 0;
-        for (int r = threadIdx.x; r < n_req; r += kThreads) {
-            const int ri = inst_a ? inst_a[r] : 0;
-            cnt += (ri == i && c.pm_rec[(long long)r * SAE_MAX_QUEUES + q] > 0) ? 1u : 0u;
+    long long n0[SAE_MAX_QUEUES];
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) n0[q] = ((c.ln_mask >> q) & 1u) ? s.ivl_n[q] : 0;
+    long long run[SAE_MAX_QUEUES];
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) run[q] = 0;
+    for (int base = 0; base < n_req; base += kPlaceThreads * PLACE_R) {
+        const int r0 = base + threadIdx.x * PLACE_R;
+        // every load is issued unconditionally (a clamped index) and masked
+        // afterwards, so the loads of all PLACE_R requests are in flight together
+        int32_t v[PLACE_R][SAE_MAX_QUEUES];  // dt per request and queue; 0: none
+#pragma unroll
+        for (int u = 0; u < PLACE_R; ++u) {
+            const int r = r0 + u;
+            const int rc = r < n_req ? r : n_req - 1;
+            const int ri = inst_a ? inst_a[rc] : 0;
+            const bool mine = r < n_req && ri == i;
+            const int4 *src = reinterpret_cast<const int4 *>(c.pm_rec + (long long)rc * SAE_MAX_QUEUES);
+            const int4 a = src[0], b = src[1];
+            v[u][0] = mine ? a.x : 0; v[u][1] = mine ? a.y : 0; v[u][2] = mine ? a.z : 0; v[u][3] = mine ? a.w : 0;
+            v[u][4] = mine ? b.x : 0; v[u][5] = mine ? b.y : 0; v[u][6] = mine ? b.z : 0; v[u][7] = mine ? b.w : 0;
         }
-        for (int o = SAE_WAVE / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
-        if (lane == 0) wsum[wave] = cnt;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t t = 0;
-            for (int w = 0; w < kThreads / SAE_WAVE; ++w) t += wsum[w];
-            tot = t;
-        }
-        __syncthreads();
-        const long long total = tot;
-        const long long n0 = s.ivl_n[q];
-        const long long keep_from = total - SAE_IVL_CAP;  // call-local ranks below this are overwritten anyway
-        int32_t *ring = ring_base + (long long)q * SAE_IVL_CAP;
-        // pass 2: request-order ranks by a workgroup scan per chunk
-        long long run = 0;
-        for (int base = 0; base < n_req; base += kThreads) {
-            const int r = base + threadIdx.x;
-            int32_t v = 0;
-            if (r < n_req) {
-                const int ri = inst_a ? inst_a[r] : 0;
-                if (ri == i) v = c.pm_rec[(long long)r * SAE_MAX_QUEUES + q];
+#pragma unroll
+        for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+            if (!((c.ln_mask >> q) & 1u)) continue;
+            uint32_t mine = 0;
+#pragma unroll
+            for (int u = 0; u < PLACE_R; ++u) mine += v[u][q] > 0 ? 1u : 0u;
+            // inclusive scan over the wave, then over the waves
+            uint32_t inc = mine;
+#pragma unroll
+            for (int o = 1; o < SAE_WAVE; o <<= 1) {
+                const uint32_t t = __shfl_up(inc, o);
+                if (lane >= o) inc += t;
             }
-            const bool f = v > 0;
-            const unsigned long long bm = __ballot(f);
-            const uint32_t below = (uint32_t)__popcll(bm & ((1ull << lane) - 1ull));
-            __syncthreads();  // wsum of the previous chunk has been read
-            if (lane == 0) wsum[wave] = (uint32_t)__popcll(bm);
+            __syncthreads();  // wsum of the previous scan has been read
+            if (lane == SAE_WAVE - 1) wsum[wave] = inc;
             __syncthreads();
-            uint32_t before = 0, chunk = 0;
-            for (int w = 0; w < kThreads / SAE_WAVE; ++w) {
+            uint32_t before = 0, round_total = 0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) {
                 const uint32_t x = wsum[w];
                 before += (w < wave) ? x : 0u;
-                chunk += x;
+                round_total += x;
             }
-            const long long rank = run + before + below;
-            if (f && rank >= keep_from) ring[(n0 + rank) % SAE_IVL_CAP] = v;
-            run += chunk;
+            long long rank = run[q] + before + (inc - mine);
+            int32_t *ring = c.ivl + ((long long)i * c.Q + q) * SAE_IVL_CAP;
+#pragma unroll
+            for (int u = 0; u < PLACE_R; ++u) {
+                if (v[u][q] > 0) {
+                    ring[(n0[q] + rank) % SAE_IVL_CAP] = v[u][q];
+                    ++rank;
+                }
+            }
+            run[q] += round_total;
         }
-        __syncthreads();
-        if (threadIdx.x == 0) s.ivl_n[q] = n0 + total;
-        __syncthreads();
+        __syncthreads();  // this round's ring stores precede the next round's
+    }
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int q = 0; q < SAE_MAX_QUEUES; ++q)
+            if ((c.ln_mask >> q) & 1u) s.ivl_n[q] = n0[q] + run[q];
     }
 }
 
@@ -714,10 +731,11 @@ hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, 
                        inst, now, flags, match_len, matched_ids);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(flags & SAE_PM_INTERVALS)) return e;
-    long long tg = (flags & SAE_PM_TOUCH) ? (long long)grid_for((long long)n_req * max_len) : 0;
-    if (tg > 2048) tg = 2048;
-    hipLaunchKernelGGL(k_pm_place, dim3((unsigned)(c.n_inst + tg)), dim3(kThreads), 0, s, c, n_req, max_len, inst,
-                       now, flags, (const int32_t *)matched_ids);
+    long long tg = 0;
+    if (flags & SAE_PM_TOUCH) tg = ((long long)n_req * max_len + kPlaceThreads - 1) / kPlaceThreads;
+    if (tg > 1024) tg = 1024;
+    hipLaunchKernelGGL(k_pm_place, dim3((unsigned)(c.n_inst + tg)), dim3(kPlaceThreads), 0, s, c, n_req, max_len,
+                       inst, now, flags, (const int32_t *)matched_ids);
     return hipGetLastError();
 }
 

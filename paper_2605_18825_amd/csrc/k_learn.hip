@@ -1,5 +1,5 @@
 // Eviction-feedback learners: Algorithms 2, 3 and 4 and the decay-power
-// learner, one workgroup of one wave per instance.  fp32 in the order the
+// learner, one workgroup per instance.  fp32 in the order the
 // algorithms state them (built with -ffp-contract=off, so no operation is
 // fused); Algorithm 4's moments are exact integer sums rounded once.
 #include "sae_internal.h"
@@ -21,50 +21,113 @@ __device__ __forceinline__ U128 add128(U128 a, U128 b)
 }
 
 // Algorithm 4 for every log-normal queue with more than 20 buffered
-// intervals.  The wave's 64 lanes split the buffer; x = ln dt in the fp32
-// recipe is 0 or >= ln 2, so X = x * 2^24 is an integer and the sums
-// S1 = sum X, S2 = sum X^2 are exact in any order.  Lane 0 then rounds:
+// intervals.  The workgroup's threads split the buffers; X = ln(dt) * 2^24
+// is an exact integer (ivl_scaled_ln), so the sums S1 = sum X, S2 = sum X^2
+// are exact in any order.  Thread q then rounds:
 // m = S1 / n * 2^-24, v = max(S2 / n * 2^-48 - m m, 0) in double,
 // mu_s = fl32(m), sigma_s = fl32(sqrt v), followed by the fp32 EMA.
-__device__ void lognormal_params(const DevCtx &c, int inst, InstState &s, int lane)
+constexpr int kLearnThreads = 1024;
+
+// Position of the k-th set bit of m (k < popcount(m)).
+__device__ __forceinline__ int nth_bit(uint32_t m, int k)
 {
-    for (int q = 0; q < c.Q; ++q) {
-        if (!((c.ln_mask >> q) & 1u)) continue;
-        const long long n = s.ivl_n[q];
-        const long long lo = s.ivl_start[q] > n - SAE_IVL_CAP ? s.ivl_start[q] : n - SAE_IVL_CAP;
-        const long long cnt = n - lo;
-        if (cnt <= 20) continue;
-        const int32_t *ring = c.ivl + ((long long)inst * c.Q + q) * SAE_IVL_CAP;
-        long long s1 = 0;
-        U128 s2 = {0ull, 0ull};
-        for (long long p = lo + lane; p < n; p += SAE_WAVE) {
-            const float x = dsr::ln((float)ring[p % SAE_IVL_CAP]);
-            const long long X = (long long)(x * 16777216.0f);
+    for (int j = 0; j < k; ++j) m &= m - 1u;
+    return __ffs(m) - 1;
+}
+
+// Per-wave partial sums of Algorithm 4, kept in LDS between its two halves.
+struct Alg4Sums {
+    long long s1[kLearnThreads / SAE_WAVE];
+    unsigned long long s2lo[kLearnThreads / SAE_WAVE], s2hi[kLearnThreads / SAE_WAVE];
+};
+
+__device__ __forceinline__ long long ivl_lo(const InstState &s, int q)
+{
+    const long long n = s.ivl_n[q];
+    return s.ivl_start[q] > n - SAE_IVL_CAP ? s.ivl_start[q] : n - SAE_IVL_CAP;
+}
+
+// First half, on all threads: the log-normal queues with more than 20
+// buffered intervals (returned as a bit mask, the same on every thread) and
+// the exact sums of their buffers, one queue per wave group; ends with a
+// workgroup barrier when the mask is not empty.
+__device__ uint32_t alg4_sums(const DevCtx &c, int inst, const InstState &s, int t, Alg4Sums &w)
+{
+    constexpr int NW = kLearnThreads / SAE_WAVE;
+    constexpr int BATCH = 8;  // loads a thread has in flight together
+    const int lane = t % SAE_WAVE, wave = t / SAE_WAVE;
+    uint32_t due = 0;
+    for (int q = 0; q < c.Q; ++q)
+        if (((c.ln_mask >> q) & 1u) && s.ivl_n[q] - ivl_lo(s, q) > 20) due |= 1u << q;
+    if (!due) return 0;
+    // wave v sums part of the (v mod nd)-th due queue's buffer
+    const int nd = __popc(due);
+    const int qi = wave % nd;
+    const int q = nth_bit(due, qi);
+    const int wq = wave / nd, nwq = (NW - 1 - qi) / nd + 1;
+    const long long n = s.ivl_n[q];
+    const long long lo = ivl_lo(s, q);
+    const int32_t *ring = c.ivl + ((long long)inst * c.Q + q) * SAE_IVL_CAP;
+    const long long stride = (long long)nwq * SAE_WAVE;
+    long long s1 = 0;
+    U128 s2 = {0ull, 0ull};
+    for (long long b0 = lo + (long long)wq * SAE_WAVE; b0 < n; b0 += BATCH * stride) {
+        int32_t d[BATCH];
+#pragma unroll
+        for (int k = 0; k < BATCH; ++k) {  // unconditional loads at clamped positions
+            const long long p = b0 + lane + k * stride;
+            d[k] = ring[(p < n ? p : lo) & (SAE_IVL_CAP - 1)];
+        }
+#pragma unroll
+        for (int k = 0; k < BATCH; ++k) {
+            const long long p = b0 + lane + k * stride;
+            const long long X = p < n ? ivl_scaled_ln(d[k]) : 0;
             const unsigned long long X2 = (unsigned long long)X * (unsigned long long)X;
             s1 += X;
             s2 = add128(s2, U128{X2, 0ull});
         }
-        for (int o = SAE_WAVE / 2; o > 0; o >>= 1) {
-            s1 += __shfl_xor(s1, o);
-            U128 t;
-            t.lo = __shfl_xor(s2.lo, o);
-            t.hi = __shfl_xor(s2.hi, o);
-            s2 = add128(s2, t);
-        }
-        if (lane == 0) {
-            const double nd = (double)cnt;
-            const double m = ((double)s1 / nd) * 0x1p-24;
-            const double s2d = (double)s2.hi * 0x1p64 + (double)s2.lo;
-            double v = (s2d / nd) * 0x1p-48 - m * m;
-            if (v < 0.0) v = 0.0;
-            const float mu_s = (float)m;
-            const float sd_s = (float)sqrt(v);
-            s.mu[q] = s.mu[q] + s.beta_ln * (mu_s - s.mu[q]);
-            const float sg = s.sigma[q] + s.beta_ln * (sd_s - s.sigma[q]);
-            s.sigma[q] = fmaxf(sg, 0.1f);
-            s.ivl_start[q] = lo > n - 200 ? lo : n - 200;  // keep the last 200
-        }
     }
+    for (int o = SAE_WAVE / 2; o > 0; o >>= 1) {
+        s1 += __shfl_xor(s1, o);
+        U128 u;
+        u.lo = __shfl_xor(s2.lo, o);
+        u.hi = __shfl_xor(s2.hi, o);
+        s2 = add128(s2, u);
+    }
+    if (lane == 0) {
+        w.s1[wave] = s1;
+        w.s2lo[wave] = s2.lo;
+        w.s2hi[wave] = s2.hi;
+    }
+    __syncthreads();
+    return due;
+}
+
+// Second half, thread j < popcount(due): the j-th due queue's moments and EMA.
+__device__ void alg4_finish(InstState &s, int j, uint32_t due, const Alg4Sums &w)
+{
+    constexpr int NW = kLearnThreads / SAE_WAVE;
+    const int nd = __popc(due);
+    const int q = nth_bit(due, j);
+    long long S1 = 0;
+    U128 S2 = {0ull, 0ull};
+    for (int v = j; v < NW; v += nd) {
+        S1 += w.s1[v];
+        S2 = add128(S2, U128{w.s2lo[v], w.s2hi[v]});
+    }
+    const long long n = s.ivl_n[q];
+    const long long lo = ivl_lo(s, q);
+    const double cnt = (double)(n - lo);
+    const double m = ((double)S1 / cnt) * 0x1p-24;
+    const double s2d = (double)S2.hi * 0x1p64 + (double)S2.lo;
+    double v = (s2d / cnt) * 0x1p-48 - m * m;
+    if (v < 0.0) v = 0.0;
+    const float mu_s = (float)m;
+    const float sd_s = (float)sqrt(v);
+    s.mu[q] = s.mu[q] + s.beta_ln * (mu_s - s.mu[q]);
+    const float sg = s.sigma[q] + s.beta_ln * (sd_s - s.sigma[q]);
+    s.sigma[q] = fmaxf(sg, 0.1f);
+    s.ivl_start[q] = lo > n - 200 ? lo : n - 200;  // keep the last 200
 }
 
 // Decay-power learner (App. B) over the positional bins: hit rate per bin,
@@ -102,39 +165,16 @@ __device__ void decay_power(InstState &s)
     for (int b = 0; b < SAE_N_BINS; ++b) s.bin_hits[b] = s.bin_missed[b] = 0;
 }
 
-// One workgroup of 64 threads per instance: first fold the striped counter
-// copies into the instance state (thread f sums field f over the copies),
-// then, if asked and due, thread 0 runs the learners.
-__global__ void k_feedback(DevCtx c, uint32_t flags, int learn)
+// Algorithms 3 and 2 and the decay-power learner on the lanes of one wave,
+// which touch disjoint fields: lane l < 5 updates token type l (Algorithm 3),
+// lane 8 + q queue q (Algorithm 2), lane 63 gamma.
+__device__ void learners_23_gamma(const DevCtx &c, InstState &s, int l)
 {
-    const int inst = blockIdx.x;
-    InstState &s = c.state[inst];
-    const int f = threadIdx.x;
-    if (f < SAE_CF_N) {
-        int32_t *base = c.cpart + (long long)inst * SAE_CSLOTS * SAE_CF_STRIDE + f;
-        int32_t sum = 0;
-        for (int k = 0; k < SAE_CSLOTS; ++k) {
-            sum += base[k * SAE_CF_STRIDE];
-            base[k * SAE_CF_STRIDE] = 0;
-        }
-        if (sum) {
-            if (f < SAE_CF_MISSED) s.evicted[f - SAE_CF_EVICTED] += sum;
-            else if (f < SAE_CF_HITS) s.missed[f - SAE_CF_MISSED] += sum;
-            else if (f < SAE_CF_EVICTIONS) s.hits[f - SAE_CF_HITS] += sum;
-            else if (f < SAE_CF_BHITS) s.evictions[f - SAE_CF_EVICTIONS] += sum;
-            else if (f < SAE_CF_BMISS) s.bin_hits[f - SAE_CF_BHITS] += sum;
-            else s.bin_missed[f - SAE_CF_BMISS] += sum;
-        }
-    }
-    __syncthreads();
-    if (!learn) return;
-    if (!s.pending && !(flags & SAE_FB_FORCE)) return;
-    if ((s.learn & SAE_LEARN_LOGNORMAL) && c.ln_mask) lognormal_params(c, inst, s, f);
-    if (f != 0) return;
-    if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
-        // Algorithm 3: raise the weight of types evicted too aggressively;
-        // both counters decay by lambda = 0.99, applied as floor(99 x / 100).
-        for (int t = 0; t < SAE_N_TYPES; ++t) {
+    if (l < SAE_N_TYPES) {
+        if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
+            // Algorithm 3: raise the weight of types evicted too aggressively;
+            // both counters decay by lambda = 0.99, applied as floor(99 x / 100).
+            const int t = l;
             int32_t ev = s.evicted[t], mi = s.missed[t];
             if (ev > 10) {
                 float rate = (float)mi / (float)ev;
@@ -145,11 +185,10 @@ __global__ void k_feedback(DevCtx c, uint32_t flags, int learn)
             s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
             s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
         }
-    }
-    if (s.learn & SAE_LEARN_QUEUE_WEIGHTS) {
-        // Algorithm 2: EMA of the queue weight toward 1 + efficiency / T.
-        for (int q = 0; q < c.Q; ++q) {
-            if (c.kind[q] == SAE_KIND_EVICT_FIRST) continue;
+    } else if (l >= 8 && l < 8 + c.Q) {
+        const int q = l - 8;
+        if ((s.learn & SAE_LEARN_QUEUE_WEIGHTS) && c.kind[q] != SAE_KIND_EVICT_FIRST) {
+            // Algorithm 2: EMA of the queue weight toward 1 + efficiency / T.
             int32_t h = s.hits[q], e = s.evictions[q];
             if (e > 5) {
                 float eff = (float)h / (float)e;
@@ -161,16 +200,76 @@ __global__ void k_feedback(DevCtx c, uint32_t flags, int learn)
             s.hits[q] = 0;
             s.evictions[q] = 0;
         }
+    } else if (l == SAE_WAVE - 1) {
+        if (s.learn & SAE_LEARN_DECAY_POWER) decay_power(s);
     }
-    if (s.learn & SAE_LEARN_DECAY_POWER) decay_power(s);
-    s.pending = 0;
-    s.n_updates += 1;
+}
+
+// One workgroup of 1024 threads per instance.  The instance state is copied
+// into LDS while the striped counter copies are read (one memory round trip)
+// and summed per field in LDS; thread f folds field f into the copy.  Then, if
+// asked and due, Algorithm 4 sums on all threads and then finishes on wave 0
+// while wave 1 runs the other learners on the copy, which is written back at
+// the end.
+static_assert(sizeof(InstState) % 4 == 0, "InstState is copied as 32-bit words");
+__global__ void __launch_bounds__(kLearnThreads) k_feedback(DevCtx c, uint32_t flags, int learn)
+{
+    constexpr int NWORDS = (int)(sizeof(InstState) / 4);
+    __shared__ InstState s;
+    __shared__ int due;
+    const int inst = blockIdx.x;
+    const int f = threadIdx.x;
+    __shared__ int32_t fsum[SAE_CF_STRIDE];
+    uint32_t *gw = reinterpret_cast<uint32_t *>(c.state + inst);
+    uint32_t *lw = reinterpret_cast<uint32_t *>(&s);
+    for (int w = f; w < NWORDS; w += kLearnThreads) lw[w] = gw[w];
+    if (f < SAE_CF_STRIDE) fsum[f] = 0;
+    // every (copy, field) word of the striped counters: all loads in flight together
+    constexpr int NC = SAE_CSLOTS * SAE_CF_STRIDE / kLearnThreads;
+    static_assert(NC * kLearnThreads == SAE_CSLOTS * SAE_CF_STRIDE, "counter words split evenly");
+    int32_t *cbase = c.cpart + (long long)inst * SAE_CSLOTS * SAE_CF_STRIDE;
+    int32_t cv[NC];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) cv[j] = cbase[f + j * kLearnThreads];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NC; ++j)
+        if (cv[j]) {
+            const int e = f + j * kLearnThreads;
+            cbase[e] = 0;
+            atomicAdd(&fsum[e % SAE_CF_STRIDE], cv[j]);
+        }
+    __syncthreads();
+    const int32_t sum = f < SAE_CF_N ? fsum[f] : 0;
+    if (f < SAE_CF_N && sum) {
+        if (f < SAE_CF_MISSED) s.evicted[f - SAE_CF_EVICTED] += sum;
+        else if (f < SAE_CF_HITS) s.missed[f - SAE_CF_MISSED] += sum;
+        else if (f < SAE_CF_EVICTIONS) s.hits[f - SAE_CF_HITS] += sum;
+        else if (f < SAE_CF_BHITS) s.evictions[f - SAE_CF_EVICTIONS] += sum;
+        else if (f < SAE_CF_BMISS) s.bin_hits[f - SAE_CF_BHITS] += sum;
+        else s.bin_missed[f - SAE_CF_BMISS] += sum;
+    }
+    if (f == 0) due = learn && (s.pending || (flags & SAE_FB_FORCE));
+    __syncthreads();
+    if (due) {
+        __shared__ Alg4Sums a4;
+        const uint32_t ln_due = ((s.learn & SAE_LEARN_LOGNORMAL) && c.ln_mask) ? alg4_sums(c, inst, s, f, a4) : 0u;
+        if (f < __popc(ln_due)) alg4_finish(s, f, ln_due, a4);                 // wave 0
+        else if (f >= SAE_WAVE && f < 2 * SAE_WAVE) learners_23_gamma(c, s, f - SAE_WAVE);  // wave 1
+        __syncthreads();
+        if (f == 0) {
+            s.pending = 0;
+            s.n_updates += 1;
+        }
+    }
+    __syncthreads();
+    for (int w = f; w < NWORDS; w += kLearnThreads) gw[w] = lw[w];
 }
 
 }  // namespace
 
 hipError_t launch_feedback(const DevCtx &c, uint32_t flags, int learn, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_feedback, dim3(c.n_inst), dim3(64), 0, s, c, flags, learn);
+    hipLaunchKernelGGL(k_feedback, dim3(c.n_inst), dim3(kLearnThreads), 0, s, c, flags, learn);
     return hipGetLastError();
 }

@@ -139,7 +139,7 @@ struct DevCtx {
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
     int32_t *sel_count;        // [n_inst][Q]
     int32_t *ivl;              // [n_inst][Q][SAE_IVL_CAP] Algorithm 4 interval rings (dt in ticks)
-    int32_t *pm_rec;           // [max_requests][SAE_MAX_QUEUES] intervals of one prefix-match call
+    int32_t *pm_rec;           // [max_requests][SAE_MAX_QUEUES] intervals of one prefix-match call (0: none)
     int32_t max_req;
     uint32_t ln_mask;          // bit q: queue q is log-normal
     uint32_t struct_mask;      // bit q: queue q is structural
@@ -301,6 +301,14 @@ __device__ __forceinline__ float erfc(float x)
 }
 
 }  // namespace dsr
+
+// Algorithm 4's summand of an interval: X = x * 2^24 with x the recipe's ln of
+// fl32(dt), dt >= 1.  x is 0 (dt = 1) or at least ln 2, so X is an integer
+// (< 2^29) and exact.
+__device__ __forceinline__ int32_t ivl_scaled_ln(int32_t dt)
+{
+    return (int32_t)(dsr::ln((float)dt) * 16777216.0f);
+}
 
 // Per-instance scoring constants, staged in LDS by every workgroup.
 struct ScoreTab {
