@@ -141,7 +141,11 @@ enum {
     SAE_LEARN_TOKEN_WEIGHTS = 1u << 0, /* Algorithm 3                              */
     SAE_LEARN_QUEUE_WEIGHTS = 1u << 1, /* Algorithm 2                              */
     SAE_LEARN_LOGNORMAL = 1u << 2,     /* Algorithm 4: mu_q, sigma_q              */
-    SAE_LEARN_DECAY_POWER = 1u << 3    /* gamma from positional hit rates (App. B) */
+    SAE_LEARN_DECAY_POWER = 1u << 3,   /* gamma from positional hit rates (App. B) */
+    SAE_LEARN_TOKEN_EMA = 1u << 4,     /* App. B text's token-weight rule; replaces
+                                          Algorithm 3 (not both)                   */
+    SAE_LEARN_QUEUE_REL = 1u << 5      /* App. B text's queue-weight rule; replaces
+                                          Algorithm 2 (not both)                   */
 };
 
 /* Feedback counters of one instance (Algorithms 1-3). */
@@ -157,6 +161,10 @@ typedef struct {
                                          structural blocks per positional bin     */
     int32_t bin_missed[SAE_N_BINS];   /* ... and misses after their eviction
                                          (both only while SAE_LEARN_DECAY_POWER) */
+    int32_t type_hits[SAE_N_TYPES];   /* SAE_LEARN_TOKEN_EMA: prefix-match hits per
+                                         block type ...                           */
+    int32_t type_added[SAE_N_TYPES];  /* ... and blocks added per type (Add())    */
+    int32_t resident[SAE_MAX_QUEUES]; /* cached (valid) blocks per queue          */
 } sae_counters;
 
 /* Caller-owned device arrays of the block pool (layout above). */
@@ -186,7 +194,8 @@ sae_status sae_destroy(sae_ctx *ctx);
 sae_status sae_bind_pool(sae_ctx *ctx, const sae_pool *pool);
 
 /* Parameters of one instance (inst >= 0) or of all (inst = -1); host struct
- * copied before return.  sigma, gamma, temperature must be > 0. */
+ * copied before return.  sigma, gamma, temperature must be > 0; at most one
+ * token-weight rule and one queue-weight rule may be chosen in `learn`. */
 sae_status sae_set_params(sae_ctx *ctx, int32_t inst, const sae_params *p, sae_stream_t stream);
 /* Read back parameters / counters of one instance; synchronizes `stream`. */
 sae_status sae_get_params(sae_ctx *ctx, int32_t inst, sae_params *out, sae_stream_t stream);
@@ -276,7 +285,8 @@ enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1, SAE_PM_INTERVALS = 1u << 
  * block); SAE_PM_STATS adds every matched block to queue_hits[its queue]
  * (Algorithm 2) and, in a structural queue of an instance whose
  * SAE_LEARN_DECAY_POWER bit is set, to the hits of its positional bin
- * floor(8 o_b / o_max) (decay-power learner, App. B).
+ * floor(8 o_b / o_max) (decay-power learner, App. B); with SAE_LEARN_TOKEN_EMA
+ * set, to type_hits[its type].
  * SAE_PM_INTERVALS records Algorithm 4's reuse intervals: for every request
  * and every log-normal queue among its matched blocks, dt = now - last_access
  * of its deepest matched block of that queue, as it was before the call,
@@ -351,6 +361,17 @@ enum { SAE_FB_FORCE = 1u << 0 };
  *    if there were more than 20 events, both halves had some and front > 0:
  *    gamma <- clamp(gamma + beta (1 / (back / front + 0.1) - gamma), 0.3, 3.0)
  *    and the bin counters restart.
+ *  Token weights, the appendix text's rule (SAE_LEARN_TOKEN_EMA): for every
+ *    type, w_target = 1 + 5 r_miss + 2 r_reuse with r_miss = missed / evicted
+ *    and r_reuse = type_hits / (type_hits + type_added) (0 when undefined),
+ *    w <- clamp((1 - eta) w + eta w_target, 0.1, 5.0); the four counters decay
+ *    as floor(0.99 x).
+ *  Queue weights, the appendix text's rule (SAE_LEARN_QUEUE_REL): over the
+ *    queues but the evict-first one that hold blocks, E_q = hits_q /
+ *    (resident_q / resident_all), E_mean their mean; if E_mean > 0,
+ *    alpha_q <- clamp(beta alpha_q + (1 - beta) (E_q / E_mean)^(1/T), 0.1, 3.0)
+ *    (the power as the fp32 recipe's exp(ln x / T), x itself for T = 1); hits
+ *    and evictions then reset.
  * Each algorithm runs only if its SAE_LEARN_* bit is set.
  */
 sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream);

@@ -50,6 +50,11 @@ Readings of points where the paper is silent (each listed in the design doc):
   more than 20 events, events in both halves and front > 0; its counters
   restart after an update.  They are gathered only while the learner is on
   (the bin of an evicted block is always kept with its entry).
+* The appendix text also states a token-weight rule (an EMA toward
+  1 + 5 r_miss + 2 r_reuse) and a queue-weight rule (relative efficiency
+  hits / capacity share, raised to 1/T); each is a learner of its own that
+  replaces Algorithm 3, respectively 2, when chosen (`token_weights_ema`,
+  `queue_weights_rel`, with their readings in their docstrings).
 """
 import math
 
@@ -116,7 +121,7 @@ class Params:
 
     def __init__(self, n_queues, w=1.0, alpha=1.0, mu=0.0, sigma=1.0, gamma=1.0,
                  eta=0.01, T=1.0, beta=0.1, K=32, learn_w=True, learn_alpha=True,
-                 beta_ln=0.1, learn_ln=False, learn_gamma=False):
+                 beta_ln=0.1, learn_ln=False, learn_gamma=False, learn_w_ema=False, learn_alpha_rel=False):
         def vec(v, n):
             a = np.zeros(n, F32)
             a[:] = np.resize(np.asarray(v, F32), n)
@@ -135,6 +140,10 @@ class Params:
         self.beta_ln = F32(beta_ln)
         self.learn_ln = bool(learn_ln)
         self.learn_gamma = bool(learn_gamma)
+        self.learn_w_ema = bool(learn_w_ema)
+        self.learn_alpha_rel = bool(learn_alpha_rel)
+        assert not (self.learn_w and self.learn_w_ema), "one token-weight rule at a time"
+        assert not (self.learn_alpha and self.learn_alpha_rel), "one queue-weight rule at a time"
 
 
 class OracleCache:
@@ -170,6 +179,8 @@ class OracleCache:
         self.ivl = [[] for _ in range(self.Q)]   # Algorithm 4 buffers (log-normal queues)
         self.bin_hits = [0] * N_BINS
         self.bin_missed = [0] * N_BINS
+        self.type_hits = [0] * N_TYPES    # text-form token weights: hit blocks per type
+        self.type_added = [0] * N_TYPES   # ... and blocks added per type
 
     # ------------------------------------------------------------------ state
     def bind(self, last_access, queue, tau, ntok, ob, omax, valid, ref_count,
@@ -333,6 +344,8 @@ class OracleCache:
                     self.hits[q] += 1
                     if self.kind[q] == STRUCTURAL and self.prm.learn_gamma:
                         self.bin_hits[self.pos_bin(b)] += 1
+                    if self.prm.learn_w_ema:
+                        self.type_hits[self.tau[b]] += 1
                 if touch:
                     touched.append(b)
                 if self.kind[q] == LOGNORMAL:
@@ -372,6 +385,8 @@ class OracleCache:
             self.ref_count[b] = 0
             self.access_count[b] = 0
             self.index[h] = b
+            if self.prm.learn_w_ema:
+                self.type_added[self.tau[b]] += 1
             g = self.ghost.pop(h, None)
             if g is not None and self.ghost_live(g):
                 self.missed[g[0]] += 1
@@ -409,6 +424,66 @@ class OracleCache:
                 p.alpha[q] = clamp(p.alpha[q] + p.beta * (target - p.alpha[q]), 0.1, 3.0)
             self.hits[q] = 0
             self.evictions[q] = 0
+
+    def token_weights_ema(self):
+        """The appendix text's token-weight rule (App. B): per type,
+        w_target = 1 + 5 r_miss + 2 r_reuse and w <- (1 - eta) w + eta w_target,
+        in fp32.  r_miss = missed / evicted (0 without evictions); r_reuse = hit
+        blocks / (hit blocks + blocks added), the type's cache hit rate (0
+        without either).  All four counters decay by 0.99 (floored) per run;
+        w stays in Algorithm 3's [0.1, 5.0]."""
+        p = self.prm
+        one = F32(1.0)
+        for t in range(N_TYPES):
+            ev, mi = self.evicted[t], self.missed[t]
+            h, a = self.type_hits[t], self.type_added[t]
+            r_miss = F32(mi) / F32(ev) if ev > 0 else F32(0.0)
+            r_reuse = F32(h) / F32(h + a) if h + a > 0 else F32(0.0)
+            target = one + r_miss * F32(5.0) + r_reuse * F32(2.0)
+            p.w[t] = clamp((one - p.eta) * p.w[t] + p.eta * target, 0.1, 5.0)
+            self.evicted[t] = (99 * ev) // 100
+            self.missed[t] = (99 * mi) // 100
+            self.type_hits[t] = (99 * h) // 100
+            self.type_added[t] = (99 * a) // 100
+
+    def resident(self):
+        """Cached (valid) blocks per queue."""
+        return [int(np.count_nonzero(self.valid & (self.queue == q))) for q in range(self.Q)]
+
+    def queue_weights_rel(self):
+        """The appendix text's queue-weight rule (App. B): E_q = H_q / C_q
+        with H_q the queue's hit blocks since the last run and C_q its share of
+        the cached blocks; alpha_q <- beta alpha_q + (1 - beta) (E_q / E_mean)^(1/T)
+        over the queues but the evict-first one that hold blocks, E_mean their
+        mean, in fp32 (x^(1/T) = exp(ln x / T) in the fp32 recipe, x itself for
+        T = 1); clamped to Algorithm 2's [0.1, 3.0].  Runs only when E_mean > 0;
+        hits and evictions restart after every run."""
+        p = self.prm
+        res = self.resident()
+        total = sum(res)
+        qs = [q for q in range(self.Q) if self.kind[q] != EVICT_FIRST and res[q] > 0]
+        if total > 0 and qs:
+            E = {}
+            for q in qs:
+                share = F32(res[q]) / F32(total)
+                E[q] = F32(self.hits[q]) / share
+            e_sum = F32(0.0)
+            for q in qs:
+                e_sum = e_sum + E[q]
+            e_mean = e_sum / F32(len(qs))
+            if e_mean > 0:
+                for q in qs:
+                    x = E[q] / e_mean
+                    if p.T == F32(1.0) or x == 0:
+                        tgt = x
+                    else:
+                        lx = _native.ln(np.array([x], F32))[0]
+                        tgt = _native.exp(np.array([lx / p.T], F32))[0]
+                    p.alpha[q] = clamp(p.beta * p.alpha[q] + (F32(1.0) - p.beta) * tgt, 0.1, 3.0)
+        for q in range(self.Q):
+            if self.kind[q] != EVICT_FIRST:
+                self.hits[q] = 0
+                self.evictions[q] = 0
 
     def lognormal_params(self):
         """Algorithm 4 for every log-normal queue (one estimator per queue)."""
@@ -457,8 +532,12 @@ class OracleCache:
             return False
         if self.prm.learn_w:
             self.token_weights()
+        if self.prm.learn_w_ema:
+            self.token_weights_ema()
         if self.prm.learn_alpha:
             self.queue_weights()
+        if self.prm.learn_alpha_rel:
+            self.queue_weights_rel()
         if self.prm.learn_ln:
             self.lognormal_params()
         if self.prm.learn_gamma:
@@ -471,7 +550,9 @@ class OracleCache:
         return dict(evicted=list(self.evicted), missed=list(self.missed),
                     hits=list(self.hits), evictions=list(self.evictions),
                     ev_count=self.ev_count, pending=self.pending,
-                    bin_hits=list(self.bin_hits), bin_missed=list(self.bin_missed))
+                    bin_hits=list(self.bin_hits), bin_missed=list(self.bin_missed),
+                    type_hits=list(self.type_hits), type_added=list(self.type_added),
+                    resident=self.resident())
 
 
 def sample_moments(intervals):

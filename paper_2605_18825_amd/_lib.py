@@ -55,6 +55,9 @@ class SaeCounters(ctypes.Structure):
         ("n_updates", ctypes.c_int32),
         ("bin_hits", ctypes.c_int32 * N_BINS),
         ("bin_missed", ctypes.c_int32 * N_BINS),
+        ("type_hits", ctypes.c_int32 * N_TYPES),
+        ("type_added", ctypes.c_int32 * N_TYPES),
+        ("resident", ctypes.c_int32 * MAX_QUEUES),
     ]
 
 

@@ -19,6 +19,9 @@ FB_FORCE = 1
 HINT_DECODE, HINT_UNTEMPLATED, HINT_MULTI_TURN, HINT_AGENTIC, HINT_CONVERSATION, HINT_SHARED_PREFIX = 1, 2, 4, 8, 16, 32
 ROLE_EVICT, ROLE_STRUCT, ROLE_CHAT, ROLE_AGENT = 0, 1, 2, 3
 LEARN_TOKEN_WEIGHTS, LEARN_QUEUE_WEIGHTS, LEARN_LOGNORMAL, LEARN_DECAY_POWER = 1, 2, 4, 8
+LEARN_TOKEN_EMA, LEARN_QUEUE_REL = 16, 32
+# the paper's initial token weights (system, user, tool, response, cot), Sec. 5
+PAPER_INIT_W = (2.0, 1.5, 1.0, 1.0, 0.1)
 ST_NAMES = {1: "INDEX_FULL", 2: "GHOST_FULL", 4: "BAD_OFFSET", 8: "FUTURE_ACCESS",
             16: "SLOT_BUSY", 32: "SELECT_FALLBACK", 64: "BAD_BLOCK"}
 

@@ -193,21 +193,42 @@ __global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
         s.n_updates = 0;
         s.last_d = 0;
         for (int b = 0; b < SAE_N_BINS; ++b) s.bin_hits[b] = s.bin_missed[b] = 0;
-        for (int q = 0; q < SAE_MAX_QUEUES; ++q) s.ivl_n[q] = s.ivl_start[q] = 0;
+        for (int t = 0; t < SAE_N_TYPES; ++t) s.type_hits[t] = s.type_added[t] = 0;
+        for (int q = 0; q < SAE_MAX_QUEUES; ++q) s.ivl_n[q] = s.ivl_start[q] = s.resident[q] = 0;
     }
 }
 
-// Insert every valid block's hash into its instance's index.
-__global__ void k_index_fill(DevCtx c)
+// Insert every valid block's hash into its instance's index and, on a full
+// build (`census`), count the cached blocks per queue (summed per workgroup in
+// LDS when the workgroup lies in one instance).  A rebuild of the index alone
+// leaves the counts, which commits and Add() keep current.
+__global__ void k_index_fill(DevCtx c, int census)
 {
-    long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    long long total = (long long)c.n_inst * c.N;
-    if (g >= total) return;
-    if (!(c.meta[g] & SAE_META_VALID)) return;
-    int inst = (int)(g / c.N);
-    int32_t b = (int32_t)(g - (long long)inst * c.N);
-    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    if (!index_insert(tab, c.index_mask, c.hash[g], b)) set_status(c.status, SAE_ST_INDEX_FULL);
+    __shared__ int32_t cnt[SAE_MAX_QUEUES];
+    if (threadIdx.x < SAE_MAX_QUEUES) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long total = (long long)c.n_inst * c.N;
+    const long long g0 = (long long)blockIdx.x * blockDim.x;
+    const long long g1 = (g0 + blockDim.x < total ? g0 + blockDim.x : total) - 1;
+    const int i0 = (int)(g0 / c.N);
+    const bool one_inst = (int)(g1 / c.N) == i0;
+    if (g < total) {
+        const uint32_t m = c.meta[g];
+        if (m & SAE_META_VALID) {
+            const int inst = (int)(g / c.N);
+            const int32_t b = (int32_t)(g - (long long)inst * c.N);
+            IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+            if (!index_insert(tab, c.index_mask, c.hash[g], b)) set_status(c.status, SAE_ST_INDEX_FULL);
+            if (census) {
+                if (one_inst) atomicAdd(&cnt[meta_queue(m)], 1);
+                else atomicAdd(counter_slot(c, inst, blockIdx.x) + SAE_CF_RES + meta_queue(m), 1);
+            }
+        }
+    }
+    __syncthreads();
+    if (census && one_inst && threadIdx.x < SAE_MAX_QUEUES && cnt[threadIdx.x])
+        atomicAdd(counter_slot(c, i0, blockIdx.x) + SAE_CF_RES + threadIdx.x, cnt[threadIdx.x]);
 }
 
 // Rebuild recently_evicted from the ring (drops tombstones).
@@ -265,6 +286,9 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     c.access_count[g] = 0;
     IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
     if (!index_insert(tab, c.index_mask, h, b)) set_status(c.status, SAE_ST_INDEX_FULL);
+    int32_t *cs = counter_slot(c, inst, i);
+    atomicAdd(cs + SAE_CF_RES + meta_queue(m), 1);
+    if (c.state[inst].learn & SAE_LEARN_TOKEN_EMA) atomicAdd(cs + SAE_CF_TADD + meta_type(m) % SAE_N_TYPES, 1);
     // recently_evicted: a hit counts one miss after eviction (Algorithm 1, Add)
     GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
     GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
@@ -274,7 +298,6 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
         if (atomicCAS(&gt[s].hash, h, SAE_TOMB_HASH) == h) {
             uint32_t old = atomicOr(&ring[rp].tq, SAE_TQ_CONSUMED);
             if (!(old & SAE_TQ_CONSUMED)) {
-                int32_t *cs = counter_slot(c, inst, i);
                 atomicAdd(cs + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
                 if (((c.struct_mask >> ((old >> 3) & 7u)) & 1u) && (c.state[inst].learn & SAE_LEARN_DECAY_POWER))
                     atomicAdd(cs + SAE_CF_BMISS + ((old >> SAE_TQ_BIN_SHIFT) & (SAE_N_BINS - 1)), 1);
@@ -324,6 +347,15 @@ __global__ void k_ref_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *i
     else meta_and(c.meta, g, (uint32_t)(~SAE_META_REF) & 0xFFFFu);
 }
 
+// Counter field of the prefix match's f-th hit count: queues, then positional
+// bins, then block types.
+__device__ __forceinline__ int pm_field(int f)
+{
+    if (f < SAE_MAX_QUEUES) return SAE_CF_HITS + f;
+    if (f < SAE_MAX_QUEUES + SAE_N_BINS) return SAE_CF_BHITS + (f - SAE_MAX_QUEUES);
+    return SAE_CF_THITS + (f - SAE_MAX_QUEUES - SAE_N_BINS);
+}
+
 // ---------------------------------------------------------------------------
 // Strict prefix matching, one wave per request.  Lanes probe 64 consecutive
 // hashes; the lowest missing lane ends the match and no later chunk is probed.
@@ -339,7 +371,7 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                                                           const int32_t *lens, const int32_t *inst_a, int32_t now,
                                                           uint32_t flags, int32_t *match_len, int32_t *matched_ids)
 {
-    constexpr int NC = SAE_MAX_QUEUES + SAE_N_BINS;
+    constexpr int NC = SAE_MAX_QUEUES + SAE_N_BINS + SAE_N_TYPES;  // queue, bin and type hits
     __shared__ int32_t winst[kThreads / SAE_WAVE];
     __shared__ uint32_t wg_hits[NC];
     const int lane = (int)__lane_id();
@@ -351,8 +383,10 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
     int inst = (active && inst_a) ? inst_a[r] : 0;
     const bool inst_ok = inst >= 0 && inst < c.n_inst;
     // positional-bin hits are gathered only while the decay-power learner is on
-    const bool bins = (flags & SAE_PM_STATS) && c.struct_mask && active && inst_ok &&
-                      (c.state[inst].learn & SAE_LEARN_DECAY_POWER);
+    const uint32_t ilearn = (active && inst_ok) ? c.state[inst].learn : 0u;
+    const bool bins = (flags & SAE_PM_STATS) && c.struct_mask && (ilearn & SAE_LEARN_DECAY_POWER);
+    // hits per block type are gathered only for the text-form token rule
+    const bool types = (flags & SAE_PM_STATS) && (ilearn & SAE_LEARN_TOKEN_EMA);
     if (threadIdx.x < NC) wg_hits[threadIdx.x] = 0;
     if (lane == 0) winst[wave] = (active && inst_ok) ? inst : -1;
     uint32_t qcount[NC];
@@ -387,12 +421,14 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                 const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
                 const int lim = min(first, len - j0);
                 const bool hit = lane < lim;
-                int q = 0;
+                int q = 0, ty = 0;
                 uint32_t bin = 0;
                 if (hit) {
                     const long long g = base + id;
                     const uint32_t off = bins ? c.off[g] : 0u;  // loaded beside meta, not after it
-                    q = meta_queue(c.meta[g]);
+                    const uint32_t mt = c.meta[g];
+                    q = meta_queue(mt);
+                    ty = meta_type(mt) % SAE_N_TYPES;
                     if (bins && ((c.struct_mask >> q) & 1u)) bin = pos_bin(off);
                     if (touch) {
                         c.la[g] = now;
@@ -411,6 +447,11 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
 #pragma unroll
                         for (int bb = 0; bb < SAE_N_BINS; ++bb)
                             qcount[SAE_MAX_QUEUES + bb] += (uint32_t)__popcll(__ballot(sh && bin == (uint32_t)bb));
+                    }
+                    if (types) {
+#pragma unroll
+                        for (int tt = 0; tt < SAE_N_TYPES; ++tt)
+                            qcount[SAE_MAX_QUEUES + SAE_N_BINS + tt] += (uint32_t)__popcll(__ballot(hit && ty == tt));
                     }
                 }
                 if (intervals) {
@@ -459,20 +500,18 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
     if (i0 < 0) return;
     if (uniform) {
         if (lane == 0 && active && inst_ok)
+#pragma unroll
             for (int qq = 0; qq < NC; ++qq)
                 if (qcount[qq]) atomicAdd(&wg_hits[qq], qcount[qq]);
         __syncthreads();
         const int f = threadIdx.x;
-        if (f < NC && wg_hits[f] && (f >= SAE_MAX_QUEUES || f < c.Q)) {
-            const int field = f < SAE_MAX_QUEUES ? SAE_CF_HITS + f : SAE_CF_BHITS + (f - SAE_MAX_QUEUES);
-            atomicAdd(counter_slot(c, i0, blockIdx.x) + field, (int)wg_hits[f]);
-        }
+        if (f < NC && wg_hits[f] && (f >= SAE_MAX_QUEUES || f < c.Q))
+            atomicAdd(counter_slot(c, i0, blockIdx.x) + pm_field(f), (int)wg_hits[f]);
     } else if (lane == 0 && active && inst_ok) {
         int32_t *cs = counter_slot(c, inst, blockIdx.x);
-        for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
-            if (qq < c.Q && qcount[qq]) atomicAdd(cs + SAE_CF_HITS + qq, (int)qcount[qq]);
-        for (int bb = 0; bb < SAE_N_BINS; ++bb)
-            if (qcount[SAE_MAX_QUEUES + bb]) atomicAdd(cs + SAE_CF_BHITS + bb, (int)qcount[SAE_MAX_QUEUES + bb]);
+#pragma unroll
+        for (int f = 0; f < NC; ++f)
+            if (qcount[f] && (f >= SAE_MAX_QUEUES || f < c.Q)) atomicAdd(cs + pm_field(f), (int)qcount[f]);
     }
 }
 
@@ -600,6 +639,7 @@ __global__ void k_commit(DevCtx c, const int32_t *decision)
         const int32_t p = c.parent[g];
         atomicAdd(&sums[SAE_CF_EVICTED + meta_type(m) % SAE_N_TYPES], 1);
         atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
+        atomicSub(&sums[SAE_CF_RES + meta_queue(m)], 1);
         meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
         IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
         index_erase(tab, c.index_mask, h);
@@ -673,7 +713,7 @@ hipError_t launch_index_build(const DevCtx &c, hipStream_t s)
     hipLaunchKernelGGL(k_clear_all, dim3(grid_for(n)), dim3(kThreads), 0, s, c, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c);
+    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c, 1);
     return hipGetLastError();
 }
 
@@ -683,7 +723,7 @@ hipError_t launch_index_rebuild(const DevCtx &c, hipStream_t s)
     hipLaunchKernelGGL(k_clear_all, dim3(grid_for(nidx)), dim3(kThreads), 0, s, c, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c);
+    hipLaunchKernelGGL(k_index_fill, dim3(grid_for((long long)c.n_inst * c.N)), dim3(kThreads), 0, s, c, 0);
     return hipGetLastError();
 }
 

@@ -165,13 +165,70 @@ __device__ void decay_power(InstState &s)
     for (int b = 0; b < SAE_N_BINS; ++b) s.bin_hits[b] = s.bin_missed[b] = 0;
 }
 
-// Algorithms 3 and 2 and the decay-power learner on the lanes of one wave,
-// which touch disjoint fields: lane l < 5 updates token type l (Algorithm 3),
-// lane 8 + q queue q (Algorithm 2), lane 63 gamma.
+// The appendix text's token-weight rule for type t (one lane): an EMA toward
+// 1 + 5 r_miss + 2 r_reuse, counters decayed by floor(0.99 x).
+__device__ void token_weight_ema(InstState &s, int t)
+{
+    const int32_t ev = s.evicted[t], mi = s.missed[t], h = s.type_hits[t], a = s.type_added[t];
+    const float r_miss = ev > 0 ? (float)mi / (float)ev : 0.0f;
+    const float r_reuse = (h + a) > 0 ? (float)h / (float)(h + a) : 0.0f;
+    const float target = 1.0f + r_miss * 5.0f + r_reuse * 2.0f;
+    s.w[t] = clampf((1.0f - s.eta) * s.w[t] + s.eta * target, 0.1f, 5.0f);
+    s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
+    s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
+    s.type_hits[t] = (int32_t)(((long long)h * 99) / 100);
+    s.type_added[t] = (int32_t)(((long long)a * 99) / 100);
+}
+
+// The appendix text's queue-weight rule over all queues (one lane):
+// relative efficiency (hits per share of the cached blocks) to the power 1/T,
+// blended as beta alpha + (1 - beta) target.
+__device__ void queue_weights_rel(const DevCtx &c, InstState &s)
+{
+    int32_t total = 0;
+    for (int q = 0; q < c.Q; ++q) total += s.resident[q];
+    float E[SAE_MAX_QUEUES];
+    float e_sum = 0.0f;
+    int m = 0;
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+        E[q] = 0.0f;
+        if (q < c.Q && c.kind[q] != SAE_KIND_EVICT_FIRST && s.resident[q] > 0 && total > 0) {
+            const float share = (float)s.resident[q] / (float)total;
+            E[q] = (float)s.hits[q] / share;
+            e_sum = e_sum + E[q];
+            ++m;
+        }
+    }
+    if (m > 0) {
+        const float e_mean = e_sum / (float)m;
+        if (e_mean > 0.0f) {
+#pragma unroll
+            for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+                if (!(q < c.Q && c.kind[q] != SAE_KIND_EVICT_FIRST && s.resident[q] > 0)) continue;
+                const float x = E[q] / e_mean;
+                const float tgt = (s.T == 1.0f || x == 0.0f) ? x : dsr::exp(dsr::ln(x) / s.T);
+                s.alpha[q] = clampf(s.beta * s.alpha[q] + (1.0f - s.beta) * tgt, 0.1f, 3.0f);
+            }
+        }
+    }
+    for (int q = 0; q < c.Q; ++q) {
+        if (c.kind[q] == SAE_KIND_EVICT_FIRST) continue;
+        s.hits[q] = 0;
+        s.evictions[q] = 0;
+    }
+}
+
+// Token-weight, queue-weight and decay-power learners on the lanes of one
+// wave, which touch disjoint fields: lane l < 5 updates token type l
+// (Algorithm 3 or the text's rule), lane 8 + q queue q (Algorithm 2), lane 16
+// every queue (the text's rule), lane 63 gamma.
 __device__ void learners_23_gamma(const DevCtx &c, InstState &s, int l)
 {
     if (l < SAE_N_TYPES) {
-        if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
+        if (s.learn & SAE_LEARN_TOKEN_EMA) {
+            token_weight_ema(s, l);
+        } else if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
             // Algorithm 3: raise the weight of types evicted too aggressively;
             // both counters decay by lambda = 0.99, applied as floor(99 x / 100).
             const int t = l;
@@ -185,6 +242,8 @@ __device__ void learners_23_gamma(const DevCtx &c, InstState &s, int l)
             s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
             s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
         }
+    } else if (l == 16) {
+        if (s.learn & SAE_LEARN_QUEUE_REL) queue_weights_rel(c, s);
     } else if (l >= 8 && l < 8 + c.Q) {
         const int q = l - 8;
         if ((s.learn & SAE_LEARN_QUEUE_WEIGHTS) && c.kind[q] != SAE_KIND_EVICT_FIRST) {
@@ -247,7 +306,10 @@ __global__ void __launch_bounds__(kLearnThreads) k_feedback(DevCtx c, uint32_t f
         else if (f < SAE_CF_EVICTIONS) s.hits[f - SAE_CF_HITS] += sum;
         else if (f < SAE_CF_BHITS) s.evictions[f - SAE_CF_EVICTIONS] += sum;
         else if (f < SAE_CF_BMISS) s.bin_hits[f - SAE_CF_BHITS] += sum;
-        else s.bin_missed[f - SAE_CF_BMISS] += sum;
+        else if (f < SAE_CF_THITS) s.bin_missed[f - SAE_CF_BMISS] += sum;
+        else if (f < SAE_CF_TADD) s.type_hits[f - SAE_CF_THITS] += sum;
+        else if (f < SAE_CF_RES) s.type_added[f - SAE_CF_TADD] += sum;
+        else s.resident[f - SAE_CF_RES] += sum;
     }
     if (f == 0) due = learn && (s.pending || (flags & SAE_FB_FORCE));
     __syncthreads();

@@ -259,6 +259,10 @@ sae_status sae_set_params(sae_ctx *c, int32_t inst, const sae_params *p, sae_str
         if (!(p->sigma[q] > 0.0f)) return fail(c, SAE_ERR_ARG, "sigma must be > 0");
     if (!(p->gamma > 0.0f) || !(p->temperature > 0.0f)) return fail(c, SAE_ERR_ARG, "gamma and temperature must be > 0");
     if (p->K < 0) return fail(c, SAE_ERR_ARG, "K must be >= 0");
+    if ((p->learn & SAE_LEARN_TOKEN_WEIGHTS) && (p->learn & SAE_LEARN_TOKEN_EMA))
+        return fail(c, SAE_ERR_ARG, "choose one token-weight rule (Algorithm 3 or the text's EMA)");
+    if ((p->learn & SAE_LEARN_QUEUE_WEIGHTS) && (p->learn & SAE_LEARN_QUEUE_REL))
+        return fail(c, SAE_ERR_ARG, "choose one queue-weight rule (Algorithm 2 or the text's relative rule)");
     InstState h;
     memset(&h, 0, sizeof(h));
     memcpy(h.w, p->w, sizeof(h.w));
@@ -323,6 +327,9 @@ sae_status sae_get_counters(sae_ctx *c, int32_t inst, sae_counters *out, sae_str
     out->n_updates = h.n_updates;
     memcpy(out->bin_hits, h.bin_hits, sizeof(out->bin_hits));
     memcpy(out->bin_missed, h.bin_missed, sizeof(out->bin_missed));
+    memcpy(out->type_hits, h.type_hits, sizeof(out->type_hits));
+    memcpy(out->type_added, h.type_added, sizeof(out->type_added));
+    memcpy(out->resident, h.resident, sizeof(out->resident));
     return SAE_OK;
 }
 
@@ -344,6 +351,9 @@ sae_status sae_set_counters(sae_ctx *c, int32_t inst, const sae_counters *in, sa
     h.n_updates = in->n_updates;
     memcpy(h.bin_hits, in->bin_hits, sizeof(h.bin_hits));
     memcpy(h.bin_missed, in->bin_missed, sizeof(h.bin_missed));
+    memcpy(h.type_hits, in->type_hits, sizeof(h.type_hits));
+    memcpy(h.type_added, in->type_added, sizeof(h.type_added));
+    memcpy(h.resident, in->resident, sizeof(h.resident));
     e = hipMemcpyAsync(c->dc.state + inst, &h, sizeof(h), hipMemcpyHostToDevice, S(stream));
     if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_set_counters write");

@@ -38,7 +38,10 @@
 #define SAE_CF_EVICTIONS 18  // 8 fields, queue_evictions[q]
 #define SAE_CF_BHITS 26      // 8 fields, hits of structural blocks per positional bin
 #define SAE_CF_BMISS 34      // 8 fields, misses after eviction per positional bin
-#define SAE_CF_N 42
+#define SAE_CF_THITS 42      // 5 fields, prefix-match hits per block type
+#define SAE_CF_TADD 47       // 5 fields, blocks added per type
+#define SAE_CF_RES 52        // 8 fields, change of the cached blocks per queue
+#define SAE_CF_N 60
 #define SAE_CF_STRIDE 64
 
 // recently_evicted entry bits: tau | queue << 3 | consumed | positional bin << 9
@@ -67,6 +70,9 @@ struct InstState {
     int32_t last_d;       // size of the last committed decision
     int32_t bin_hits[SAE_N_BINS];    // decay-power learner counters
     int32_t bin_missed[SAE_N_BINS];
+    int32_t type_hits[SAE_N_TYPES];  // text-form token-weight counters
+    int32_t type_added[SAE_N_TYPES];
+    int32_t resident[SAE_MAX_QUEUES];  // cached blocks per queue
     long long ivl_n[SAE_MAX_QUEUES];      // Algorithm 4: intervals recorded so far, per queue
     long long ivl_start[SAE_MAX_QUEUES];  // first interval still in the buffer (before the cap)
 };

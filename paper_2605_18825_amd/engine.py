@@ -90,7 +90,8 @@ class DeviceBackend:
         c = api.sae_get_counters(self.ctx, i)
         return dict(evicted=list(c.evicted), missed=list(c.missed), hits=list(c.hits[:self.Q]),
                     evictions=list(c.evictions[:self.Q]), ev_count=int(c.eviction_count), pending=bool(c.pending),
-                    n_updates=int(c.n_updates), bin_hits=list(c.bin_hits), bin_missed=list(c.bin_missed))
+                    n_updates=int(c.n_updates), bin_hits=list(c.bin_hits), bin_missed=list(c.bin_missed),
+                    type_hits=list(c.type_hits), type_added=list(c.type_added), resident=list(c.resident[:self.Q]))
 
     def params(self, i):
         p = api.sae_get_params(self.ctx, i)

@@ -35,7 +35,8 @@ class Pair:
         K = max_k if K is None else K
         self.prm = oracle.Params(Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma, eta=eta, T=T, beta=beta, K=K,
                                  learn_w=bool(learn & 1), learn_alpha=bool(learn & 2), beta_ln=beta_ln,
-                                 learn_ln=bool(learn & 4), learn_gamma=bool(learn & 8))
+                                 learn_ln=bool(learn & 4), learn_gamma=bool(learn & 8),
+                                 learn_w_ema=bool(learn & 16), learn_alpha_rel=bool(learn & 32))
         self.oc = oracle.OracleCache(N, kinds, self.prm, ghost_window=ghost_window or None)
         self.tau_oracle = oracle.block_type(pool["counts"])
         self.oc.bind(pool["last_access"], pool["queue"], self.tau_oracle, pool["ntok"], pool["ob"], pool["omax"],
@@ -158,6 +159,9 @@ class Pair:
         assert bool(c.pending) == o.pending
         assert list(c.bin_hits) == o.bin_hits, ("bin_hits", list(c.bin_hits), o.bin_hits)
         assert list(c.bin_missed) == o.bin_missed, ("bin_missed", list(c.bin_missed), o.bin_missed)
+        assert list(c.type_hits) == o.type_hits, ("type_hits", list(c.type_hits), o.type_hits)
+        assert list(c.type_added) == o.type_added, ("type_added", list(c.type_added), o.type_added)
+        assert list(c.resident[:self.Q]) == o.resident(), ("resident", list(c.resident[:self.Q]), o.resident())
 
     def check_pool(self):
         torch.cuda.synchronize()

@@ -16,7 +16,8 @@ class OracleBackend:
         for i in self.insts:
             prm = oracle.Params(self.Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma, eta=eta, T=T, beta=beta,
                                 K=K, learn_w=bool(learn & 1), learn_alpha=bool(learn & 2), learn_ln=bool(learn & 4),
-                                learn_gamma=bool(learn & 8))
+                                learn_gamma=bool(learn & 8), learn_w_ema=bool(learn & 16),
+                                learn_alpha_rel=bool(learn & 32))
             self.c[i] = oracle.OracleCache(capacity, kinds, prm, ghost_window=ghost_window)
 
     def prefix_match(self, now, insts, prompts):

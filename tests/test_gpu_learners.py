@@ -13,14 +13,16 @@ from harness import Pair, say  # noqa: E402
 from paper_2605_18825_amd import api  # noqa: E402
 
 ALL = api.LEARN_TOKEN_WEIGHTS | api.LEARN_QUEUE_WEIGHTS | api.LEARN_LOGNORMAL | api.LEARN_DECAY_POWER
+# the appendix text's token and queue rules in place of Algorithms 3 and 2
+TEXT = api.LEARN_TOKEN_EMA | api.LEARN_QUEUE_REL | api.LEARN_LOGNORMAL | api.LEARN_DECAY_POWER
 FLAGS = api.PM_TOUCH | api.PM_STATS | api.PM_INTERVALS
 
 
-def five_queue_pair(n_blocks, seed, max_requests, **over):
+def five_queue_pair(n_blocks, seed, max_requests, learn=ALL, **over):
     """The 5-queue layout (evict-first, structural, chat, agent, default)."""
     cfg = synth.pool_config("large")
     pool = synth.make_pool(cfg, n_blocks=n_blocks, seed=seed)
-    p = Pair(cfg["kinds"], pool, over.pop("max_k", 256), mu=cfg["mu"], sigma=cfg["sigma"], learn=ALL,
+    p = Pair(cfg["kinds"], pool, over.pop("max_k", 256), mu=cfg["mu"], sigma=cfg["sigma"], learn=learn,
              max_requests=max_requests, **over)
     return p, pool, cfg
 
@@ -92,17 +94,22 @@ def test_interval_buffer_cap():
         p.close()
 
 
-def test_learning_cycle_all_learners():
+@pytest.mark.parametrize("rules", ["algorithms", "text"])
+def test_learning_cycle_all_learners(rules):
     """Prefix matches, decisions with commit, re-added victims and the
     learners every K evictions: all parameters, counters and buffers agree
-    after every step."""
-    p, pool, cfg = five_queue_pair(8192, 4103, 512, K=200)
+    after every step.  `text`: the appendix text's token and queue rules from
+    the paper's initial token weights."""
+    if rules == "text":
+        p, pool, cfg = five_queue_pair(8192, 4105, 512, learn=TEXT, K=200, w=list(api.PAPER_INIT_W), T=2.0)
+    else:
+        p, pool, cfg = five_queue_pair(8192, 4103, 512, K=200)
     try:
         rng = np.random.default_rng(3)
         now = pool["now"]
         gamma0 = float(p.prm.gamma)
         for step in range(10):
-            say("learners: cycle step %d" % step)
+            say("learners: %s cycle step %d" % (rules, step))
             R, L = synth.make_requests(pool["chains"], 512, 48, 0.6, 100 + step)
             p.prefix_match(R, L, now, FLAGS)
             lists, key, dec = p.select(now, 256, commit=True)
@@ -144,6 +151,10 @@ def test_interval_argument_errors():
             api.sae_prefix_match(p.ctx, R, L, 5, api.PM_INTERVALS, ml, matched_ids=mid)
         with pytest.raises(api.SaeError, match="log-normal"):
             api.sae_get_intervals(p.ctx, 0, 1)
+        with pytest.raises(api.SaeError, match="token-weight rule"):
+            api.sae_set_params(p.ctx, 0, api.make_params(5, learn=api.LEARN_TOKEN_WEIGHTS | api.LEARN_TOKEN_EMA))
+        with pytest.raises(api.SaeError, match="queue-weight rule"):
+            api.sae_set_params(p.ctx, 0, api.make_params(5, learn=api.LEARN_QUEUE_WEIGHTS | api.LEARN_QUEUE_REL))
         assert api.sae_get_intervals(p.ctx, 0, 2) == []
         assert not p.status()
     finally:

@@ -33,6 +33,13 @@ def test_trace_balanced_all_learners():
     assert o.n_updates > 0 and len(o.ivl[2]) + len(o.ivl[3]) > 0
 
 
+def test_trace_balanced_text_rules():
+    """The appendix text's token and queue rules with Algorithm 4 and the
+    decay power, from the paper's initial token weights."""
+    rd, ro, _ = run_pair("trace_balanced", 1200, [0], learn=60, check_every=200, w=[2.0, 1.5, 1.0, 1.0, 0.1])
+    assert ro.be.c[0].n_updates > 0
+
+
 def test_batched_sweep_all_learners():
     """Interval placement across 256 instances of one context."""
     rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], learn=15, check_every=300)

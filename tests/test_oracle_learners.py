@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 from oracle import _native as N
-from oracle.policy import (IVL_CAP, LOGNORMAL, N_BINS, RECENCY, STRUCTURAL, OracleCache, Params,
+from oracle.policy import (EVICT_FIRST, IVL_CAP, LOGNORMAL, N_BINS, RECENCY, STRUCTURAL, OracleCache, Params,
                            sample_moments)
 
 F32 = np.float32
@@ -284,3 +284,89 @@ def test_bins_only_while_the_learner_is_on():
     c.commit(np.array([7], np.int32))
     c.insert([7], [h[7]], [6], [20], [0], [0], [16], [7], [7])
     assert c.bin_missed == [0] * N_BINS and c.missed[0] == 1
+
+
+# ------------------------------------------- the appendix text's rule forms
+def _form_cache(kinds=(EVICT_FIRST, STRUCTURAL, LOGNORMAL, RECENCY), n=64, **kw):
+    prm = Params(len(kinds), K=4, learn_w=False, learn_alpha=False, learn_w_ema=True, learn_alpha_rel=True, **kw)
+    return OracleCache(n, list(kinds), prm, ghost_window=1000)
+
+
+def test_token_weight_ema_worked_examples():
+    c = _form_cache()
+    c.prm.w[:] = [2.0, 0.1, 4.99, 1.0, 1.0]
+    c.evicted = [20, 0, 10, 0, 0]
+    c.missed = [5, 0, 10, 0, 0]
+    c.type_hits = [30, 0, 10, 0, 7]
+    c.type_added = [10, 0, 0, 0, 7]
+    c.feedback(force=True)
+    # target 1 + 5 (5/20) + 2 (30/40) = 3.75: 0.99 * 2 + 0.01 * 3.75
+    assert abs(float(c.prm.w[0]) - 2.0175) < 1e-6
+    assert abs(float(c.prm.w[1]) - 0.109) < 1e-7                  # no data: target 1
+    assert c.prm.w[2] == F32(5.0)                                 # target 8, clamped at 5
+    assert abs(float(c.prm.w[4]) - 1.01) < 1e-6                   # r_reuse 1/2: target 2
+    assert c.evicted[0] == 19 and c.missed[0] == 4 and c.type_hits[0] == 29 and c.type_added[0] == 9
+
+
+def test_token_weight_ema_converges_to_its_target():
+    c = _form_cache()
+    c.prm.w[:] = 1.0
+    for _ in range(700):
+        c.evicted[:] = [100, 100, 100, 100, 100]
+        c.missed[:] = [25, 0, 50, 10, 0]
+        c.type_hits[:] = [90, 60, 0, 20, 2]
+        c.type_added[:] = [10, 40, 100, 80, 98]
+        c.feedback(force=True)
+    want = [1 + 5 * 0.25 + 2 * 0.9, 1 + 2 * 0.6, 1 + 5 * 0.5, 1 + 5 * 0.1 + 2 * 0.2, 1 + 2 * 0.02]
+    assert np.allclose(c.prm.w, want, atol=5e-3), (c.prm.w, want)
+    assert c.prm.w[0] > c.prm.w[2] > c.prm.w[1] > c.prm.w[3] > c.prm.w[4]
+
+
+def test_queue_weight_relative_efficiency_worked_examples():
+    c = _form_cache()
+    c.valid[:] = False
+    c.valid[:60] = True
+    c.queue[:] = np.repeat([0, 1, 2, 3], 16)[:64]
+    c.queue[:60] = np.concatenate([np.full(10, 0), np.full(30, 1), np.full(10, 2), np.full(10, 3)])
+    assert c.resident() == [10, 30, 10, 10]
+    c.hits = [9, 30, 10, 0]
+    c.evictions = [1, 1, 1, 1]
+    c.feedback(force=True)
+    # shares 30/60, 10/60, 10/60: E = 60, 60, 0, mean 40: targets 1.5, 1.5, 0
+    assert abs(float(c.prm.alpha[1]) - (0.1 + 0.9 * 1.5)) < 1e-6
+    assert abs(float(c.prm.alpha[2]) - (0.1 + 0.9 * 1.5)) < 1e-6
+    assert c.prm.alpha[3] == F32(0.1)                             # 0.1 * 1 + 0: at the floor
+    assert c.prm.alpha[0] == F32(1.0) and c.hits[0] == 9          # evict-first untouched
+    assert c.hits[1:] == [0, 0, 0] and c.evictions[1:] == [0, 0, 0]
+    # temperature 2: the square root of the relative efficiency
+    c.prm.alpha[:] = 1.0
+    c.prm.T = F32(2.0)
+    c.hits = [0, 30, 10, 0]
+    c.feedback(force=True)
+    assert abs(float(c.prm.alpha[1]) - (0.1 + 0.9 * math.sqrt(1.5))) < 2e-6
+    # equal efficiencies: every target is 1
+    c.prm.alpha[:] = [1.0, 2.0, 0.5, 3.0]
+    c.hits = [0, 30, 10, 10]
+    c.feedback(force=True)
+    assert np.allclose(c.prm.alpha[1:], [0.1 * 2.0 + 0.9, 0.1 * 0.5 + 0.9, 0.1 * 3.0 + 0.9], atol=1e-6)
+    # no hits at all: nothing moves
+    before = c.prm.alpha.copy()
+    c.feedback(force=True)
+    assert np.array_equal(before, c.prm.alpha)
+
+
+def test_text_forms_count_only_when_chosen():
+    c = _form_cache(kinds=(STRUCTURAL, RECENCY), n=16)
+    h = _bind_chains(c, [list(range(8))], np.zeros(16, np.int32), np.zeros(16, np.int32))
+    c.tau[:] = [0, 0, 1, 1, 2, 3, 3, 4] + [0] * 8
+    c.prefix_match(h[None, :8], [8], now=10)
+    assert c.type_hits == [2, 2, 1, 2, 1]
+    c.commit(np.array([7], np.int32))
+    c.insert([7], [h[7]], [6], [20], [1], [4], [16], [0], [0])
+    assert c.type_added == [0, 0, 0, 0, 1] and c.resident() == [7, 1]
+    off = _ln_cache(n=16, kinds=(STRUCTURAL, RECENCY), learn_ln=False)
+    h = _bind_chains(off, [list(range(8))], np.zeros(16, np.int32), np.zeros(16, np.int32))
+    off.prefix_match(h[None, :8], [8], now=10)
+    assert off.type_hits == [0] * 5
+    with pytest.raises(AssertionError):
+        Params(2, learn_w=True, learn_w_ema=True)

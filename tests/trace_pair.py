@@ -55,7 +55,8 @@ def check_pool(dev, orc, i):
 
 def check_state(dev, orc, i):
     cd, co = dev.counters(i), orc.counters(i)
-    for key in ("evicted", "missed", "hits", "evictions", "ev_count", "pending", "n_updates", "bin_hits", "bin_missed"):
+    for key in ("evicted", "missed", "hits", "evictions", "ev_count", "pending", "n_updates", "bin_hits", "bin_missed",
+                "type_hits", "type_added", "resident"):
         assert cd[key] == co[key], "instance %d: %s %s vs oracle %s" % (i, key, cd[key], co[key])
     (wd, ad), (wo, ao) = dev.params(i), orc.params(i)
     assert np.array_equal(wd.view(np.uint32), wo.view(np.uint32)), "instance %d: w %s vs %s" % (i, wd, wo)
@@ -66,13 +67,13 @@ def check_state(dev, orc, i):
     assert gd.view(np.uint32) == go.view(np.uint32), "instance %d: gamma %r vs %r" % (i, gd, go)
 
 
-def run_pair(name, steps, oracle_insts, n_inst=None, capacity=None, learn=3, check_every=100, **gen_over):
+def run_pair(name, steps, oracle_insts, n_inst=None, capacity=None, learn=3, check_every=100, w=1.0, **gen_over):
     cfg = TRACE_CONFIGS[name]
     n_inst = cfg["n_inst"] if n_inst is None else n_inst
     capacity = cfg["capacity"] if capacity is None else capacity
     gens = trace_gens(name, n_inst, **gen_over)
-    dev = DeviceBackend(n_inst, capacity, KINDS, ROLES, cfg["max_k"], MU, SIGMA, cfg["K"], learn)
-    orc = OracleBackend(oracle_insts, capacity, KINDS, ROLES, MU, SIGMA, cfg["K"], learn)
+    dev = DeviceBackend(n_inst, capacity, KINDS, ROLES, cfg["max_k"], MU, SIGMA, cfg["K"], learn, w=w)
+    orc = OracleBackend(oracle_insts, capacity, KINDS, ROLES, MU, SIGMA, cfg["K"], learn, w=w)
     rd = Replay(dev, n_inst, capacity, cfg["k_min"], cfg["max_k"], cfg["concurrency"])
     ro = Replay(orc, n_inst, capacity, cfg["k_min"], cfg["max_k"], cfg["concurrency"], insts=oracle_insts)
     try:
