@@ -282,6 +282,70 @@ class OracleCache:
             ev[victim] = False
         return np.array(out, np.int32)
 
+    def cascade_literal(self, now, k):
+        """Algorithm 1's Evict() called k times on the live state (no
+        snapshot): after each removal the victim's parent loses a child, and a
+        parent left with none is evictable (valid, unreferenced, now a leaf)
+        for the next call.  Written as the algorithm states it: every call
+        rebuilds the evictable set and scans it (strict '<', blocks in id
+        order).  Slow; for tiny pools."""
+        key, _ = self.keys(now)
+        P = key.view(np.float32)
+        child = self.child_count.copy()
+        gone = np.zeros(self.N, bool)
+        ef = [q for q in range(self.Q) if self.kind[q] == EVICT_FIRST]
+        out = []
+        for _ in range(k):
+            ev = self.valid & ~gone & (child == 0) & (self.ref_count == 0)
+            victim = None
+            if ef:
+                best = None
+                for b in range(self.N):
+                    if ev[b] and self.queue[b] == ef[0] and (best is None or self.ntok[b] < best):
+                        best, victim = self.ntok[b], b
+            if victim is None:
+                best = math.inf
+                for b in range(self.N):
+                    if ev[b] and self.kind[self.queue[b]] != EVICT_FIRST and (victim is None or P[b] < best):
+                        best, victim = P[b], b
+            if victim is None:
+                break
+            out.append(victim)
+            gone[victim] = True
+            if self.parent[victim] >= 0:
+                child[self.parent[victim]] -= 1
+        return np.array(out, np.int32)
+
+    def decide_cascade(self, now, k):
+        """The same sequence as `cascade_literal`, with two heaps: the
+        evict-first queue by (num_tokens, id) and the other queues by
+        (P, id); a parent whose last child leaves is pushed with its own key."""
+        import heapq
+        key, _ = self.keys(now)
+        child = self.child_count.copy()
+        ev = self.evictable()
+        h1, h2 = [], []
+        for b in np.nonzero(ev)[0].tolist():
+            if self.kind[self.queue[b]] == EVICT_FIRST:
+                h1.append((int(self.ntok[b]), b))
+            else:
+                h2.append((int(key[b]), b))
+        heapq.heapify(h1)
+        heapq.heapify(h2)
+        out = []
+        while len(out) < k and (h1 or h2):
+            _, v = heapq.heappop(h1 if h1 else h2)
+            out.append(v)
+            par = int(self.parent[v])
+            if par >= 0:
+                child[par] -= 1
+                if child[par] == 0 and self.valid[par] and self.ref_count[par] == 0:
+                    if self.kind[self.queue[par]] == EVICT_FIRST:
+                        heapq.heappush(h1, (int(self.ntok[par]), par))
+                    else:
+                        heapq.heappush(h2, (int(key[par]), par))
+        return np.array(out, np.int32)
+
     def score_select(self, now, k, commit=False):
         lists, key, p = self.select_per_queue(now, k)
         decision = self.decide(lists, key, k)

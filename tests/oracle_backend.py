@@ -7,9 +7,10 @@ import oracle
 
 class OracleBackend:
     def __init__(self, insts, capacity, kinds, roles, mu, sigma, K, learn, w=1.0, alpha=1.0, gamma=1.0, eta=0.01,
-                 T=1.0, beta=0.1, ghost_window=None):
+                 T=1.0, beta=0.1, ghost_window=None, cascade=False):
         self.insts = list(insts)
         self.intervals = bool(learn & 4)
+        self.cascade = bool(cascade)  # Algorithm 1 one victim at a time instead of a snapshot decision
         self.roles = list(roles)
         self.Q = len(kinds)
         self.c = {}
@@ -39,7 +40,11 @@ class OracleBackend:
     def evict(self, now, k):
         out = {}
         for i in self.insts:
-            if k[i] > 0:
+            if k[i] > 0 and self.cascade:
+                dec = self.c[i].decide_cascade(now, int(k[i]))
+                self.c[i].commit(dec)
+                out[i] = dec
+            elif k[i] > 0:
                 _, _, dec = self.c[i].score_select(now, int(k[i]), commit=True)
                 out[i] = dec
             else:
