@@ -135,6 +135,10 @@ def main():
         c = caches[i % R]
         c["out"].run(c["ctx"], c["now"], k, 0, stream=stream)
 
+    def select_cascade(i):
+        c = caches[i % R]
+        c["out"].run(c["ctx"], c["now"], k, api.SS_CASCADE, stream=stream)
+
     def step_all_learners(i):
         c = caches[i % R]
         api.sae_prefix_match(c["ctx"], d_reqs, d_lens, c["now"], api.PM_TOUCH | api.PM_STATS | api.PM_INTERVALS,
@@ -171,6 +175,15 @@ def main():
             select_only(i)
         torch.cuda.synchronize()
         s1 = time.perf_counter()
+        # --- score+select with a cascading decision (Algorithm 1 one victim at a time)
+        for i in range(args.warmup):
+            select_cascade(i)
+        torch.cuda.synchronize()
+        c0 = time.perf_counter()
+        for i in range(args.steps):
+            select_cascade(i)
+        torch.cuda.synchronize()
+        c1 = time.perf_counter()
         # --- the same step with every learner on: Algorithms 2, 3, 4 and the
         # decay power, the prefix match recording reuse intervals
         for c in caches:
@@ -194,6 +207,7 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     ms_sel = (s1 - s0) * 1e3 / args.steps
     ms_all = (a1 - a0) * 1e3 / args.steps
+    ms_casc = (c1 - c0) * 1e3 / args.steps
     scan_avg_ms = scan_ms / max(scan_n, 1)
     alg_bytes = BYTES_PER_BLOCK * N
     achieved = alg_bytes / (scan_avg_ms * 1e-3) / 1e9
@@ -220,6 +234,10 @@ def main():
         "score_select": {
             "value": N / (ms_sel * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_sel,
             "hbm_frac_at_10B_per_block": BYTES_PER_BLOCK * N / (ms_sel * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        },
+        "score_select_cascade": {
+            "value": N / (ms_casc * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_casc,
+            "decision": "Algorithm 1 one victim at a time (SAE_SS_CASCADE)",
         },
         "all_learners": {
             "value": N / (ms_all * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_all,

@@ -304,7 +304,8 @@ enum {
     SAE_SS_COMMIT = 1u << 0,          /* evict the decision (see below)                  */
     SAE_SS_ENGINE_SCAN = 1u << 1,     /* force the pool-scan engine                      */
     SAE_SS_ENGINE_BATCHED = 1u << 2,  /* force the one-workgroup-per-instance engine     */
-    SAE_SS_FORCE_FALLBACK = 1u << 3   /* pool-scan engine: take its exact slow path      */
+    SAE_SS_FORCE_FALLBACK = 1u << 3,  /* pool-scan engine: take its exact slow path      */
+    SAE_SS_CASCADE = 1u << 4          /* decision: Algorithm 1 one victim at a time      */
 };
 
 /*
@@ -332,6 +333,11 @@ enum {
  * left with no child becomes a leaf, eligible from the next call), and the
  * learners are marked due when eviction_count crosses a multiple of K.
  * Ties are broken by block id.  Results do not depend on the engine.
+ * SAE_SS_CASCADE makes the decision the one of k successive Evict() calls on
+ * the live state (Algorithm 1 as printed): a parent whose last cached child
+ * is taken becomes a leaf, evictable by the next call, so a decision can hold
+ * a block together with its ancestors.  Needs max_k <= 4096; the per-queue
+ * lists stay the snapshot's.
  */
 sae_status sae_score_select(sae_ctx *ctx, int32_t now, int32_t k, const int32_t *k_per_inst,
                             uint32_t flags, int32_t *victims, float *scores, int32_t *count,

@@ -14,7 +14,7 @@ from ._lib import IVL_CAP, N_BINS, SaeConfig, SaeCounters, SaeError, SaeParams, 
 KIND_EVICT_FIRST, KIND_STRUCTURAL, KIND_LOGNORMAL, KIND_RECENCY = 0, 1, 2, 3
 META_VALID, META_LEAF, META_REF = 0x40, 0x80, 0x100
 PM_TOUCH, PM_STATS, PM_INTERVALS = 1, 2, 4
-SS_COMMIT, SS_ENGINE_SCAN, SS_ENGINE_BATCHED, SS_FORCE_FALLBACK = 1, 2, 4, 8
+SS_COMMIT, SS_ENGINE_SCAN, SS_ENGINE_BATCHED, SS_FORCE_FALLBACK, SS_CASCADE = 1, 2, 4, 8, 16
 FB_FORCE = 1
 HINT_DECODE, HINT_UNTEMPLATED, HINT_MULTI_TURN, HINT_AGENTIC, HINT_CONVERSATION, HINT_SHARED_PREFIX = 1, 2, 4, 8, 16, 32
 ROLE_EVICT, ROLE_STRUCT, ROLE_CHAT, ROLE_AGENT = 0, 1, 2, 3

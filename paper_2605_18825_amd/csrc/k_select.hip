@@ -1701,7 +1701,8 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
                                  copy1);
     if (tid == 0) {
         a.decision_count[inst] = d;
-        commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
+        // a cascading decision is completed (and counted) by k_cascade
+        if (!(a.flags & SAE_SS_CASCADE)) commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
         set_status(c.status, st_s);
     }
 }
@@ -1818,7 +1819,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
     int d = merge_decision(lists, P, cnt_s, Q, c.ef_queue, kk, a.decision + (long long)inst * c.max_k);
     if (tid == 0) {
         a.decision_count[inst] = d;
-        commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
+        if (!(a.flags & SAE_SS_CASCADE)) commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
         set_status(c.status, st_s);
     }
 }
@@ -1848,6 +1849,229 @@ int pow2_at_least(int x)
     int p = 1;
     while (p < x) p <<= 1;
     return p;
+}
+
+// ---------------------------------------------------------------------------
+// Cascading decision (SAE_SS_CASCADE): k successive Evict() calls of
+// Algorithm 1 on the live state, where a parent whose last cached child is
+// taken becomes a leaf for the next call.  With kappa(b) = (stage, key, id)
+// (stage 0 for the evict-first queue, keyed by num_tokens), a block can be
+// taken once every cached child has been, and the calls take blocks in the
+// order of E(b) = max(kappa(b), E(children)), equal E (one path of the tree)
+// child first.  Every block among the first k has E at most kappa of the
+// snapshot decision's k-th victim, so all of them are reached from that
+// decision by walking up parents: round r takes the blocks added in round
+// r - 1 (round 0: the snapshot decision, sorted by kappa), counts them
+// towards their parents (global counters, reset afterwards) and adds a parent
+// when its last cached child arrives, with E = max(kappa(parent), the largest
+// E of its children) and round r + 1 (which orders equal E child first).  The
+// new blocks are sorted and merged into the sorted candidates, which keep
+// only the first k.  One workgroup of 1024 threads per instance.
+constexpr int CASC_THREADS = 1024;
+constexpr int CASC_PER = 4;  // candidates per thread: k <= CASC_THREADS * CASC_PER
+
+struct CascEl {
+    unsigned long long e;  // E (stage << 56 | key << 24 | id of the block that sets it)
+    uint32_t id, rnd;
+};
+
+__device__ __forceinline__ bool casc_less(const CascEl &a, const CascEl &b)
+{
+    return a.e < b.e || (a.e == b.e && a.rnd < b.rnd);
+}
+
+__device__ __forceinline__ unsigned long long casc_kappa(const DevCtx &c, const ScoreTab &tab, int32_t now,
+                                                         long long base, uint32_t b, uint32_t &st)
+{
+    const uint32_t m = c.meta[base + b];
+    const uint32_t key = block_key(now, c.la[base + b], m, c.off[base + b], tab, st);
+    const unsigned long long stage = (tab.kind[meta_queue(m)] == SAE_KIND_EVICT_FIRST) ? 0ull : 1ull;
+    return (stage << 56) | ((unsigned long long)key << 24) | (unsigned long long)(b & 0xFFFFFFu);
+}
+
+// number of elements of the sorted x[0..n) below v
+__device__ __forceinline__ int casc_rank(const CascEl *x, int n, const CascEl &v)
+{
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (casc_less(x[mid], v)) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+__global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a)
+{
+    extern __shared__ unsigned long long casc_lds[];
+    const int kmax = c.max_k;
+    CascEl *cur = reinterpret_cast<CascEl *>(casc_lds);  // [kmax] sorted candidates
+    CascEl *nw = cur + kmax;                             // [pow2 >= kmax] the round's new blocks
+    __shared__ ScoreTab tab;
+    __shared__ int n_cur_s, n_new_s, n_touch_s;
+    __shared__ uint32_t st_s;
+    const int inst = blockIdx.x;
+    const int tid = threadIdx.x;
+    const long long base = (long long)inst * c.N;
+    const int k = inst_k(a, inst, kmax);
+    int32_t *dec = a.decision + (long long)inst * kmax;
+    int32_t *cnt = c.casc_cnt + base;
+    unsigned long long *emax = c.casc_e + base;
+    int32_t *touch = c.casc_touch + (long long)inst * c.casc_tl;
+    load_score_tab(tab, c.state[inst], c);
+    if (tid == 0) {
+        n_cur_s = a.decision_count[inst];
+        n_touch_s = 0;
+        st_s = 0;
+    }
+    __syncthreads();
+    const int d0 = n_cur_s;
+    uint32_t st = 0;
+    // round 0: the snapshot decision, already in kappa order
+    for (int j = tid; j < d0; j += CASC_THREADS) {
+        const uint32_t b = (uint32_t)dec[j];
+        CascEl x;
+        x.e = casc_kappa(c, tab, a.now, base, b, st);
+        x.id = b;
+        x.rnd = 0;
+        cur[j] = x;
+    }
+    __syncthreads();
+    for (uint32_t r = 0;; ++r) {
+        if (tid == 0) n_new_s = 0;
+        __syncthreads();
+        const int n_cur = n_cur_s;
+        // admission bound: the k-th candidate so far (none while fewer than k)
+        CascEl bound;
+        bound.e = ~0ull;
+        bound.rnd = 0xFFFFFFFFu;
+        if (n_cur >= k && k > 0) bound = cur[k - 1];
+        // each thread's (up to CASC_PER) frontier blocks, their loads and
+        // atomics in flight together
+        CascEl fx[CASC_PER];
+        int32_t fp[CASC_PER];
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            const int j = tid + u * CASC_THREADS;
+            fx[u] = cur[j < n_cur ? j : 0];
+            const bool f = j < n_cur && fx[u].rnd == r;
+            const int32_t p = c.parent[base + (f ? fx[u].id : 0u)];
+            fp[u] = (f && p >= 0 && p < c.N) ? p : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u)
+            if (fp[u] >= 0) atomicMax(&emax[fp[u]], fx[u].e);
+        // the children's E are in before they are counted: this workgroup's
+        // atomics all go to one L2, so waiting for them to complete suffices
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        int old[CASC_PER], cc[CASC_PER];
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            old[u] = fp[u] >= 0 ? atomicAdd(&cnt[fp[u]], 1) : -2;
+            cc[u] = c.child_count[base + (fp[u] >= 0 ? fp[u] : 0)];
+        }
+        // pairs with the release above: a last child sees every sibling's E
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        bool last[CASC_PER];
+        uint32_t pm[CASC_PER];
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            if (old[u] == 0) {
+                const int t = atomicAdd(&n_touch_s, 1);
+                if (t < c.casc_tl) touch[t] = fp[u];
+            }
+            last[u] = fp[u] >= 0 && old[u] + 1 == cc[u];  // its last cached child
+            pm[u] = c.meta[base + (fp[u] >= 0 ? fp[u] : 0)];
+            last[u] = last[u] && (pm[u] & (SAE_META_VALID | SAE_META_REF)) == SAE_META_VALID;
+        }
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            if (!last[u]) continue;
+            const uint32_t p = (uint32_t)fp[u];
+            CascEl y;
+            const unsigned long long kp = casc_kappa(c, tab, a.now, base, p, st);
+            const unsigned long long ec = atomicMax(&emax[p], 0ull);  // every child's E is in by now
+            y.e = kp > ec ? kp : ec;
+            y.id = p;
+            y.rnd = r + 1;
+            if (!casc_less(y, bound)) continue;  // cannot be among the first k
+            nw[atomicAdd(&n_new_s, 1)] = y;
+        }
+        __syncthreads();
+        const int n_new = n_new_s;
+        if (n_new == 0) break;  // uniform
+        // sort the new blocks (bitonic over the next power of two)
+        int P = 1;
+        while (P < n_new) P <<= 1;
+        for (int j = n_new + tid; j < P; j += CASC_THREADS) {
+            nw[j].e = ~0ull;
+            nw[j].id = 0xFFFFFFFFu;
+            nw[j].rnd = 0xFFFFFFFFu;
+        }
+        __syncthreads();
+        for (int size = 2; size <= P; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int i = tid; i < P / 2; i += CASC_THREADS) {
+                    const int lo = 2 * i - (i & (stride - 1));
+                    const int hi = lo + stride;
+                    const bool up = (lo & size) == 0;
+                    const CascEl u = nw[lo], v = nw[hi];
+                    if (casc_less(v, u) == up) {
+                        nw[lo] = v;
+                        nw[hi] = u;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        // merge by rank, everything read before anything is written
+        CascEl xc[CASC_PER], xn[CASC_PER];
+        int rc[CASC_PER], rn[CASC_PER];
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            const int j = tid + u * CASC_THREADS;
+            rc[u] = rn[u] = 0x7FFFFFFF;
+            if (j < n_cur) {
+                xc[u] = cur[j];
+                rc[u] = j + casc_rank(nw, n_new, xc[u]);
+            }
+            if (j < n_new) {
+                xn[u] = nw[j];
+                rn[u] = j + casc_rank(cur, n_cur, xn[u]);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < CASC_PER; ++u) {
+            if (rc[u] < k) cur[rc[u]] = xc[u];
+            if (rn[u] < k) cur[rn[u]] = xn[u];
+        }
+        if (tid == 0) n_cur_s = min(k, n_cur + n_new);
+        __syncthreads();
+    }
+    const int d = min(k, n_cur_s);
+    for (int j = tid; j < d; j += CASC_THREADS) dec[j] = (int32_t)cur[j].id;
+    // reset the per-block entries this call changed
+    const int nt = n_touch_s;
+    if (nt <= c.casc_tl) {
+        for (int t = tid; t < nt; t += CASC_THREADS) {
+            const int32_t p = touch[t];
+            cnt[p] = 0;
+            emax[p] = 0ull;
+        }
+    } else {
+        for (long long b = tid; b < c.N; b += CASC_THREADS) {
+            cnt[b] = 0;
+            emax[b] = 0ull;
+        }
+    }
+    if (st) atomicOr(&st_s, st);
+    __syncthreads();
+    if (tid == 0) {
+        a.decision_count[inst] = d;
+        commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
+        set_status(c.status, st_s);
+    }
 }
 
 }  // namespace
@@ -1925,5 +2149,16 @@ hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream
     hipError_t e = allow_lds((const void *)k_batched, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_batched, dim3(c.n_inst), dim3(SEL_THREADS), lds, s, c, a, P);
+    return hipGetLastError();
+}
+
+hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s)
+{
+    int P = 1;
+    while (P < c.max_k) P <<= 1;
+    const size_t lds = (size_t)(c.max_k + P) * sizeof(CascEl);
+    hipError_t e = allow_lds((const void *)k_cascade, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_cascade, dim3(c.n_inst), dim3(CASC_THREADS), lds, s, c, a);
     return hipGetLastError();
 }

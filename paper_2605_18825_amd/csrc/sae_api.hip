@@ -151,6 +151,7 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
         if (k.queue_kind[q] == SAE_KIND_STRUCTURAL) d.struct_mask |= 1u << q;
     }
     d.max_req = k.max_requests;
+    d.casc_tl = 8 * k.max_k;
     d.W = k.ghost_window ? k.ghost_window : k.blocks_per_instance;
     d.ring_cap = d.W + d.max_k;
     int il = k.index_log2 ? k.index_log2 : log2_ceil(2ll * d.N);
@@ -191,7 +192,9 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
               dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N) &&
               dev_alloc(c, &d.ivl, d.ln_mask ? I * Q * SAE_IVL_CAP : 0) &&
-              dev_alloc(c, &d.pm_rec, (long long)d.max_req * SAE_MAX_QUEUES);
+              dev_alloc(c, &d.pm_rec, (long long)d.max_req * SAE_MAX_QUEUES) &&
+              dev_alloc(c, &d.casc_cnt, I * d.N) && dev_alloc(c, &d.casc_e, I * d.N) &&
+              dev_alloc(c, &d.casc_touch, I * 8ll * d.max_k);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);
         delete c;
@@ -496,8 +499,11 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
 {
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
     if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
-    const uint32_t known = SAE_SS_COMMIT | SAE_SS_ENGINE_SCAN | SAE_SS_ENGINE_BATCHED | SAE_SS_FORCE_FALLBACK;
+    const uint32_t known =
+        SAE_SS_COMMIT | SAE_SS_ENGINE_SCAN | SAE_SS_ENGINE_BATCHED | SAE_SS_FORCE_FALLBACK | SAE_SS_CASCADE;
     if (flags & ~known) return fail(c, SAE_ERR_ARG, "unknown score-select flag");
+    if ((flags & SAE_SS_CASCADE) && c->dc.max_k > 4096)
+        return fail(c, SAE_ERR_ARG, "SAE_SS_CASCADE needs max_k <= 4096");
     if ((flags & SAE_SS_ENGINE_SCAN) && (flags & SAE_SS_ENGINE_BATCHED))
         return fail(c, SAE_ERR_ARG, "choose at most one engine");
     if (!k_per_inst && (k < 0 || k > c->dc.max_k)) return fail(c, SAE_ERR_ARG, "k must be in 0..max_k");
@@ -545,6 +551,7 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
         e = launch_select_scan(c->dc, a, s, e0, e1);
         if (e == hipSuccess) e = launch_merge(c->dc, a, s);
     }
+    if (e == hipSuccess && (flags & SAE_SS_CASCADE)) e = launch_cascade(c->dc, a, s);
     if (e != hipSuccess) return hip_fail(c, e, "sae_score_select");
     if (flags & SAE_SS_COMMIT) {
         e = launch_commit(c->dc, a, s);

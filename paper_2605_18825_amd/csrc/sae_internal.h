@@ -149,6 +149,13 @@ struct DevCtx {
     int32_t max_req;
     uint32_t ln_mask;          // bit q: queue q is log-normal
     uint32_t struct_mask;      // bit q: queue q is structural
+    // cascading decisions (SAE_SS_CASCADE): per block, cached children found
+    // among the candidates so far and the largest rank among them (zero
+    // between calls), and the blocks whose entries a call changed
+    int32_t *casc_cnt;              // [n_inst][N]
+    unsigned long long *casc_e;     // [n_inst][N]
+    int32_t *casc_touch;            // [n_inst][casc_tl]
+    int32_t casc_tl;
 };
 
 // Positional bin of a block (decay-power learner): floor(8 o_b / o_max) with
@@ -444,6 +451,7 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
                               hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_feedback(const DevCtx &c, uint32_t flags, int learn, hipStream_t s);
 int scan_grid_x(int n_inst, int N);

@@ -18,11 +18,12 @@ def _dev(a, dtype):
 
 class DeviceBackend:
     def __init__(self, n_inst, capacity, kinds, roles, max_k, mu, sigma, K, learn, w=1.0, alpha=1.0, gamma=1.0,
-                 eta=0.01, T=1.0, beta=0.1, ghost_window=0):
+                 eta=0.01, T=1.0, beta=0.1, ghost_window=0, cascade=False):
         self.n_inst, self.N, self.Q = n_inst, capacity, len(kinds)
         self.roles = list(roles)
         self.max_k = max_k
         self.intervals = bool(learn & api.LEARN_LOGNORMAL)
+        self.select_flags = api.SS_COMMIT | (api.SS_CASCADE if cascade else 0)
         self.ctx = api.sae_create(n_inst, capacity, kinds, max_k=max_k, ghost_window=ghost_window,
                                   max_requests=n_inst if self.intervals else 0)
         self.pool = DevicePool(n_inst, capacity)
@@ -61,7 +62,7 @@ class DeviceBackend:
 
     def evict(self, now, k):
         kd = _dev(k, torch.int32)
-        self.out.run(self.ctx, now, self.max_k, api.SS_COMMIT, k_per_inst=kd)
+        self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd)
         cnt = self.out.decision_count.cpu().numpy()
         dec = self.out.decision.cpu().numpy()
         self.select_calls += 1

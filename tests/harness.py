@@ -63,11 +63,18 @@ class Pair:
 
     def select(self, now, k, flags=0, commit=False, check=True):
         """Run both sides; compare per-queue victims, their key bits and the
-        decision element by element."""
+        decision element by element.  With api.SS_CASCADE the oracle's decision
+        is its sequential cascade (the per-queue lists stay the snapshot's)."""
         if commit:
             flags |= api.SS_COMMIT
         self.out.run(self.ctx, now, k, flags)
-        lists, key, dec = self.oc.score_select(now, k, commit=commit)
+        if flags & api.SS_CASCADE:
+            lists, key, _ = self.oc.select_per_queue(now, k)
+            dec = self.oc.decide_cascade(now, k)
+            if commit:
+                self.oc.commit(dec)
+        else:
+            lists, key, dec = self.oc.score_select(now, k, commit=commit)
         if check:
             torch.cuda.synchronize()
             cnt = self.out.count[0].cpu().numpy()

@@ -40,6 +40,18 @@ def test_trace_balanced_text_rules():
     assert ro.be.c[0].n_updates > 0
 
 
+def test_trace_balanced_cascading_decisions():
+    """Algorithm 1 one victim at a time (SAE_SS_CASCADE) on the balanced
+    trace: every decision equals the oracle's sequential cascade."""
+    rd, ro, _ = run_pair("trace_balanced", 1500, [0], check_every=250, cascade=True)
+    assert rd.summary()["evicted"] > 0
+
+
+def test_batched_sweep_cascading_decisions():
+    rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], check_every=300, cascade=True)
+    assert rd.summary()["evicted"] > 0
+
+
 def test_batched_sweep_all_learners():
     """Interval placement across 256 instances of one context."""
     rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], learn=15, check_every=300)

@@ -67,13 +67,14 @@ def check_state(dev, orc, i):
     assert gd.view(np.uint32) == go.view(np.uint32), "instance %d: gamma %r vs %r" % (i, gd, go)
 
 
-def run_pair(name, steps, oracle_insts, n_inst=None, capacity=None, learn=3, check_every=100, w=1.0, **gen_over):
+def run_pair(name, steps, oracle_insts, n_inst=None, capacity=None, learn=3, check_every=100, w=1.0, cascade=False,
+             **gen_over):
     cfg = TRACE_CONFIGS[name]
     n_inst = cfg["n_inst"] if n_inst is None else n_inst
     capacity = cfg["capacity"] if capacity is None else capacity
     gens = trace_gens(name, n_inst, **gen_over)
-    dev = DeviceBackend(n_inst, capacity, KINDS, ROLES, cfg["max_k"], MU, SIGMA, cfg["K"], learn, w=w)
-    orc = OracleBackend(oracle_insts, capacity, KINDS, ROLES, MU, SIGMA, cfg["K"], learn, w=w)
+    dev = DeviceBackend(n_inst, capacity, KINDS, ROLES, cfg["max_k"], MU, SIGMA, cfg["K"], learn, w=w, cascade=cascade)
+    orc = OracleBackend(oracle_insts, capacity, KINDS, ROLES, MU, SIGMA, cfg["K"], learn, w=w, cascade=cascade)
     rd = Replay(dev, n_inst, capacity, cfg["k_min"], cfg["max_k"], cfg["concurrency"])
     ro = Replay(orc, n_inst, capacity, cfg["k_min"], cfg["max_k"], cfg["concurrency"], insts=oracle_insts)
     try:
