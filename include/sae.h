@@ -401,6 +401,35 @@ sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
  * memory of 4 * n_queues words; synchronizes `stream`. */
 sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_stream_t stream);
 
+/*
+ * Multi-turn session predictor (Sec. 3.3): for each request, the serving
+ * model's final-layer hidden state h of its last prompt token goes through
+ *   y = W3 relu(W2 relu(W1 h + b1) + b2) + b3
+ * (hidden widths 256 and 64); y > 0 predicts that the session continues.
+ *  h[n][d]       device bf16 (uint16 bit patterns), row-major
+ *  w->w1[256][d] device bf16, row-major (one row per first-layer unit)
+ *  w->b1[256], w->w2[64][256] (row-major), w->b2[64], w->w3[64], w->b3[1]
+ *                device float
+ *  work[n][256]  device float scratch (the first layer's output)
+ *  logit[n]      device float out: y
+ *  pred[n]       device uint8 out: 1 if y > 0, else 0 (or NULL)
+ * Layer 1 multiplies bf16 exactly and sums in fp32 (matrix cores); layers 2
+ * and 3 are fp32.  Needs 1 <= d <= 16384 with d a multiple of 64, n >= 0.
+ * Returns SAE_ERR_ARG (nothing launched) otherwise or for a NULL array.
+ */
+#define SAE_PRED_H1 256
+#define SAE_PRED_H2 64
+typedef struct {
+    const uint16_t *w1;
+    const float *b1;
+    const float *w2;
+    const float *b2;
+    const float *w3;
+    const float *b3;
+} sae_predictor;
+sae_status sae_predict_sessions(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, float *work,
+                                float *logit, uint8_t *pred, sae_stream_t stream);
+
 /* Device realisation of the fp32 recipe's elementary functions (the ones
  * Eq. 1 and Eq. 2 are built from), element-wise, for checking it:
  *  fn = SAE_FN_LN    y = ln x    (x a positive normal float)
