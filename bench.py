@@ -197,6 +197,32 @@ def main():
             step_all_learners(i)
         torch.cuda.synchronize()
         a1 = time.perf_counter()
+    # --- session predictor (Sec. 3.3) on 4,096 last-token hidden states of
+    # d = 4,096, rotating over 8 batches (256 MB, beyond the last-level cache)
+    from synth import predictor as SP
+    PN, PD = 4096, 4096
+    h0 = SP.hidden_states(PN, PD, 5).view(np.int16)
+    hbat = [torch.as_tensor(h0).cuda() for _ in range(R)]
+    wnp = SP.weights(PD, 6)
+    wp = {k: torch.as_tensor(v.view(np.int16) if k == "w1" else v).cuda() for k, v in wnp.items()}
+    pwork = torch.empty((4, PN, 256), dtype=torch.float32, device="cuda")
+    plogit = torch.empty(PN, dtype=torch.float32, device="cuda")
+    ppred = torch.empty(PN, dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for i in range(args.steps):
+            api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+    ms_pred = ev0.elapsed_time(ev1) / args.steps
+    pred_bytes = PN * PD * 2 + 256 * PD * 2 + PN * 5  # hidden states, W1, logits and predictions
+    pred_flops = 2.0 * PN * PD * 256 + 2.0 * PN * 256 * 64 + 2.0 * PN * 64
+    del hbat
     st = 0
     for c in caches:
         st |= api.sae_poll_status(c["ctx"])
@@ -243,6 +269,13 @@ def main():
             "value": N / (ms_all * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_all,
             "step": "the same step with Algorithms 2, 3, 4 and the decay-power learner on "
                     "(prefix match records reuse intervals)",
+        },
+        "predictor": {
+            "value": PN / (ms_pred * 1e-3), "unit": "predictions/s", "ms_per_call": ms_pred,
+            "batch": PN, "d": PD,
+            "roofline": {"bound": "hbm", "achieved": pred_bytes / (ms_pred * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": pred_bytes / (ms_pred * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                         "mfma_tflops_bf16": pred_flops / (ms_pred * 1e-3) / 1e12, "mfma_peak_bf16": 2500.0},
         },
         "roofline": {
             "kernel": "k_scan", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -410,11 +410,12 @@ sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_strea
  *  w->w1[256][d] device bf16, row-major (one row per first-layer unit)
  *  w->b1[256], w->w2[64][256] (row-major), w->b2[64], w->w3[64], w->b3[1]
  *                device float
- *  work[n][256]  device float scratch (the first layer's output)
+ *  work[4][n][256] device float scratch (the first layer's partial sums)
  *  logit[n]      device float out: y
  *  pred[n]       device uint8 out: 1 if y > 0, else 0 (or NULL)
- * Layer 1 multiplies bf16 exactly and sums in fp32 (matrix cores); layers 2
- * and 3 are fp32.  Needs 1 <= d <= 16384 with d a multiple of 64, n >= 0.
+ * Layer 1 multiplies bf16 exactly and sums in fp32 (matrix cores), in four k
+ * slices added in a fixed order; layers 2 and 3 are fp32.  Needs
+ * 256 <= d <= 16384 with d a multiple of 256, n >= 0.
  * Returns SAE_ERR_ARG (nothing launched) otherwise or for a NULL array.
  */
 #define SAE_PRED_H1 256

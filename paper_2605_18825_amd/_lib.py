@@ -61,6 +61,10 @@ class SaeCounters(ctypes.Structure):
     ]
 
 
+class SaePredictor(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w1", "b1", "w2", "b2", "w3", "b3")]
+
+
 class SaePool(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "last_access", "meta", "off", "hash", "parent", "child_count", "ref_count", "access_count")]
@@ -92,6 +96,7 @@ SIGNATURES = {
     "sae_feedback_update": (_I32, [_P, _U32, _P]),
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
     "sae_get_intervals": (_I32, [_P, _I32, _I32, _P, _I32, ctypes.POINTER(_I32), _P]),
+    "sae_predict_sessions": (_I32, [_I32, _I32, _P, ctypes.POINTER(SaePredictor), _P, _P, _P, _P]),
     "sae_select_stats": (_I32, [_P, _I32, _P, _P]),
     "sae_profile_enable": (_I32, [_P, _I32]),
     "sae_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),

@@ -9,7 +9,7 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import IVL_CAP, N_BINS, SaeConfig, SaeCounters, SaeError, SaeParams, SaePool  # noqa: F401
+from ._lib import IVL_CAP, N_BINS, SaeConfig, SaeCounters, SaeError, SaeParams, SaePool, SaePredictor  # noqa: F401
 
 KIND_EVICT_FIRST, KIND_STRUCTURAL, KIND_LOGNORMAL, KIND_RECENCY = 0, 1, 2, 3
 META_VALID, META_LEAF, META_REF = 0x40, 0x80, 0x100
@@ -234,6 +234,18 @@ def sae_get_intervals(ctx, inst, queue, cap=IVL_CAP, stream=None):
     _check(ctx, _lib.load().sae_get_intervals(ctx, inst, queue, ctypes.cast(buf, ctypes.c_void_p), cap,
                                               ctypes.byref(n), _stream(stream)))
     return list(buf[:min(n.value, cap)])
+
+
+def sae_predict_sessions(h_bf16, w, work, logit, pred=None, stream=None):
+    """Session predictor (Sec. 3.3) on n hidden states: h_bf16 is an int16
+    tensor [n][d] of bf16 bit patterns; w holds device tensors w1 (int16
+    [256][d], bf16 bits), b1, w2 [64][256], b2, w3 [64], b3 [1] (float32)."""
+    n, d = h_bf16.shape
+    p = SaePredictor()
+    for name in ("w1", "b1", "w2", "b2", "w3", "b3"):
+        setattr(p, name, _ptr(w[name]).value)
+    _check(None, _lib.load().sae_predict_sessions(n, d, _ptr(h_bf16), ctypes.byref(p), _ptr(work), _ptr(logit),
+                                                  _ptr(pred), _stream(stream)))
 
 
 def status_names(bits):

@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libsae.so")
-SOURCES = ["sae_api.hip", "k_select.hip", "k_index.hip", "k_learn.hip"]
+SOURCES = ["sae_api.hip", "k_select.hip", "k_index.hip", "k_learn.hip", "k_predict.hip"]
 ARCH = os.environ.get("SAE_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [

@@ -393,6 +393,22 @@ sae_status sae_get_intervals(sae_ctx *c, int32_t inst, int32_t queue, int32_t *o
     return SAE_OK;
 }
 
+sae_status sae_predict_sessions(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, float *work,
+                                float *logit, uint8_t *pred, sae_stream_t stream)
+{
+    if (n < 0) return fail(nullptr, SAE_ERR_ARG, "n must be >= 0");
+    if (d < 256 || d > 16384 || d % 256 != 0)
+        return fail(nullptr, SAE_ERR_ARG, "d must be a multiple of 256 in 256..16384");
+    if (n == 0) return SAE_OK;
+    if (!h || !w || !w->w1 || !w->b1 || !w->w2 || !w->b2 || !w->w3 || !w->b3 || !work || !logit)
+        return fail(nullptr, SAE_ERR_ARG, "h, every weight, work and logit must be non-NULL");
+    if (!aligned(h, 16) || !aligned(w->w1, 16) || !aligned(w->w2, 16) || !aligned(work, 16))
+        return fail(nullptr, SAE_ERR_ARG, "h, w1, w2 and work must be 16-byte aligned");
+    hipError_t e = launch_predict(n, d, h, w->w1, w->b1, w->w2, w->b2, w->w3, w->b3, work, logit, pred, S(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "sae_predict_sessions");
+    return SAE_OK;
+}
+
 sae_status sae_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, sae_stream_t stream)
 {
     if (n < 0 || (n > 0 && (!counts || !tau))) return fail(nullptr, SAE_ERR_ARG, "counts/tau must be non-NULL, n >= 0");

@@ -452,6 +452,9 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_predict(int n, int d, const uint16_t *h, const uint16_t *w1, const float *b1, const float *w2,
+                          const float *b2, const float *w3, const float *b3, float *work, float *logit,
+                          uint8_t *pred, hipStream_t s);
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_feedback(const DevCtx &c, uint32_t flags, int learn, hipStream_t s);
 int scan_grid_x(int n_inst, int N);
