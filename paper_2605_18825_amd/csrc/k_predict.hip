@@ -14,8 +14,9 @@
 // through one L2.
 //
 // Layers 2 and 3 are fp32: v_mfma_f32_32x32x2f32 for (32 rows x 256) . (256 x
-// 64) in a workgroup of 4 waves (two column halves times two k halves, summed
-// in a fixed order), then the 64-term layer 3 by shuffles.  Layer 1's four k
+// 64) in a workgroup of 8 waves (two column halves times four k quarters,
+// every load of a wave issued at once, the quarters summed in a fixed order),
+// then the 64-term layer 3 by shuffles.  Layer 1's four k
 // slices are added here, in slice order, before b1 and the ReLU.
 #include "sae_internal.h"
 
@@ -29,7 +30,7 @@ constexpr int L1_TILE = 128;       // rows and columns of a workgroup's tile
 constexpr int KSTEP = 64;          // k per step
 constexpr int KSPLIT = 4;          // k slices (workgroups per tile); their sums meet in layer 2
 constexpr int LDS_ROW16 = 9;       // LDS row of a tile: 128 bytes of k + 16 bytes of padding
-constexpr int L23_THREADS = 256;   // 4 waves: layer-2 columns 0-31 / 32-63 times k halves
+constexpr int L23_THREADS = 512;   // 8 waves: layer-2 columns 0-31 / 32-63 times k quarters
 constexpr int L23_ROWS = 32;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v)
@@ -179,13 +180,14 @@ k_pred_l1(int n, int d, const uint16_t *h, const uint16_t *w1,
         }
 }
 
-__global__ void __launch_bounds__(L23_THREADS) k_pred_l23(int n, const float *part, const float *b1, const float *w2,
-                                                         const float *b2, const float *w3, const float *b3,
-                                                         float *logit, uint8_t *pred)
+__global__ void __launch_bounds__(L23_THREADS) __attribute__((amdgpu_waves_per_eu(1, 2)))
+k_pred_l23(int n, const float *part, const float *b1, const float *w2, const float *b2, const float *w3,
+           const float *b3, float *logit, uint8_t *pred)
 {
-    // wave w: layer-2 units 32 (w & 1) .. + 31 over k half w >> 1 (128 each);
-    // the k halves meet in LDS in a fixed order
-    __shared__ float hsum[2][16][SAE_WAVE];   // k half 1's layer-2 sums, per column wave
+    // wave w: layer-2 units 32 (w & 1) .. + 31 over k quarter w >> 1 (64 k);
+    // the quarters meet in LDS and are added in quarter order
+    constexpr int NQ = 4;
+    __shared__ float hsum[NQ - 1][2][16][SAE_WAVE];
     __shared__ float ysum[2][L23_ROWS];
     const int lane = (int)__lane_id(), wave = threadIdx.x / SAE_WAVE;
     const int ctile = wave & 1, g = wave >> 1;
@@ -193,40 +195,39 @@ __global__ void __launch_bounds__(L23_THREADS) k_pred_l23(int n, const float *pa
     const int row = r0 + (lane & 31);
     const int rowc = row < n ? row : n - 1;
     const int col = ctile * 32 + (lane & 31);  // layer-2 unit
-    const int kb = g * (SAE_PRED_H1 / 2) + (lane >> 5) * (SAE_PRED_H1 / 4);
-    // lane half h supplies k = 128 g + 64 h + s in MFMA s, for both operands;
+    const int kb = g * (SAE_PRED_H1 / NQ) + (lane >> 5) * (SAE_PRED_H1 / NQ / 2);
+    // lane half h supplies k = 64 g + 32 h + s in MFMA s, for both operands;
     // the layer-1 value is the sum of its k slices in slice order, plus b1, ReLU
-    const long long slice = (long long)n * SAE_PRED_H1;
+    const long long slice = (long long)n * SAE_PRED_H1 / 4;  // in float4
     const float4 *pa = reinterpret_cast<const float4 *>(part + (long long)rowc * SAE_PRED_H1 + kb);
     const float4 *pb = reinterpret_cast<const float4 *>(w2 + (long long)col * SAE_PRED_H1 + kb);
     const float4 *pc = reinterpret_cast<const float4 *>(b1 + kb);
+    float4 v[KSPLIT][8], b[8], c[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {  // every load of the wave in flight together
+#pragma unroll
+        for (int q = 0; q < KSPLIT; ++q) v[q][u] = pa[q * slice + u];
+        b[u] = pb[u];
+        c[u] = pc[u];
+    }
+    __builtin_amdgcn_sched_barrier(0);
     floatx16 acc;
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-    float4 v[16], b[16];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {  // 64 k per lane: every load in flight together
-        v[u] = pa[u];
-        b[u] = pb[u];
-    }
+    for (int u = 0; u < 8; ++u) {
+        float4 a = v[0][u];
 #pragma unroll
-    for (int q = 1; q < KSPLIT; ++q)
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const float4 w = pa[q * slice / 4 + u];
-            v[u].x = v[u].x + w.x;
-            v[u].y = v[u].y + w.y;
-            v[u].z = v[u].z + w.z;
-            v[u].w = v[u].w + w.w;
+        for (int q = 1; q < KSPLIT; ++q) {
+            a.x = a.x + v[q][u].x;
+            a.y = a.y + v[q][u].y;
+            a.z = a.z + v[q][u].z;
+            a.w = a.w + v[q][u].w;
         }
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-        const float4 bb = pc[u];
-        float4 a;
-        a.x = v[u].x + bb.x;
-        a.y = v[u].y + bb.y;
-        a.z = v[u].z + bb.z;
-        a.w = v[u].w + bb.w;
+        a.x = a.x + c[u].x;
+        a.y = a.y + c[u].y;
+        a.z = a.z + c[u].z;
+        a.w = a.w + c[u].w;
         a.x = a.x > 0.0f ? a.x : 0.0f;
         a.y = a.y > 0.0f ? a.y : 0.0f;
         a.z = a.z > 0.0f ? a.z : 0.0f;
@@ -236,20 +237,23 @@ __global__ void __launch_bounds__(L23_THREADS) k_pred_l23(int n, const float *pa
         acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, b[u].z, acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, b[u].w, acc, 0, 0, 0);
     }
-    if (g == 1) {
+    if (g > 0) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) hsum[ctile][i][lane] = acc[i];
+        for (int i = 0; i < 16; ++i) hsum[g - 1][ctile][i][lane] = acc[i];
     }
     __syncthreads();
     if (g == 0) {
-        // layer 2 complete (k half 0 + k half 1); layer 3: this lane's column
+        // layer 2 complete (quarters in order); layer 3: this lane's column
         // weight times relu(h2) for its 16 rows, summed over the wave's 32
         // columns (lanes of one half share rows)
         const float bias = b2[col], wt = w3[col];
         float t[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float h2 = (acc[i] + hsum[ctile][i][lane]) + bias;
+            float h2 = acc[i];
+#pragma unroll
+            for (int q = 0; q < NQ - 1; ++q) h2 = h2 + hsum[q][ctile][i][lane];
+            h2 = h2 + bias;
             t[i] = wt * (h2 > 0.0f ? h2 : 0.0f);
         }
 #pragma unroll
