@@ -1866,9 +1866,14 @@ int pow2_at_least(int x)
 // when its last cached child arrives, with E = max(kappa(parent), the largest
 // E of its children) and round r + 1 (which orders equal E child first).  The
 // new blocks are sorted and merged into the sorted candidates, which keep
-// only the first k.  One workgroup of 1024 threads per instance.
+// only the first k.  Round 0 (up to k blocks), the E of the parents it
+// completes and the final reset of the counters run over many workgroups
+// (k_casc_round0, k_casc_parents, k_casc_reset); the later rounds, whose
+// frontiers are small, in one workgroup of 1024 threads per instance
+// (k_cascade).
 constexpr int CASC_THREADS = 1024;
 constexpr int CASC_PER = 4;  // candidates per thread: k <= CASC_THREADS * CASC_PER
+constexpr int CASC0_THREADS = 64;
 
 struct CascEl {
     unsigned long long e;  // E (stage << 56 | key << 24 | id of the block that sets it)
@@ -1880,13 +1885,18 @@ __device__ __forceinline__ bool casc_less(const CascEl &a, const CascEl &b)
     return a.e < b.e || (a.e == b.e && a.rnd < b.rnd);
 }
 
+__device__ __forceinline__ unsigned long long casc_kappa_of(const ScoreTab &tab, int32_t now, uint32_t b, uint32_t m,
+                                                            int32_t la, uint32_t off, uint32_t &st)
+{
+    const uint32_t key = block_key(now, la, m, off, tab, st);
+    const unsigned long long stage = (tab.kind[meta_queue(m)] == SAE_KIND_EVICT_FIRST) ? 0ull : 1ull;
+    return (stage << 56) | ((unsigned long long)key << 24) | (unsigned long long)(b & 0xFFFFFFu);
+}
+
 __device__ __forceinline__ unsigned long long casc_kappa(const DevCtx &c, const ScoreTab &tab, int32_t now,
                                                          long long base, uint32_t b, uint32_t &st)
 {
-    const uint32_t m = c.meta[base + b];
-    const uint32_t key = block_key(now, c.la[base + b], m, c.off[base + b], tab, st);
-    const unsigned long long stage = (tab.kind[meta_queue(m)] == SAE_KIND_EVICT_FIRST) ? 0ull : 1ull;
-    return (stage << 56) | ((unsigned long long)key << 24) | (unsigned long long)(b & 0xFFFFFFu);
+    return casc_kappa_of(tab, now, b, c.meta[base + b], c.la[base + b], c.off[base + b], st);
 }
 
 // number of elements of the sorted x[0..n) below v
@@ -1901,6 +1911,98 @@ __device__ __forceinline__ int casc_rank(const CascEl *x, int n, const CascEl &v
     return lo;
 }
 
+// Round 0: one thread per snapshot victim records its kappa, raises its
+// parent's largest E and counts itself towards the parent; the victim that
+// completes a parent's count of cached children lists the parent if it is
+// valid and unreferenced.  Listing needs only the count, and k_cascade reads
+// the maxima after this launch has ended, so no ordering between the
+// workgroups (and the XCDs they run on) is needed.
+__global__ void __launch_bounds__(CASC0_THREADS) k_casc_round0(DevCtx c, SelectArgs a)
+{
+    __shared__ ScoreTab tab;
+    const int inst = blockIdx.y;
+    const long long base = (long long)inst * c.N;
+    load_score_tab(tab, c.state[inst], c);
+    __syncthreads();
+    const int j = blockIdx.x * CASC0_THREADS + threadIdx.x;
+    if (j >= a.decision_count[inst]) return;
+    const long long slot = (long long)inst * c.max_k + j;
+    const uint32_t b = (uint32_t)a.decision[slot];
+    const int32_t p = c.parent[base + b];
+    uint32_t st = 0;
+    const unsigned long long e = casc_kappa(c, tab, a.now, base, b, st);
+    c.casc_k0[slot] = e;
+    if (p >= 0 && p < c.N) {
+        atomicMax(&c.casc_e[base + p], e);
+        const int cc = c.child_count[base + p];
+        const uint32_t pm = c.meta[base + p];
+        const int old = atomicAdd(&c.casc_cnt[base + p], 1);
+        int32_t *n = c.casc_n + 4 * inst;
+        if (old == 0) {
+            const int t = atomicAdd(&n[0], 1);
+            if (t < c.casc_tl) c.casc_touch[(long long)inst * c.casc_tl + t] = p;
+        }
+        if (old + 1 == cc && (pm & (SAE_META_VALID | SAE_META_REF)) == SAE_META_VALID)
+            c.casc_prom[(long long)inst * c.max_k + atomicAdd(&n[1], 1)] = p;
+    }
+    if (st) set_status(c.status, st);
+}
+
+// E of each parent that round 0 completed (every child's E is in: the
+// previous launch has ended); the parents below the admission bound, the
+// snapshot decision's k-th victim (none while it holds fewer than k), are
+// listed with their E for k_cascade.  They enter round 1, so E equal to the
+// bound does not pass.
+__global__ void __launch_bounds__(CASC0_THREADS) k_casc_parents(DevCtx c, SelectArgs a)
+{
+    __shared__ ScoreTab tab;
+    const int inst = blockIdx.y;
+    const long long base = (long long)inst * c.N;
+    load_score_tab(tab, c.state[inst], c);
+    __syncthreads();
+    const int i = blockIdx.x * CASC0_THREADS + threadIdx.x;
+    if (i >= c.casc_n[4 * inst + 1]) return;
+    const int k = inst_k(a, inst, c.max_k);
+    const int d0 = a.decision_count[inst];
+    const long long row = (long long)inst * c.max_k;
+    const unsigned long long bound = (d0 >= k && k > 0) ? c.casc_k0[row + k - 1] : ~0ull;
+    const uint32_t p = (uint32_t)c.casc_prom[row + i];
+    uint32_t st = 0;
+    const unsigned long long kp = casc_kappa(c, tab, a.now, base, p, st);
+    const unsigned long long ec = c.casc_e[base + p];
+    const unsigned long long e = kp > ec ? kp : ec;
+    if (e < bound) {
+        const int t = atomicAdd(&c.casc_n[4 * inst + 3], 1);
+        c.casc_pe[row + t] = e;
+        c.casc_aid[row + t] = (int32_t)p;
+    }
+    if (st) set_status(c.status, st);
+}
+
+// Zero the per-block counters and maxima the call changed: the listed
+// blocks, or every block when the list overflowed.
+__global__ void __launch_bounds__(256) k_casc_reset(DevCtx c)
+{
+    const int inst = blockIdx.y;
+    const long long base = (long long)inst * c.N;
+    const int nt = c.casc_n[4 * inst + 2];
+    const long long stride = (long long)gridDim.x * 256;
+    const long long i0 = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (nt <= c.casc_tl) {
+        const int32_t *touch = c.casc_touch + (long long)inst * c.casc_tl;
+        for (long long i = i0; i < nt; i += stride) {
+            const int32_t p = touch[i];
+            c.casc_cnt[base + p] = 0;
+            c.casc_e[base + p] = 0ull;
+        }
+    } else {
+        for (long long b = i0; b < c.N; b += stride) {
+            c.casc_cnt[base + b] = 0;
+            c.casc_e[base + b] = 0ull;
+        }
+    }
+}
+
 __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a)
 {
     extern __shared__ unsigned long long casc_lds[];
@@ -1908,7 +2010,7 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
     CascEl *cur = reinterpret_cast<CascEl *>(casc_lds);  // [kmax] sorted candidates
     CascEl *nw = cur + kmax;                             // [pow2 >= kmax] the round's new blocks
     __shared__ ScoreTab tab;
-    __shared__ int n_cur_s, n_new_s, n_touch_s;
+    __shared__ int n_cur_s, n_new_s, n_touch_s, n_adm_s;
     __shared__ uint32_t st_s;
     const int inst = blockIdx.x;
     const int tid = threadIdx.x;
@@ -1918,21 +2020,22 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
     int32_t *cnt = c.casc_cnt + base;
     unsigned long long *emax = c.casc_e + base;
     int32_t *touch = c.casc_touch + (long long)inst * c.casc_tl;
+    const int32_t *adm = c.casc_aid + (long long)inst * kmax;
+    const unsigned long long *adm_e = c.casc_pe + (long long)inst * kmax;
+    const int d0 = a.decision_count[inst];
     load_score_tab(tab, c.state[inst], c);
     if (tid == 0) {
-        n_cur_s = a.decision_count[inst];
-        n_touch_s = 0;
+        n_cur_s = d0;
+        n_touch_s = c.casc_n[4 * inst];
+        n_adm_s = c.casc_n[4 * inst + 3];
         st_s = 0;
     }
-    __syncthreads();
-    const int d0 = n_cur_s;
     uint32_t st = 0;
-    // round 0: the snapshot decision, already in kappa order
+    // the snapshot decision, already in kappa order
     for (int j = tid; j < d0; j += CASC_THREADS) {
-        const uint32_t b = (uint32_t)dec[j];
         CascEl x;
-        x.e = casc_kappa(c, tab, a.now, base, b, st);
-        x.id = b;
+        x.e = c.casc_k0[(long long)inst * kmax + j];
+        x.id = (uint32_t)dec[j];
         x.rnd = 0;
         cur[j] = x;
     }
@@ -1946,56 +2049,70 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
         bound.e = ~0ull;
         bound.rnd = 0xFFFFFFFFu;
         if (n_cur >= k && k > 0) bound = cur[k - 1];
-        // each thread's (up to CASC_PER) frontier blocks, their loads and
-        // atomics in flight together
-        CascEl fx[CASC_PER];
-        int32_t fp[CASC_PER];
-#pragma unroll
-        for (int u = 0; u < CASC_PER; ++u) {
-            const int j = tid + u * CASC_THREADS;
-            fx[u] = cur[j < n_cur ? j : 0];
-            const bool f = j < n_cur && fx[u].rnd == r;
-            const int32_t p = c.parent[base + (f ? fx[u].id : 0u)];
-            fp[u] = (f && p >= 0 && p < c.N) ? p : -1;
-        }
-#pragma unroll
-        for (int u = 0; u < CASC_PER; ++u)
-            if (fp[u] >= 0) atomicMax(&emax[fp[u]], fx[u].e);
-        // the children's E are in before they are counted: this workgroup's
-        // atomics all go to one L2, so waiting for them to complete suffices
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        int old[CASC_PER], cc[CASC_PER];
-#pragma unroll
-        for (int u = 0; u < CASC_PER; ++u) {
-            old[u] = fp[u] >= 0 ? atomicAdd(&cnt[fp[u]], 1) : -2;
-            cc[u] = c.child_count[base + (fp[u] >= 0 ? fp[u] : 0)];
-        }
-        // pairs with the release above: a last child sees every sibling's E
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        bool last[CASC_PER];
-        uint32_t pm[CASC_PER];
-#pragma unroll
-        for (int u = 0; u < CASC_PER; ++u) {
-            if (old[u] == 0) {
-                const int t = atomicAdd(&n_touch_s, 1);
-                if (t < c.casc_tl) touch[t] = fp[u];
+        if (r == 0) {
+            // the parents that round 0 completed, below the snapshot's bound
+            const int n_adm = n_adm_s;
+            for (int i = tid; i < n_adm; i += CASC_THREADS) {
+                CascEl y;
+                y.e = adm_e[i];
+                y.id = (uint32_t)adm[i];
+                y.rnd = 1;
+                nw[i] = y;
             }
-            last[u] = fp[u] >= 0 && old[u] + 1 == cc[u];  // its last cached child
-            pm[u] = c.meta[base + (fp[u] >= 0 ? fp[u] : 0)];
-            last[u] = last[u] && (pm[u] & (SAE_META_VALID | SAE_META_REF)) == SAE_META_VALID;
-        }
+            if (tid == 0) n_new_s = n_adm;
+        } else {
+            // each thread's (up to CASC_PER) frontier blocks; once the parent
+            // is known, its maximum, count and every field its kappa needs go
+            // out together
+            CascEl fx[CASC_PER];
+            int32_t fp[CASC_PER];
 #pragma unroll
-        for (int u = 0; u < CASC_PER; ++u) {
-            if (!last[u]) continue;
-            const uint32_t p = (uint32_t)fp[u];
-            CascEl y;
-            const unsigned long long kp = casc_kappa(c, tab, a.now, base, p, st);
-            const unsigned long long ec = atomicMax(&emax[p], 0ull);  // every child's E is in by now
-            y.e = kp > ec ? kp : ec;
-            y.id = p;
-            y.rnd = r + 1;
-            if (!casc_less(y, bound)) continue;  // cannot be among the first k
-            nw[atomicAdd(&n_new_s, 1)] = y;
+            for (int u = 0; u < CASC_PER; ++u) {
+                const int j = tid + u * CASC_THREADS;
+                fx[u] = cur[j < n_cur ? j : 0];
+                const bool f = j < n_cur && fx[u].rnd == r;
+                const int32_t p = c.parent[base + (f ? fx[u].id : 0u)];  // unconditional: no wait per block
+                fp[u] = (f && p >= 0 && p < c.N) ? p : -1;
+            }
+            int old[CASC_PER], cc[CASC_PER], pla[CASC_PER];
+            uint32_t pm[CASC_PER], po[CASC_PER];
+#pragma unroll
+            for (int u = 0; u < CASC_PER; ++u) {
+                old[u] = -2;
+                if (fp[u] >= 0) {
+                    const long long q = base + fp[u];
+                    atomicMax(&emax[fp[u]], fx[u].e);
+                    old[u] = atomicAdd(&cnt[fp[u]], 1);
+                    cc[u] = c.child_count[q];
+                    pm[u] = c.meta[q];
+                    pla[u] = c.la[q];
+                    po[u] = c.off[q];
+                }
+            }
+            // every maximum of this round is performed (in the one L2 this
+            // workgroup's atomics go to) before any is read back below
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __syncthreads();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+            for (int u = 0; u < CASC_PER; ++u) {
+                if (fp[u] < 0) continue;
+                if (old[u] == 0) {
+                    const int t = atomicAdd(&n_touch_s, 1);
+                    if (t < c.casc_tl) touch[t] = fp[u];
+                }
+                // its last cached child, of a valid and unreferenced parent
+                if (old[u] + 1 != cc[u] || (pm[u] & (SAE_META_VALID | SAE_META_REF)) != SAE_META_VALID) continue;
+                const uint32_t p = (uint32_t)fp[u];
+                CascEl y;
+                const unsigned long long kp = casc_kappa_of(tab, a.now, p, pm[u], pla[u], po[u], st);
+                const unsigned long long ec = __hip_atomic_load(&emax[p], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                y.e = kp > ec ? kp : ec;
+                y.id = p;
+                y.rnd = r + 1;
+                if (!casc_less(y, bound)) continue;  // cannot be among the first k
+                nw[atomicAdd(&n_new_s, 1)] = y;
+            }
         }
         __syncthreads();
         const int n_new = n_new_s;
@@ -2024,20 +2141,23 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
                 __syncthreads();
             }
         }
-        // merge by rank, everything read before anything is written
+        // merge by rank, everything read before anything is written; the
+        // candidates below the smallest new block keep their places
+        const int pos0 = casc_rank(cur, n_cur, nw[0]);
         CascEl xc[CASC_PER], xn[CASC_PER];
         int rc[CASC_PER], rn[CASC_PER];
 #pragma unroll
         for (int u = 0; u < CASC_PER; ++u) {
             const int j = tid + u * CASC_THREADS;
+            const int jc = pos0 + j;
             rc[u] = rn[u] = 0x7FFFFFFF;
-            if (j < n_cur) {
-                xc[u] = cur[j];
-                rc[u] = j + casc_rank(nw, n_new, xc[u]);
+            if (jc < n_cur) {
+                xc[u] = cur[jc];
+                rc[u] = jc + casc_rank(nw, n_new, xc[u]);
             }
             if (j < n_new) {
                 xn[u] = nw[j];
-                rn[u] = j + casc_rank(cur, n_cur, xn[u]);
+                rn[u] = j + pos0 + casc_rank(cur + pos0, n_cur - pos0, xn[u]);
             }
         }
         __syncthreads();
@@ -2051,23 +2171,14 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
     }
     const int d = min(k, n_cur_s);
     for (int j = tid; j < d; j += CASC_THREADS) dec[j] = (int32_t)cur[j].id;
-    // reset the per-block entries this call changed
-    const int nt = n_touch_s;
-    if (nt <= c.casc_tl) {
-        for (int t = tid; t < nt; t += CASC_THREADS) {
-            const int32_t p = touch[t];
-            cnt[p] = 0;
-            emax[p] = 0ull;
-        }
-    } else {
-        for (long long b = tid; b < c.N; b += CASC_THREADS) {
-            cnt[b] = 0;
-            emax[b] = 0ull;
-        }
-    }
+    // the per-block entries this call changed are reset by k_casc_reset
     if (st) atomicOr(&st_s, st);
     __syncthreads();
     if (tid == 0) {
+        c.casc_n[4 * inst] = 0;
+        c.casc_n[4 * inst + 1] = 0;
+        c.casc_n[4 * inst + 2] = n_touch_s;
+        c.casc_n[4 * inst + 3] = 0;
         a.decision_count[inst] = d;
         commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
         set_status(c.status, st_s);
@@ -2159,6 +2270,14 @@ hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s)
     const size_t lds = (size_t)(c.max_k + P) * sizeof(CascEl);
     hipError_t e = allow_lds((const void *)k_cascade, lds);
     if (e != hipSuccess) return e;
+    const dim3 g0((c.max_k + CASC0_THREADS - 1) / CASC0_THREADS, c.n_inst);
+    hipLaunchKernelGGL(k_casc_round0, g0, dim3(CASC0_THREADS), 0, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_casc_parents, g0, dim3(CASC0_THREADS), 0, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_cascade, dim3(c.n_inst), dim3(CASC_THREADS), lds, s, c, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the touched-block list holds at most 8 max_k entries: 4 per thread
+    hipLaunchKernelGGL(k_casc_reset, dim3((c.casc_tl + 4 * 256 - 1) / (4 * 256), c.n_inst), dim3(256), 0, s, c);
     return hipGetLastError();
 }

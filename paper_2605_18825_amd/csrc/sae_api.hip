@@ -194,7 +194,10 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.ivl, d.ln_mask ? I * Q * SAE_IVL_CAP : 0) &&
               dev_alloc(c, &d.pm_rec, (long long)d.max_req * SAE_MAX_QUEUES) &&
               dev_alloc(c, &d.casc_cnt, I * d.N) && dev_alloc(c, &d.casc_e, I * d.N) &&
-              dev_alloc(c, &d.casc_touch, I * 8ll * d.max_k);
+              dev_alloc(c, &d.casc_touch, I * 8ll * d.max_k) && dev_alloc(c, &d.casc_k0, I * d.max_k) &&
+              dev_alloc(c, &d.casc_prom, I * d.max_k) && dev_alloc(c, &d.casc_pe, I * d.max_k) &&
+              dev_alloc(c, &d.casc_aid, I * d.max_k) &&
+              dev_alloc(c, &d.casc_n, I * 4);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);
         delete c;

@@ -156,6 +156,16 @@ struct DevCtx {
     unsigned long long *casc_e;     // [n_inst][N]
     int32_t *casc_touch;            // [n_inst][casc_tl]
     int32_t casc_tl;
+    // the first round's output: kappa of each snapshot victim, the parents
+    // whose last cached child it was, those of them below the admission
+    // bound with their E, and per instance the counts of touched blocks,
+    // listed and admitted parents (zero between calls) and the call's final
+    // count of touched blocks
+    unsigned long long *casc_k0;    // [n_inst][max_k]
+    int32_t *casc_prom;             // [n_inst][max_k]
+    int32_t *casc_aid;              // [n_inst][max_k]
+    unsigned long long *casc_pe;    // [n_inst][max_k]
+    int32_t *casc_n;                // [n_inst][4]: touched, listed, final touched, admitted
 };
 
 // Positional bin of a block (decay-power learner): floor(8 o_b / o_max) with
