@@ -91,7 +91,7 @@ def main():
                          "(a plain copy of known size for calibrating HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU: this build has no multi-GPU path (see DESIGN.md, sharding).",
+        print("bench.py measures one GPU: the library has no multi-GPU path, so --gpus must be 1.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -16,7 +16,7 @@ One `OracleCache` object is one cache instance.  Its state follows the paper:
   ``queue_hits[q]`` / ``queue_evictions[q]`` (Algorithm 2);
 * the learned parameters w_tau, alpha_q, mu_q, sigma_q, gamma.
 
-Readings of points where the paper is silent (each listed in the design doc):
+Readings of points where the paper is silent:
 
 * A block is evictable iff it is valid, a leaf (no cached child) and
   unreferenced: tail-first eviction (Sec. 2.1 figure b) of free blocks.

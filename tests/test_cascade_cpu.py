@@ -3,7 +3,7 @@ with a parent that loses its last child evictable for the next call) against
 the snapshot decision the HIP path takes: the oracle's two cascade versions
 agree, the cascade reduces to the snapshot decision when no parent can be
 promoted, and what batching changes is measured on the synthetic pool and on
-trace replay (printed; the design doc quotes it)."""
+trace replay (printed)."""
 import numpy as np
 import pytest
 

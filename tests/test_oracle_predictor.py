@@ -10,7 +10,8 @@ import pytest
 from oracle import predictor as P
 from synth import predictor as S
 
-# parity tolerance of the predictor's logit, relative to 1 + |y|
+# parity tolerance of the predictor's logit, relative to 1 + |y|: the rigorous fp32
+# bound is far too loose here, so the tests below pin this one instead
 TOL = 1e-4
 
 
