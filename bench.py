@@ -78,6 +78,37 @@ def cpu_baseline(cfg, pool, reqs, lens, budget_s):
                        "blocks, feedback) on one host core, %.1f s" % (steps, el))
 
 
+def cpu_recency_lists(cfg, pool, reps=10):
+    """Part of the CPU baseline leg: a faster exact CPU selection (per-(queue, type) recency lists, the
+    per-queue heap idea) on the same pool: score+select without commit, timed
+    apart from building the lists (which a live cache keeps up incrementally);
+    the oracle's full-sort selection of the same call is timed beside it and
+    the two decisions are compared."""
+    import numpy as np
+    import oracle
+    from oracle.recency import RecencyLists
+    prm = oracle.Params(len(cfg["kinds"]), mu=cfg["mu"], sigma=cfg["sigma"], K=cfg["k"])
+    oc = oracle.OracleCache(pool["n_blocks"], cfg["kinds"], prm)
+    oc.bind(pool["last_access"], pool["queue"], oracle.block_type(pool["counts"]), pool["ntok"], pool["ob"],
+            pool["omax"], pool["valid"], pool["ref_count"], pool["parent"], pool["hash"], pool["access_count"])
+    now, k = pool["now"], cfg["k"]
+    t0 = time.perf_counter()
+    rl = RecencyLists(oc)
+    t_build = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        _, _, dec = rl.score_select(now, k)
+    t_sel = (time.perf_counter() - t0) / reps
+    t0 = time.perf_counter()
+    _, _, dec_o = oc.score_select(now, k)
+    t_or = time.perf_counter() - t0
+    return dict(value=pool["n_blocks"] / t_sel / 1e9, unit="G blk/s", cores=1, kind="recency lists (exact)",
+                ms_per_select=t_sel * 1e3, build_s=t_build, blocks_scored=int(rl.visited),
+                oracle_select_ms=t_or * 1e3, same_decision_as_oracle=bool(np.array_equal(dec, dec_o)),
+                sample="%d score+select calls (no commit) on one host core; log-normal and recency queues walk "
+                       "their per-type lists, the structural queue is scanned whole" % reps)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -296,6 +327,7 @@ def main():
         line["calib_copy_bytes"] = n * 4
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(cfg, pool, reqs, lens, args.cpu_seconds)
+        line["cpu_baseline"]["recency_lists"] = cpu_recency_lists(cfg, pool)
     print(json.dumps(line), flush=True)
 
 

@@ -12,6 +12,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dsr.c")
+_SRC_RL = os.path.join(_HERE, "recency.c")  # the recency-list selection (a second CPU baseline)
 _LIB = os.path.join(_HERE, "liboracle_dsr.so")
 
 # -ffp-contract=off: no fused multiply-add unless written as fmaf();
@@ -20,11 +21,11 @@ CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-st
 
 
 def build(force=True):
-    """Compile dsr.c into liboracle_dsr.so with gcc."""
+    """Compile dsr.c and recency.c into liboracle_dsr.so with gcc."""
     if not force and os.path.exists(_LIB):
         return _LIB
     tmp = _LIB + ".tmp%d" % os.getpid()
-    subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+    subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, _SRC_RL, "-lm"])
     os.replace(tmp, _LIB)
     return _LIB
 
@@ -35,7 +36,8 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC),
+                                                                   os.path.getmtime(_SRC_RL)):
             build()
         L = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
@@ -57,6 +59,10 @@ def lib():
         L.oracle_pow01_v.argtypes = [i64, P, f32, P]
         L.oracle_p_lognormal_v.argtypes = [i64, P, f32, f32, P]
         L.oracle_p_structural_v.argtypes = [i64, P, P, f32, P]
+        L.oracle_rl_select.argtypes = [i32, i32, i32, i32, f32, f32, P, P, P, P, P, P, P, P]
+        L.oracle_rl_select.restype = i32
+        L.oracle_struct_select.argtypes = [i32, i32, f32, P, i64, P, P, P, P, P, P, P, P]
+        L.oracle_struct_select.restype = i32
         _lib = L
     return _lib
 

@@ -618,7 +618,9 @@ __global__ void __launch_bounds__(kPlaceThreads) k_pm_place(DevCtx c, int n_req,
 // Commit, per victim: free the block, erase its index entry, count it
 // (Algorithm 3 evicted[tau], Algorithm 2 queue_evictions[q]), update its
 // parent and record it in recently_evicted.
-__global__ void k_commit(DevCtx c, const int32_t *decision)
+constexpr int kCommitThreads = 64;
+static_assert(SAE_CF_N <= kCommitThreads, "one thread per counter field");
+__global__ void __launch_bounds__(kCommitThreads) k_commit(DevCtx c, const int32_t *decision)
 {
     __shared__ int32_t sums[SAE_CF_N];
     const int inst = blockIdx.y;
@@ -781,7 +783,9 @@ hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, 
 
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s)
 {
-    dim3 grid((unsigned)((c.max_k + kThreads - 1) / kThreads), (unsigned)c.n_inst);
-    hipLaunchKernelGGL(k_commit, grid, dim3(kThreads), 0, s, c, (const int32_t *)a.decision);
+    // one wave per workgroup: a victim is a chain of scattered accesses, so
+    // the victims are spread over as many compute units as possible
+    dim3 grid((unsigned)((c.max_k + kCommitThreads - 1) / kCommitThreads), (unsigned)c.n_inst);
+    hipLaunchKernelGGL(k_commit, grid, dim3(kCommitThreads), 0, s, c, (const int32_t *)a.decision);
     return hipGetLastError();
 }
