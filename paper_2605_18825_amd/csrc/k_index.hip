@@ -413,9 +413,14 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
             const uint64_t *hr = hashes + (long long)r * max_len;
             int m = 0;
             int j0 = 0;
+            // software-pipelined over chunks of 64 hashes: the next chunk's
+            // hashes are fetched with this chunk's probe, and its probe goes
+            // out right after this chunk's block fields are requested, so a
+            // matched chunk costs no extra round trip for its fields
+            int32_t id = (lane < len) ? index_find(tab, c.index_mask, hr[lane]) : -1;
+            unsigned long long hnext = (SAE_WAVE + lane < len) ? hr[SAE_WAVE + lane] : 0ull;
             for (; j0 < len; j0 += SAE_WAVE) {
                 const int j = j0 + lane;
-                const int32_t id = (j < len) ? index_find(tab, c.index_mask, hr[j]) : -1;
                 const bool miss = (j < len) && (id < 0);
                 const unsigned long long mm = __ballot(miss);
                 const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
@@ -423,10 +428,19 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                 const bool hit = lane < lim;
                 int q = 0, ty = 0;
                 uint32_t bin = 0;
+                // unconditional (block 0 for lanes without a hit): a load in a
+                // divergent block would be waited for at its end
+                const long long gh = base + (hit ? id : 0);
+                const uint32_t off = bins ? c.off[gh] : 0u;  // loaded beside meta, not after it
+                const uint32_t mt = c.meta[gh];
+                int32_t idn = -1;
+                if (!mm && j0 + SAE_WAVE < len) {  // uniform: this chunk matched whole
+                    const int jn = j + SAE_WAVE;
+                    idn = (jn < len) ? index_find(tab, c.index_mask, hnext) : -1;
+                    hnext = (jn + SAE_WAVE < len) ? hr[jn + SAE_WAVE] : 0ull;
+                }
                 if (hit) {
                     const long long g = base + id;
-                    const uint32_t off = bins ? c.off[g] : 0u;  // loaded beside meta, not after it
-                    const uint32_t mt = c.meta[g];
                     q = meta_queue(mt);
                     ty = meta_type(mt) % SAE_N_TYPES;
                     if (bins && ((c.struct_mask >> q) & 1u)) bin = pos_bin(off);
@@ -467,6 +481,7 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                     j0 += SAE_WAVE;
                     break;
                 }
+                id = idn;
             }
             if (mid)
                 for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
