@@ -1866,11 +1866,12 @@ int pow2_at_least(int x)
 // when its last cached child arrives, with E = max(kappa(parent), the largest
 // E of its children) and round r + 1 (which orders equal E child first).  The
 // new blocks are sorted and merged into the sorted candidates, which keep
-// only the first k.  Round 0 (up to k blocks), the E of the parents it
-// completes and the final reset of the counters run over many workgroups
-// (k_casc_round0, k_casc_parents, k_casc_reset); the later rounds, whose
-// frontiers are small, in one workgroup of 1024 threads per instance
-// (k_cascade).
+// only the first k.  Round 0 (up to k blocks) and the E of the parents it
+// completes run over many workgroups (k_casc_round0, k_casc_parents); the
+// later rounds, whose frontiers are small, in one workgroup of 1024 threads
+// per instance (k_cascade).  The per-block counters come in two sets that
+// calls alternate between; round 0 also zeroes the entries the previous call
+// left in the other set, so they are clean when the call after uses them.
 constexpr int CASC_THREADS = 1024;
 constexpr int CASC_PER = 4;  // candidates per thread: k <= CASC_THREADS * CASC_PER
 constexpr int CASC0_THREADS = 64;
@@ -1923,6 +1924,26 @@ __global__ void __launch_bounds__(CASC0_THREADS) k_casc_round0(DevCtx c, SelectA
     const int inst = blockIdx.y;
     const long long base = (long long)inst * c.N;
     load_score_tab(tab, c.state[inst], c);
+    {
+        // zero what the previous call left in the other set: its touched
+        // blocks, or every block when its list overflowed
+        const int nt = c.casc_nt_prev[inst];
+        const long long stride = (long long)gridDim.x * CASC0_THREADS;
+        const long long i0 = (long long)blockIdx.x * CASC0_THREADS + threadIdx.x;
+        if (nt <= c.casc_tl) {
+            const int32_t *touch = c.casc_touch_prev + (long long)inst * c.casc_tl;
+            for (long long i = i0; i < nt; i += stride) {
+                const int32_t p = touch[i];
+                c.casc_cnt_prev[base + p] = 0;
+                c.casc_e_prev[base + p] = 0ull;
+            }
+        } else {
+            for (long long b = i0; b < c.N; b += stride) {
+                c.casc_cnt_prev[base + b] = 0;
+                c.casc_e_prev[base + b] = 0ull;
+            }
+        }
+    }
     __syncthreads();
     const int j = blockIdx.x * CASC0_THREADS + threadIdx.x;
     if (j >= a.decision_count[inst]) return;
@@ -1977,30 +1998,6 @@ __global__ void __launch_bounds__(CASC0_THREADS) k_casc_parents(DevCtx c, Select
         c.casc_aid[row + t] = (int32_t)p;
     }
     if (st) set_status(c.status, st);
-}
-
-// Zero the per-block counters and maxima the call changed: the listed
-// blocks, or every block when the list overflowed.
-__global__ void __launch_bounds__(256) k_casc_reset(DevCtx c)
-{
-    const int inst = blockIdx.y;
-    const long long base = (long long)inst * c.N;
-    const int nt = c.casc_n[4 * inst + 2];
-    const long long stride = (long long)gridDim.x * 256;
-    const long long i0 = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (nt <= c.casc_tl) {
-        const int32_t *touch = c.casc_touch + (long long)inst * c.casc_tl;
-        for (long long i = i0; i < nt; i += stride) {
-            const int32_t p = touch[i];
-            c.casc_cnt[base + p] = 0;
-            c.casc_e[base + p] = 0ull;
-        }
-    } else {
-        for (long long b = i0; b < c.N; b += stride) {
-            c.casc_cnt[base + b] = 0;
-            c.casc_e[base + b] = 0ull;
-        }
-    }
 }
 
 __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a)
@@ -2171,13 +2168,14 @@ __global__ void __launch_bounds__(CASC_THREADS) k_cascade(DevCtx c, SelectArgs a
     }
     const int d = min(k, n_cur_s);
     for (int j = tid; j < d; j += CASC_THREADS) dec[j] = (int32_t)cur[j].id;
-    // the per-block entries this call changed are reset by k_casc_reset
+    // the per-block entries this call changed are zeroed by the next call's
+    // round 0 (the other set is then in use)
     if (st) atomicOr(&st_s, st);
     __syncthreads();
     if (tid == 0) {
         c.casc_n[4 * inst] = 0;
         c.casc_n[4 * inst + 1] = 0;
-        c.casc_n[4 * inst + 2] = n_touch_s;
+        c.casc_nt[inst] = n_touch_s;
         c.casc_n[4 * inst + 3] = 0;
         a.decision_count[inst] = d;
         commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
@@ -2263,8 +2261,20 @@ hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream
     return hipGetLastError();
 }
 
-hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s)
+hipError_t launch_cascade(const DevCtx &c0, const SelectArgs &a, hipStream_t s, int set)
 {
+    // this call's counter set and the other one
+    DevCtx c = c0;
+    const long long nb = (long long)c0.n_inst * c0.N, nl = (long long)c0.n_inst * c0.casc_tl;
+    const long long mine = set ? 1 : 0, other = 1 - mine;
+    c.casc_cnt = c0.casc_cnt + mine * nb;
+    c.casc_e = c0.casc_e + mine * nb;
+    c.casc_touch = c0.casc_touch + mine * nl;
+    c.casc_nt = c0.casc_nt + mine * c0.n_inst;
+    c.casc_cnt_prev = c0.casc_cnt + other * nb;
+    c.casc_e_prev = c0.casc_e + other * nb;
+    c.casc_touch_prev = c0.casc_touch + other * nl;
+    c.casc_nt_prev = c0.casc_nt + other * c0.n_inst;
     int P = 1;
     while (P < c.max_k) P <<= 1;
     const size_t lds = (size_t)(c.max_k + P) * sizeof(CascEl);
@@ -2276,8 +2286,5 @@ hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_casc_parents, g0, dim3(CASC0_THREADS), 0, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_cascade, dim3(c.n_inst), dim3(CASC_THREADS), lds, s, c, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    // the touched-block list holds at most 8 max_k entries: 4 per thread
-    hipLaunchKernelGGL(k_casc_reset, dim3((c.casc_tl + 4 * 256 - 1) / (4 * 256), c.n_inst), dim3(256), 0, s, c);
     return hipGetLastError();
 }

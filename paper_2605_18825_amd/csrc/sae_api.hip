@@ -22,6 +22,7 @@ struct sae_ctx {
     long long skip_cap = 0;
     std::vector<void *> allocs;
     bool prof = false;
+    int casc_set = 0;  // the counter set the next cascading decision uses
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_used;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_free;
 };
@@ -193,8 +194,9 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N) &&
               dev_alloc(c, &d.ivl, d.ln_mask ? I * Q * SAE_IVL_CAP : 0) &&
               dev_alloc(c, &d.pm_rec, (long long)d.max_req * SAE_MAX_QUEUES) &&
-              dev_alloc(c, &d.casc_cnt, I * d.N) && dev_alloc(c, &d.casc_e, I * d.N) &&
-              dev_alloc(c, &d.casc_touch, I * 8ll * d.max_k) && dev_alloc(c, &d.casc_k0, I * d.max_k) &&
+              dev_alloc(c, &d.casc_cnt, 2 * I * d.N) && dev_alloc(c, &d.casc_e, 2 * I * d.N) &&
+              dev_alloc(c, &d.casc_touch, 2 * I * 8ll * d.max_k) && dev_alloc(c, &d.casc_nt, 2 * I) &&
+              dev_alloc(c, &d.casc_k0, I * d.max_k) &&
               dev_alloc(c, &d.casc_prom, I * d.max_k) && dev_alloc(c, &d.casc_pe, I * d.max_k) &&
               dev_alloc(c, &d.casc_aid, I * d.max_k) &&
               dev_alloc(c, &d.casc_n, I * 4);
@@ -570,7 +572,10 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
         e = launch_select_scan(c->dc, a, s, e0, e1);
         if (e == hipSuccess) e = launch_merge(c->dc, a, s);
     }
-    if (e == hipSuccess && (flags & SAE_SS_CASCADE)) e = launch_cascade(c->dc, a, s);
+    if (e == hipSuccess && (flags & SAE_SS_CASCADE)) {
+        e = launch_cascade(c->dc, a, s, c->casc_set);
+        c->casc_set ^= 1;
+    }
     if (e != hipSuccess) return hip_fail(c, e, "sae_score_select");
     if (flags & SAE_SS_COMMIT) {
         e = launch_commit(c->dc, a, s);

@@ -150,11 +150,19 @@ struct DevCtx {
     uint32_t ln_mask;          // bit q: queue q is log-normal
     uint32_t struct_mask;      // bit q: queue q is structural
     // cascading decisions (SAE_SS_CASCADE): per block, cached children found
-    // among the candidates so far and the largest rank among them (zero
-    // between calls), and the blocks whose entries a call changed
+    // among the candidates so far and the largest rank among them, and the
+    // blocks whose entries a call changed with their count.  Two sets that
+    // calls alternate between: a call's first round clears what the previous
+    // call left in the other set (the pointers below are the call's own set
+    // and, in the *_prev fields, the other one).
     int32_t *casc_cnt;              // [n_inst][N]
     unsigned long long *casc_e;     // [n_inst][N]
     int32_t *casc_touch;            // [n_inst][casc_tl]
+    int32_t *casc_nt;               // [n_inst] touched blocks of the set's last call
+    int32_t *casc_cnt_prev;
+    unsigned long long *casc_e_prev;
+    int32_t *casc_touch_prev;
+    int32_t *casc_nt_prev;
     int32_t casc_tl;
     // the first round's output: kappa of each snapshot victim, the parents
     // whose last cached child it was, those of them below the admission
@@ -165,7 +173,7 @@ struct DevCtx {
     int32_t *casc_prom;             // [n_inst][max_k]
     int32_t *casc_aid;              // [n_inst][max_k]
     unsigned long long *casc_pe;    // [n_inst][max_k]
-    int32_t *casc_n;                // [n_inst][4]: touched, listed, final touched, admitted
+    int32_t *casc_n;                // [n_inst][4]: touched, listed, (unused), admitted
 };
 
 // Positional bin of a block (decay-power learner): floor(8 o_b / o_max) with
@@ -461,7 +469,7 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
                               hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
-hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s);
+hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s, int set);
 hipError_t launch_predict(int n, int d, const uint16_t *h, const uint16_t *w1, const float *b1, const float *w2,
                           const float *b2, const float *w3, const float *b3, float *work, float *logit,
                           uint8_t *pred, hipStream_t s);
