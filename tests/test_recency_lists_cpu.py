@@ -97,3 +97,17 @@ def test_walk_visits_few_blocks():
     struct = int((ev & (c.queue == 1)).sum())
     walked = rl.visited - struct  # the structural queue is scanned whole
     assert walked < 0.05 * lnrec, (walked, lnrec)
+
+
+def test_nothing_evictable_and_one_queue():
+    """Every block referenced: every list empty, the decision empty; then
+    only one log-normal queue holds evictable blocks."""
+    c = make_cache(13, 5_000, mu=[0, 0, 11.7, 9.2, 0], sigma=[1, 1, 1.25, 1.34, 1])
+    c.ref_count[:] = 1
+    rl = check_equal(c, 64)
+    assert rl.visited == 0
+    _, _, dec = rl.score_select(NOW, 64)
+    assert dec.size == 0
+    c.ref_count[:] = np.where(c.queue == 2, 0, 1)
+    check_equal(c, 64)
+    check_equal(c, 100_000)
