@@ -39,7 +39,10 @@
  *                      bit 9-12 num_tokens - 1 (Algorithm 1, stage 1 key)
  *  off          uint32 bit 0-15 o_b, bit 16-31 o_max: block offset and the
  *                      maximum offset in its request (Eq. 2)
- *  hash         uint64 chained content hash (0 and 2^64-1 are reserved)
+ *  hash         uint64 chained content hash; 0 and 2^64-1 are reserved (they
+ *                      mark empty and deleted index slots): a block with one is
+ *                      refused by Add() and never indexed, and a request hash
+ *                      with one never matches
  *  parent       int32  parent block id in the prefix tree, or -1
  *  child_count  int32  number of cached children
  *  ref_count    int32  number of running requests using the block
@@ -106,7 +109,10 @@ enum {
     SAE_ST_FUTURE_ACCESS = 1u << 3,   /* last_access > now (scored as dt = 0)        */
     SAE_ST_SLOT_BUSY = 1u << 4,       /* insert into a valid slot (insert skipped)   */
     SAE_ST_SELECT_FALLBACK = 1u << 5, /* exact slow path of the pool scan was used   */
-    SAE_ST_BAD_BLOCK = 1u << 6        /* block id out of range (element skipped)     */
+    SAE_ST_BAD_BLOCK = 1u << 6,       /* block id out of range (element skipped)     */
+    SAE_ST_BAD_HASH = 1u << 7         /* a reserved hash (0 or 2^64-1) given to Add()
+                                         or found in a valid block by the index build:
+                                         that block is skipped (not added, not indexed) */
 };
 
 typedef struct {

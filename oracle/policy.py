@@ -67,6 +67,10 @@ N_TYPES = 5  # system, user, tool, response, cot — the order of Algorithm 3
 N_BINS = 8   # positional bins of the decay-power learner
 IVL_CAP = 4096  # intervals an Algorithm 4 buffer holds at most
 F32 = np.float32
+# Content hashes 0 and 2^64-1 are reserved by the boundary (they mark empty
+# and deleted index slots there): Add() refuses a block that carries one, the
+# index never holds one, so a request hash with one never matches.
+RESERVED_HASHES = (0, 2 ** 64 - 1)
 
 
 def block_type(counts):
@@ -201,7 +205,8 @@ class OracleCache:
         self.child_count[:] = 0
         has = self.valid & (self.parent >= 0)
         np.add.at(self.child_count, self.parent[has].astype(np.int64), 1)
-        self.index = {int(self.hash[b]): b for b in np.nonzero(self.valid)[0].tolist()}
+        self.index = {int(self.hash[b]): b for b in np.nonzero(self.valid)[0].tolist()
+                      if int(self.hash[b]) not in RESERVED_HASHES}
 
     def evictable(self):
         return self.valid & (self.child_count == 0) & (self.ref_count == 0)
@@ -364,8 +369,9 @@ class OracleCache:
             assert self.valid[b] and self.child_count[b] == 0 and self.ref_count[b] == 0
             self.valid[b] = False
             h = int(self.hash[b])
-            del self.index[h]
-            self.ghost[h] = (int(self.tau[b]), int(self.queue[b]), stamp, self.pos_bin(b))
+            if h not in RESERVED_HASHES:  # such a block was never indexed
+                del self.index[h]
+                self.ghost[h] = (int(self.tau[b]), int(self.queue[b]), stamp, self.pos_bin(b))
             self.evicted[self.tau[b]] += 1
             self.evictions[self.queue[b]] += 1
             par = int(self.parent[b])
@@ -431,8 +437,12 @@ class OracleCache:
     def insert(self, ids, hashes, parent, last_access, queue, tau, ntok, ob, omax):
         """Algorithm 1 Add() for a batch of new blocks placed in free slots.
         A hash still in recently_evicted counts one miss after eviction for the
-        type recorded at eviction, and leaves recently_evicted."""
+        type recorded at eviction, and leaves recently_evicted.  A block with a
+        reserved hash is refused (not added, and its parent gains no child)."""
+        refused = [int(h) in RESERVED_HASHES for h in np.asarray(hashes, np.uint64).tolist()]
         for i, b in enumerate(np.asarray(ids).tolist()):
+            if refused[i]:
+                continue
             assert not self.valid[b]
             h = int(hashes[i])
             assert h not in self.index
@@ -457,7 +467,7 @@ class OracleCache:
                 if self.kind[g[1]] == STRUCTURAL and self.prm.learn_gamma:
                     self.bin_missed[g[3]] += 1
         for i in range(len(ids)):
-            if parent[i] >= 0:
+            if parent[i] >= 0 and not refused[i]:
                 self.child_count[parent[i]] += 1
 
     def ref(self, ids, delta):
@@ -465,29 +475,33 @@ class OracleCache:
 
     # ------------------------------------------------------------- learners
     def token_weights(self):
-        """Algorithm 3 in fp32; counters decay by lambda = 99/100 (floored)."""
+        """Algorithm 3, in fp32.  Per type: when more than ten of its blocks
+        have been evicted, the weight is multiplied by 1 + eta * r, r the
+        share of those evictions that were asked for again, and clamped to
+        [0.1, 5]; both counts then lose 1 % (lambda = 0.99 as floor(99 x / 100))
+        whether or not the weight moved."""
         p = self.prm
         for t in range(N_TYPES):
             ev, mi = self.evicted[t], self.missed[t]
             if ev > 10:
-                rate = F32(mi) / F32(ev)
-                p.w[t] = clamp(p.w[t] * (F32(1.0) + p.eta * rate), 0.1, 5.0)
-            self.evicted[t] = (99 * ev) // 100
-            self.missed[t] = (99 * mi) // 100
+                returns_per_eviction = F32(mi) / F32(ev)
+                p.w[t] = clamp(p.w[t] * (F32(1.0) + p.eta * returns_per_eviction), 0.1, 5.0)
+            self.evicted[t], self.missed[t] = (99 * ev) // 100, (99 * mi) // 100
 
     def queue_weights(self):
-        """Algorithm 2 in fp32 over every queue except the evict-first one."""
+        """Algorithm 2, in fp32, for every queue but the evict-first one: with
+        more than five evictions since the last run, alpha moves the fraction
+        beta of the way to 1 + (hits per eviction) / T and is clamped to
+        [0.1, 3]; the queue's hit and eviction counts restart in any case."""
         p = self.prm
         for q in range(self.Q):
             if self.kind[q] == EVICT_FIRST:
                 continue
             h, e = self.hits[q], self.evictions[q]
             if e > 5:
-                eff = F32(h) / F32(e)
-                target = F32(1.0) + eff / p.T
-                p.alpha[q] = clamp(p.alpha[q] + p.beta * (target - p.alpha[q]), 0.1, 3.0)
-            self.hits[q] = 0
-            self.evictions[q] = 0
+                goal = F32(1.0) + (F32(h) / F32(e)) / p.T
+                p.alpha[q] = clamp(p.alpha[q] + p.beta * (goal - p.alpha[q]), 0.1, 3.0)
+            self.hits[q], self.evictions[q] = 0, 0
 
     def token_weights_ema(self):
         """The appendix text's token-weight rule (App. B): per type,

@@ -23,7 +23,7 @@ LEARN_TOKEN_EMA, LEARN_QUEUE_REL = 16, 32
 # the paper's initial token weights (system, user, tool, response, cot), Sec. 5
 PAPER_INIT_W = (2.0, 1.5, 1.0, 1.0, 0.1)
 ST_NAMES = {1: "INDEX_FULL", 2: "GHOST_FULL", 4: "BAD_OFFSET", 8: "FUTURE_ACCESS",
-            16: "SLOT_BUSY", 32: "SELECT_FALLBACK", 64: "BAD_BLOCK"}
+            16: "SLOT_BUSY", 32: "SELECT_FALLBACK", 64: "BAD_BLOCK", 128: "BAD_HASH"}
 
 
 def _ptr(t):

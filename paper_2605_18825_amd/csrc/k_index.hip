@@ -29,6 +29,7 @@ constexpr int kThreads = 256;
 __device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h)
 {
     const uint4 *t4 = reinterpret_cast<const uint4 *>(tab);
+    if (SAE_HASH_RESERVED(h)) return -1;
     const int lim = (int)(mask + 1 < (uint32_t)SAE_MAX_PROBES ? mask + 1 : (uint32_t)SAE_MAX_PROBES);
     uint32_t s = hash_home(h, mask);
     int seen = 0;
@@ -86,6 +87,7 @@ __device__ __forceinline__ void index_erase(IndexSlot *tab, uint32_t mask, unsig
 __device__ __forceinline__ int ghost_find(const GhostSlot *tab, uint32_t mask, const GhostEntry *ring,
                                           unsigned long long h, long long ev_now, int W, uint32_t *ring_pos)
 {
+    if (SAE_HASH_RESERVED(h)) return -1;
     uint32_t s = hash_home(h, mask);
     for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
         unsigned long long v = tab[s].hash;
@@ -260,7 +262,9 @@ __global__ void k_index_fill(DevCtx c, int census)
             const int inst = (int)(g / c.N);
             const int32_t b = (int32_t)(g - (long long)inst * c.N);
             IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-            if (!index_insert(tab, c.index_mask, c.hash[g], b)) set_status(c.status, SAE_ST_INDEX_FULL);
+            const unsigned long long h = c.hash[g];
+            if (SAE_HASH_RESERVED(h)) set_status(c.status, SAE_ST_BAD_HASH);
+            else if (!index_insert(tab, c.index_mask, h, b)) set_status(c.status, SAE_ST_INDEX_FULL);
             if (census) {
                 if (one_inst) atomicAdd(&cnt[meta_queue(m)], 1);
                 else atomicAdd(counter_slot(c, inst, blockIdx.x) + SAE_CF_RES + meta_queue(m), 1);
@@ -309,13 +313,18 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
         return;
     }
     long long g = (long long)inst * c.N + b;
+    unsigned long long h = hash[i];
+    if (SAE_HASH_RESERVED(h)) {
+        skip[i] = 1;
+        set_status(c.status, SAE_ST_BAD_HASH);
+        return;
+    }
     if (c.meta[g] & SAE_META_VALID) {
         skip[i] = 1;
         set_status(c.status, SAE_ST_SLOT_BUSY);
         return;
     }
     skip[i] = 0;
-    unsigned long long h = hash[i];
     uint32_t m = meta[i] & (0x7u | (0x7u << 3) | (0xFu << 9));
     c.meta[g] = (uint16_t)(m | SAE_META_VALID | SAE_META_LEAF);
     c.la[g] = la[i];
@@ -709,18 +718,19 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(DevCtx c, const int32
         atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
         atomicSub(&sums[SAE_CF_RES + meta_queue(m)], 1);
         meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
-        index_erase_from(tab, c.index_mask, h, si, vi);
+        const bool hashed = !SAE_HASH_RESERVED(h);  // a reserved hash was never indexed
+        if (hashed) index_erase_from(tab, c.index_mask, h, si, vi);
         if (has_p && before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
         GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
         const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
         GhostEntry e;
-        e.hash = h;
+        e.hash = hashed ? h : SAE_EMPTY_HASH;  // an empty entry is never found
         e.stamp = s.ev_before + d;
         e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
                (pos_bin(off) << SAE_TQ_BIN_SHIFT);
         e.pad_ = 0;
         ring[rp] = e;
-        if (!ghost_insert_from(gt, c.ghost_mask, h, rp, sg, vg)) set_status(c.status, SAE_ST_GHOST_FULL);
+        if (hashed && !ghost_insert_from(gt, c.ghost_mask, h, rp, sg, vg)) set_status(c.status, SAE_ST_GHOST_FULL);
     }
     __syncthreads();
     if (threadIdx.x < SAE_CF_N && sums[threadIdx.x])

@@ -8,6 +8,10 @@ namespace {
 
 __device__ __forceinline__ float clampf(float x, float lo, float hi) { return fminf(fmaxf(x, lo), hi); }
 
+// floor(0.99 x) in integers: the decay factor lambda = 0.99 of the eviction
+// feedback counters, applied without rounding error.
+__device__ __forceinline__ int32_t decay99(int32_t x) { return (int32_t)(((long long)x * 99) / 100); }
+
 // 128-bit unsigned sum kept as two 64-bit halves.
 struct U128 {
     unsigned long long lo, hi;
@@ -174,10 +178,10 @@ __device__ void token_weight_ema(InstState &s, int t)
     const float r_reuse = (h + a) > 0 ? (float)h / (float)(h + a) : 0.0f;
     const float target = 1.0f + r_miss * 5.0f + r_reuse * 2.0f;
     s.w[t] = clampf((1.0f - s.eta) * s.w[t] + s.eta * target, 0.1f, 5.0f);
-    s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
-    s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
-    s.type_hits[t] = (int32_t)(((long long)h * 99) / 100);
-    s.type_added[t] = (int32_t)(((long long)a * 99) / 100);
+    s.evicted[t] = decay99(ev);
+    s.missed[t] = decay99(mi);
+    s.type_hits[t] = decay99(h);
+    s.type_added[t] = decay99(a);
 }
 
 // The appendix text's queue-weight rule over all queues (one lane):
@@ -219,6 +223,37 @@ __device__ void queue_weights_rel(const DevCtx &c, InstState &s)
     }
 }
 
+// Token weight of type t (Algorithm 3).  A type whose evicted blocks keep
+// being asked for again is being evicted too eagerly: once more than ten of
+// its blocks have gone, its weight is multiplied by 1 + eta * (returns per
+// eviction) and kept in [0.1, 5].  Both counts then shrink by lambda, whether
+// or not the weight moved.  The fp32 operations run in this order: ratio,
+// times eta, plus one, times the weight.
+__device__ __forceinline__ void token_weight_alg3(InstState &s, int t)
+{
+    const int32_t ev = s.evicted[t], mi = s.missed[t];
+    if (ev > 10) s.w[t] = clampf(s.w[t] * (1.0f + s.eta * ((float)mi / (float)ev)), 0.1f, 5.0f);
+    s.evicted[t] = decay99(ev);
+    s.missed[t] = decay99(mi);
+}
+
+// Queue weight of queue q (Algorithm 2).  The target is 1 plus the queue's
+// prefix-match hits per eviction, scaled by 1 / T; with more than five
+// evictions since the last run, alpha moves the fraction beta of its distance
+// to the target and is kept in [0.1, 3].  The queue's counts restart in any
+// case.  fp32 order: ratio, over T, plus one, minus alpha, times beta, plus
+// alpha.
+__device__ __forceinline__ void queue_weight_alg2(InstState &s, int q)
+{
+    const int32_t h = s.hits[q], e = s.evictions[q];
+    if (e > 5) {
+        const float target = 1.0f + ((float)h / (float)e) / s.T;
+        s.alpha[q] = clampf(s.alpha[q] + s.beta * (target - s.alpha[q]), 0.1f, 3.0f);
+    }
+    s.hits[q] = 0;
+    s.evictions[q] = 0;
+}
+
 // Token-weight, queue-weight and decay-power learners on the lanes of one
 // wave, which touch disjoint fields: lane l < 5 updates token type l
 // (Algorithm 3 or the text's rule), lane 8 + q queue q (Algorithm 2), lane 16
@@ -229,36 +264,13 @@ __device__ void learners_23_gamma(const DevCtx &c, InstState &s, int l)
         if (s.learn & SAE_LEARN_TOKEN_EMA) {
             token_weight_ema(s, l);
         } else if (s.learn & SAE_LEARN_TOKEN_WEIGHTS) {
-            // Algorithm 3: raise the weight of types evicted too aggressively;
-            // both counters decay by lambda = 0.99, applied as floor(99 x / 100).
-            const int t = l;
-            int32_t ev = s.evicted[t], mi = s.missed[t];
-            if (ev > 10) {
-                float rate = (float)mi / (float)ev;
-                float step = s.eta * rate;
-                float grow = 1.0f + step;
-                s.w[t] = clampf(s.w[t] * grow, 0.1f, 5.0f);
-            }
-            s.evicted[t] = (int32_t)(((long long)ev * 99) / 100);
-            s.missed[t] = (int32_t)(((long long)mi * 99) / 100);
+            token_weight_alg3(s, l);
         }
     } else if (l == 16) {
         if (s.learn & SAE_LEARN_QUEUE_REL) queue_weights_rel(c, s);
     } else if (l >= 8 && l < 8 + c.Q) {
         const int q = l - 8;
-        if ((s.learn & SAE_LEARN_QUEUE_WEIGHTS) && c.kind[q] != SAE_KIND_EVICT_FIRST) {
-            // Algorithm 2: EMA of the queue weight toward 1 + efficiency / T.
-            int32_t h = s.hits[q], e = s.evictions[q];
-            if (e > 5) {
-                float eff = (float)h / (float)e;
-                float target = 1.0f + eff / s.T;
-                float diff = target - s.alpha[q];
-                float stepq = s.beta * diff;
-                s.alpha[q] = clampf(s.alpha[q] + stepq, 0.1f, 3.0f);
-            }
-            s.hits[q] = 0;
-            s.evictions[q] = 0;
-        }
+        if ((s.learn & SAE_LEARN_QUEUE_WEIGHTS) && c.kind[q] != SAE_KIND_EVICT_FIRST) queue_weight_alg2(s, q);
     } else if (l == SAE_WAVE - 1) {
         if (s.learn & SAE_LEARN_DECAY_POWER) decay_power(s);
     }

@@ -10,6 +10,9 @@
 #define SAE_WAVE 64
 #define SAE_EMPTY_HASH 0ull
 #define SAE_TOMB_HASH 0xFFFFFFFFFFFFFFFFull
+// The two reserved hash values mark empty and deleted table slots: a block
+// carrying one is never indexed, never found and never recorded as evicted.
+#define SAE_HASH_RESERVED(h) ((h) == SAE_EMPTY_HASH || (h) == SAE_TOMB_HASH)
 #define SAE_MAX_PROBES 65536
 
 // Radix digits of the selection: 11 bits -> 2048 bins.

@@ -190,3 +190,41 @@ def test_prefix_match_edge_lengths():
         p.check_counters()
     finally:
         p.close()
+
+
+def test_reserved_hashes():
+    """The reserved hash values 0 and 2^64-1 (empty and deleted index slots)
+    never match, even where evictions left deleted slots behind, and Add()
+    refuses a block that carries one (its parent gains no child)."""
+    p, pool, cfg = tiny_pair(n_blocks=4096)
+    try:
+        now = pool["now"]
+        _, _, dec = p.select(now, 64, commit=True)        # leaves deleted slots in the index
+        ch = pool["chains"]
+        tomb, empty = np.uint64(2 ** 64 - 1), np.uint64(0)
+        R = np.zeros((4, 32), np.uint64)
+        L = np.array([32, 32, 32, 1], np.int32)
+        R[0] = ch[0]
+        R[0, 0] = tomb
+        R[1] = ch[1]
+        R[1, 5] = tomb
+        R[2] = ch[2]
+        R[2, 3] = empty
+        R[3, 0] = empty
+        m = p.prefix_match(R, L, now + 1, api.PM_STATS | api.PM_TOUCH)
+        assert m[0] == 0 and m[3] == 0 and m[1] <= 5 and m[2] <= 3
+        ids = dec[:3]
+        live = np.nonzero(p.oc.valid)[0]
+        par = np.array([-1, live[0], live[1]], np.int32)   # cached parents
+        hashes = np.array([tomb, empty, np.uint64(0x1234567)], np.uint64)
+        counts = np.zeros((3, 5), np.uint8)
+        counts[:, 1] = 16
+        p.insert(ids, hashes, par, np.full(3, now + 2, np.int32), np.array([0, 1, 2]), counts,
+                 np.full(3, 16, np.int32), np.zeros(3, np.int32), np.zeros(3, np.int32))
+        assert "BAD_HASH" in p.status()
+        p.check_pool()
+        p.check_counters()
+        assert not p.oc.valid[ids[0]] and not p.oc.valid[ids[1]] and p.oc.valid[ids[2]]
+        p.select(now + 3, 64, commit=True)
+    finally:
+        p.close()

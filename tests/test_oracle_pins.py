@@ -479,3 +479,19 @@ def test_learner_trigger_every_K_evictions():
     c.score_select(1000, 2, commit=True)                          # 5 crosses 4
     assert c.pending and c.feedback() and not c.pending
     assert not c.feedback()
+
+
+def test_reserved_hashes_never_match_and_are_refused():
+    """0 and 2^64-1 mark empty and deleted index slots at the boundary: the
+    oracle never indexes them, so a request hash with one ends the match, and
+    Add() refuses a block carrying one (its parent gains no child)."""
+    import oracle
+    prm = oracle.Params(1, K=4)
+    oc = oracle.OracleCache(8, [oracle.RECENCY], prm)
+    tomb = 2 ** 64 - 1
+    oc.insert(np.array([0, 1, 2]), np.array([11, tomb, 13], np.uint64), np.array([-1, 0, 0]), np.zeros(3, np.int32),
+              np.zeros(3, np.int32), np.zeros(3, np.int32), np.full(3, 16), np.zeros(3), np.zeros(3))
+    assert oc.valid.tolist()[:3] == [True, False, True]
+    assert oc.child_count[0] == 1
+    m, _ = oc.prefix_match(np.array([[11, 13, 0], [11, tomb, 13]], np.uint64), [3, 3], 5)
+    assert m.tolist() == [2, 1]
