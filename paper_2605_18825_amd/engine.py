@@ -4,6 +4,11 @@ One context holds n_inst independent caches.  Each method marshals one
 batched C-ABI call (all instances at once) and copies back what the caller's
 block manager needs on the host: match lengths and matched block ids, and
 eviction decisions.  No policy step runs here.
+
+Host arrays go to the device through pinned staging buffers with
+asynchronous copies, and results come back the same way with one stream
+synchronisation per call that returns them, so a replay step costs few
+host-device round trips.
 """
 import numpy as np
 import torch
@@ -12,8 +17,52 @@ from . import api
 from .pool import DevicePool, SelectBuffers
 
 
-def _dev(a, dtype):
-    return torch.as_tensor(np.ascontiguousarray(a)).to(device="cuda", dtype=dtype)
+class _Staging:
+    """Pinned host buffers and device buffers, reused call after call.
+
+    put(name, array) copies a host array into the pinned buffer `name` and
+    from there, asynchronously on the current stream, into the device buffer
+    `name`; it returns the device view.  Before a pinned buffer is written
+    again, the copy that last read it must have finished (its event); the
+    device buffer needs no such wait, since everything runs on one stream."""
+
+    def __init__(self):
+        self.host = {}
+        self.dev = {}
+        self.ev = {}
+
+    def _bufs(self, name, nbytes):
+        h = self.host.get(name)
+        if h is None or h.numel() < nbytes:
+            n = max(nbytes, 2 * (h.numel() if h is not None else 0), 4096)
+            if name in self.ev:
+                self.ev[name].synchronize()
+            self.host[name] = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+            self.dev[name] = torch.empty(n, dtype=torch.uint8, device="cuda")
+            self.ev[name] = torch.cuda.Event()
+            self.ev[name].record()
+        return self.host[name], self.dev[name]
+
+    def put(self, name, a, dtype):
+        a = np.ascontiguousarray(a)
+        nb = a.nbytes
+        h, d = self._bufs(name, max(nb, 1))
+        self.ev[name].synchronize()
+        h.numpy()[:nb] = a.view(np.uint8).ravel()
+        d[:nb].copy_(h[:nb], non_blocking=True)
+        self.ev[name].record()
+        return d[:nb].view(dtype).view(a.shape) if nb else d[:0].view(dtype)
+
+    def get(self, name, t):
+        """Start copying device tensor t into the pinned buffer `name`; the
+        numpy view is valid after the stream has been synchronised."""
+        t = t.contiguous()
+        nb = t.numel() * t.element_size()
+        h, _ = self._bufs("out_" + name, max(nb, 1))
+        self.ev["out_" + name].synchronize()
+        h[:nb].copy_(t.view(-1).view(torch.uint8), non_blocking=True)
+        self.ev["out_" + name].record()
+        return h[:nb].numpy()
 
 
 class DeviceBackend:
@@ -32,10 +81,12 @@ class DeviceBackend:
         api.sae_set_params(self.ctx, -1, api.make_params(self.Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma,
                                                          eta=eta, temperature=T, beta=beta, K=K, learn=learn))
         self.out = SelectBuffers(n_inst, self.Q, max_k)
-        self.select_ms = 0.0
+        self.st = _Staging()
+        self.stream = torch.cuda.current_stream()
         self.select_calls = 0
 
     def close(self):
+        self.stream.synchronize()
         api.sae_destroy(self.ctx)
 
     # ---------------------------------------------------------------- calls
@@ -47,41 +98,64 @@ class DeviceBackend:
         for j, p in enumerate(prompts):
             h[j, :len(p)] = p
             lens[j] = len(p)
-        ml = torch.zeros(n, dtype=torch.int32, device="cuda")
+        hd = self.st.put("pm_h", h.view(np.int64), torch.int64)
+        ld = self.st.put("pm_len", lens, torch.int32)
+        idv = self.st.put("pm_inst", np.asarray(insts, np.int32), torch.int32)
+        ml = torch.empty(n, dtype=torch.int32, device="cuda")
         mid = torch.empty((n, L), dtype=torch.int32, device="cuda")
         flags = api.PM_TOUCH | api.PM_STATS | (api.PM_INTERVALS if self.intervals else 0)
-        api.sae_prefix_match(self.ctx, _dev(h.view(np.int64), torch.int64), _dev(lens, torch.int32), now,
-                             flags, ml, matched_ids=mid, inst=_dev(insts, torch.int32))
-        ml = ml.cpu().numpy()
-        mid = mid.cpu().numpy()
-        return ml, [mid[j, :ml[j]] for j in range(n)]
+        api.sae_prefix_match(self.ctx, hd, ld, now, flags, ml, matched_ids=mid, inst=idv)
+        mlh = self.st.get("pm_ml", ml)
+        midh = self.st.get("pm_mid", mid)
+        self.stream.synchronize()
+        mlv = mlh.view(np.int32)[:n].copy()
+        midv = midh.view(np.int32)[:n * L].reshape(n, L)
+        return mlv, [midv[j, :mlv[j]].copy() for j in range(n)]
 
     def ref(self, inst, ids, delta):
         if len(ids):
-            api.sae_ref_blocks(self.ctx, _dev(ids, torch.int32), delta, inst=_dev(inst, torch.int32))
+            both = np.stack([np.asarray(inst, np.int32), np.asarray(ids, np.int32)])
+            d = self.st.put("ref%d" % (delta > 0), both, torch.int32)
+            api.sae_ref_blocks(self.ctx, d[1], delta, inst=d[0])
 
     def evict(self, now, k):
-        kd = _dev(k, torch.int32)
+        kd = self.st.put("k", np.asarray(k, np.int32), torch.int32)
         self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd)
-        cnt = self.out.decision_count.cpu().numpy()
-        dec = self.out.decision.cpu().numpy()
+        cnt = self.st.get("cnt", self.out.decision_count)
+        self.stream.synchronize()
+        cnt = cnt.view(np.int32)[:self.n_inst].copy()
+        m = int(cnt.max()) if len(cnt) else 0
         self.select_calls += 1
+        if m == 0:
+            return [np.zeros(0, np.int32) for _ in range(self.n_inst)]
+        dec = self.st.get("dec", self.out.decision[:, :m])
+        self.stream.synchronize()
+        dec = dec.view(np.int32)[:self.n_inst * m].reshape(self.n_inst, m)
         return [dec[i, :cnt[i]].copy() for i in range(self.n_inst)]
 
     def insert(self, now, f):
         n = len(f["ids"])
-        types = f["types"]
-        counts = np.zeros((n, 5), np.uint8)
-        counts[np.arange(n), types] = 16
+        types = np.asarray(f["types"])
+        # int32 columns: instance, id, parent, last_access, off (o_b | o_max << 16 as 32-bit pattern)
+        off = (np.asarray(f["omax"], np.int64) << 16) | (np.asarray(f["ob"], np.int64) & 0xFFFF)
+        cols = np.stack([np.asarray(f["inst"], np.int32), np.asarray(f["ids"], np.int32),
+                         np.asarray(f["parent"], np.int32), np.full(n, now, np.int32),
+                         off.astype(np.uint32).view(np.int32)])
+        # uint8 columns: token-type counts of one-type blocks (16 tokens of the block's type), hints
+        u8 = np.zeros((n, 6), np.uint8)
+        u8[np.arange(n), types] = 16
+        u8[:, 5] = f["hints"]
+        ci = self.st.put("ins_i32", cols, torch.int32)
+        cb = self.st.put("ins_u8", u8, torch.uint8)
+        hd = self.st.put("ins_h", np.asarray(f["hash"], np.uint64).view(np.int64), torch.int64)
+        counts = cb[:, :5].contiguous()
+        hints = cb[:, 5].contiguous()
         tau = torch.empty(n, dtype=torch.uint8, device="cuda")
-        api.sae_block_type(_dev(counts, torch.uint8), tau)
-        zeros = torch.zeros(n, dtype=torch.int32, device="cuda")
-        meta = api.meta_to_u16(api.pack_meta(zeros, tau.to(torch.int32), zeros + 16))
-        api.sae_classify_blocks(self.ctx, _dev(f["hints"], torch.uint8), meta, self.roles)
-        off = api.off_to_u32(api.pack_off(_dev(f["ob"], torch.int64), _dev(f["omax"], torch.int64)))
-        api.sae_insert_blocks(self.ctx, _dev(f["ids"], torch.int32), _dev(f["hash"].view(np.int64), torch.int64),
-                              _dev(f["parent"], torch.int32), _dev(np.full(n, now, np.int32), torch.int32), meta,
-                              off, inst=_dev(f["inst"], torch.int32))
+        api.sae_block_type(counts, tau)
+        # meta before Classify: type, num_tokens - 1 = 15 (the queue bits are Classify's)
+        meta = ((tau.to(torch.int32) << 3) | (15 << 9)).to(torch.int16)
+        api.sae_classify_blocks(self.ctx, hints, meta, self.roles)
+        api.sae_insert_blocks(self.ctx, ci[1], hd, ci[2], ci[3], meta, ci[4], inst=ci[0])
 
     def feedback(self):
         api.sae_feedback_update(self.ctx, 0)

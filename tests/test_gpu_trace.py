@@ -1,12 +1,15 @@
-"""GPU parity on trace replay.
+"""GPU parity on trace replay, with the oracle replaying beside the GPU.
 
-* Balanced mix (Table 2), one cache of 2,250 blocks (36K tokens), online
-  learning on: every step's match length and every eviction decision equal the
-  oracle's; counters, learned weights and the pool state agree.
-* Batched sweep: 256 caches of 65,536 blocks in one context (half
-  single-turn-dominated, half multi-turn-dominated traces), decisions of at
-  least 256 victims; two sampled instances (one of each half) are replayed by
-  the oracle beside the GPU and compared the same way."""
+* Balanced mix (Table 2), one cache of 2,250 blocks (36K tokens): every step's
+  match length and every eviction decision equal the oracle's; counters,
+  learned weights and the whole pool state (valid, leaf and reference bits,
+  child counts, access times) agree.  Learner sets and decision modes that
+  the full-length runs (tests/test_gpu_trace_full.py) do not cover: fixed
+  weights, the appendix text's rules, cascading decisions.
+* Batched sweep: 256 caches of 65,536 blocks in one context, decisions of at
+  least 256 victims, two instances (one of each half) replayed by the oracle:
+  every learner with interval recording across 256 instances, and cascading
+  decisions."""
 import pytest
 
 pytestmark = pytest.mark.gpu
@@ -23,14 +26,6 @@ def test_trace_balanced_first_1500_requests():
 def test_trace_balanced_fixed_weights():
     rd, ro, _ = run_pair("trace_balanced", 400, [0], learn=0, check_every=200)
     assert rd.summary()["evicted"] > 0
-
-
-def test_trace_balanced_all_learners():
-    """Algorithms 2, 3 and 4 and the decay-power learner together: every
-    step's matches and decisions, and mu / sigma / gamma, agree bit for bit."""
-    rd, ro, _ = run_pair("trace_balanced", 1200, [0], learn=15, check_every=200)
-    o = ro.be.c[0]
-    assert o.n_updates > 0 and len(o.ivl[2]) + len(o.ivl[3]) > 0
 
 
 def test_trace_balanced_text_rules():
@@ -57,9 +52,3 @@ def test_batched_sweep_all_learners():
     rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], learn=15, check_every=300)
     assert rd.summary()["evicted"] > 0
     assert all(len(ro.be.c[i].ivl[2]) + len(ro.be.c[i].ivl[3]) > 0 for i in (5, 200))
-
-
-def test_batched_sweep_sampled_instances():
-    rd, ro, _ = run_pair("batched_sweep", 900, [5, 200], check_every=150)
-    s = rd.summary()
-    assert s["evicted"] > 0 and s["decisions"] > 0

@@ -12,23 +12,9 @@ from harness import say
 from oracle_backend import OracleBackend
 from paper_2605_18825_amd import api
 from paper_2605_18825_amd.engine import DeviceBackend
-from synth.pools import MU_AGENT_MS, MU_CHAT_MS, SIGMA_AGENT, SIGMA_CHAT
 from synth.replay import Replay
-from synth.trace import TRACE_CONFIGS, TraceGen
-
-# the paper's four queues (Sec. 3.1): evict-first, structural, chat, agent
-KINDS = [api.KIND_EVICT_FIRST, api.KIND_STRUCTURAL, api.KIND_LOGNORMAL, api.KIND_LOGNORMAL]
-ROLES = [0, 1, 2, 3]
-MU = [0.0, 0.0, MU_CHAT_MS, MU_AGENT_MS]
-SIGMA = [1.0, 1.0, SIGMA_CHAT, SIGMA_AGENT]
-
-
-def trace_gens(name, n_inst, **over):
-    cfg = TRACE_CONFIGS[name]
-    if "mixes" in cfg:
-        half = n_inst // 2
-        return [TraceGen(cfg["mixes"][0 if i < half else 1], cfg["seed"] * 1000 + i, **over) for i in range(n_inst)]
-    return [TraceGen(cfg["mix"], cfg["seed"] * 1000 + i, **over) for i in range(n_inst)]
+from synth.trace import TRACE_CONFIGS
+from trace_setup import KINDS, MU, ROLES, SIGMA, trace_gens  # noqa: F401
 
 
 def check_pool(dev, orc, i):
