@@ -402,9 +402,10 @@ sae_status sae_poll_status(sae_ctx *ctx, sae_stream_t stream, uint32_t *bits);
 /* Diagnostics of the last pool-scan selection of one instance: for each
  * queue q, out[4q..4q+3] = {evictable blocks (0xFFFFFFFF when the selection
  * did not need the count: the bound admitted only part of the queue and the
- * exact slow path did not run), candidates under the bound, candidates beyond
- * a scan workgroup's region, 1 if the exact slow path ran}.  out is host
- * memory of 4 * n_queues words; synchronizes `stream`. */
+ * exact slow path did not run), candidates under the bound that were kept,
+ * candidates beyond the capacity of the candidate stripes (they send the
+ * selection to the exact slow path), 1 if the exact slow path ran}.  out is
+ * host memory of 4 * n_queues words; synchronizes `stream`. */
 sae_status sae_select_stats(sae_ctx *ctx, int32_t inst, uint32_t *out, sae_stream_t stream);
 
 /*

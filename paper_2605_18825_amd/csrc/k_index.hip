@@ -123,47 +123,6 @@ __device__ __forceinline__ bool ghost_insert(GhostSlot *tab, uint32_t mask, unsi
     return false;
 }
 
-// index_erase and ghost_insert continued from the home slot s0 whose hash v0
-// the caller has already loaded (so that several first probes can be in
-// flight together); the same probe sequences as above.
-__device__ __forceinline__ void index_erase_from(IndexSlot *tab, uint32_t mask, unsigned long long h, uint32_t s0,
-                                                 unsigned long long v0)
-{
-    uint32_t s = s0;
-    unsigned long long v = v0;
-    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        if (p > 0) v = tab[s].hash;
-        if (v == h) {
-            tab[s].hash = SAE_TOMB_HASH;
-            return;
-        }
-        if (v == SAE_EMPTY_HASH) return;
-        s = (s + 1) & mask;
-    }
-}
-
-__device__ __forceinline__ bool ghost_insert_from(GhostSlot *tab, uint32_t mask, unsigned long long h,
-                                                  uint32_t ring_pos, uint32_t s0, unsigned long long v0)
-{
-    uint32_t s = s0;
-    unsigned long long v = v0;
-    bool fresh = true;  // v holds slot s's hash as loaded
-    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        if (!fresh) v = tab[s].hash;
-        fresh = false;
-        if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
-            unsigned long long old = atomicCAS(&tab[s].hash, v, h);
-            if (old == v) {
-                tab[s].ring = ring_pos;
-                return true;
-            }
-            continue;
-        }
-        s = (s + 1) & mask;
-    }
-    return false;
-}
-
 // ---------------------------------------------------------------------------
 // tau(b): type holding the lower-median token when tokens are ranked by type.
 __global__ void k_block_type(const uint8_t *counts, long long n, uint8_t *tau)
@@ -699,39 +658,7 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(DevCtx c, const int32
         set_status(c.status, SAE_ST_BAD_BLOCK);
         v = -1;
     }
-    if (v >= 0) {
-        const long long g = (long long)inst * c.N + v;
-        // one round trip for the block's fields, then one for the parent's
-        // count and the first probes of both tables together
-        const uint32_t m = c.meta[g];
-        const unsigned long long h = c.hash[g];
-        const int32_t p = c.parent[g];
-        const uint32_t off = c.off[g];
-        IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-        GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-        const uint32_t si = hash_home(h, c.index_mask), sg = hash_home(h, c.ghost_mask);
-        const unsigned long long vi = tab[si].hash, vg = gt[sg].hash;
-        const bool has_p = p >= 0 && p < c.N;
-        const long long gp = (long long)inst * c.N + (has_p ? p : 0);
-        const int before = has_p ? atomicSub(&c.child_count[gp], 1) : 0;
-        atomicAdd(&sums[SAE_CF_EVICTED + meta_type(m) % SAE_N_TYPES], 1);
-        atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
-        atomicSub(&sums[SAE_CF_RES + meta_queue(m)], 1);
-        meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
-        const bool hashed = !SAE_HASH_RESERVED(h);  // a reserved hash was never indexed
-        if (hashed) index_erase_from(tab, c.index_mask, h, si, vi);
-        if (has_p && before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
-        GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
-        const uint32_t rp = (uint32_t)((s.ev_before + j) % c.ring_cap);
-        GhostEntry e;
-        e.hash = hashed ? h : SAE_EMPTY_HASH;  // an empty entry is never found
-        e.stamp = s.ev_before + d;
-        e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
-               (pos_bin(off) << SAE_TQ_BIN_SHIFT);
-        e.pad_ = 0;
-        ring[rp] = e;
-        if (hashed && !ghost_insert_from(gt, c.ghost_mask, h, rp, sg, vg)) set_status(c.status, SAE_ST_GHOST_FULL);
-    }
+    if (v >= 0) commit_victim(c, inst, j, v, s.ev_before, d, sums);
     __syncthreads();
     if (threadIdx.x < SAE_CF_N && sums[threadIdx.x])
         atomicAdd(counter_slot(c, inst, blockIdx.x) + threadIdx.x, sums[threadIdx.x]);

@@ -185,8 +185,9 @@ __device__ void sel_step(SelState &st, int nq, int shift, int width, bool last)
 }
 
 // Bitonic sort, ascending, of nseg independent segments of length P (a power
-// of two) stored back to back in LDS.  Index arithmetic by shifts and masks.
-__device__ void bitonic_sort_segments(unsigned long long *a, int nseg, int P)
+// of two) that start `stride` elements apart in LDS.  Index arithmetic by
+// shifts and masks.
+__device__ void bitonic_sort_segments(unsigned long long *a, int nseg, int P, int stride)
 {
     if (P < 2) return;
     const int lp = 31 - __clz(P);
@@ -199,7 +200,7 @@ __device__ void bitonic_sort_segments(unsigned long long *a, int nseg, int P)
                 const int u = t & ((1 << lh) - 1);
                 const int lo = ((u >> lj) << (lj + 1)) | (u & ((1 << lj) - 1));
                 const int hi = lo + (1 << lj);
-                unsigned long long *sg = a + ((long long)sgi << lp);
+                unsigned long long *sg = a + (long long)sgi * stride;
                 const unsigned long long x = sg[lo], y = sg[hi];
                 const bool up = ((lo >> lk) & 1) == 0;
                 if ((x > y) == up) {
@@ -703,16 +704,6 @@ __device__ __forceinline__ int last_le(const uint32_t *a, int n, uint32_t x)
     return l;
 }
 
-// Number of elements of the ascending a[0..n) below x (n <= 256, result <= 255).
-__device__ __forceinline__ int count_lt256(const unsigned long long *a, int n, unsigned long long x)
-{
-    int l = 0;
-#pragma unroll
-    for (int st = 128; st > 0; st >>= 1)
-        if (l + st <= n && a[l + st - 1] < x) l += st;
-    return l;
-}
-
 // Ascending sort of n distinct elements src[0..n) (LDS) into dst[0..n) (LDS):
 // each element's position is the number of smaller elements, counted with
 // reads that every lane of a wave makes at the same address.  All threads call.
@@ -824,7 +815,7 @@ __device__ uint32_t lognormal_dt_floor(const ScoreTab &t, int q, int ty, uint32_
 // a single bucket for all of them.  Bucket upper ends are the sampled elements
 // at or below the bound -- all of them up to SAE_NBUCKET - 1, else an evenly
 // spread subset -- and the last one is the bound.  Also writes the scan's
-// filter entries and resets its spill list.
+// filter entries and empties the queue's candidate stripes.
 #define ALL_EST 2048.0
 static_assert(SAMPLE_WGS <= SAE_WAVE, "the chunks' counts fit one wave");
 static_assert(SAMPLE_WGS * SAMPLE_CHUNK <= LCAP, "a queue's sampled elements fit the LDS staging area");
@@ -864,8 +855,9 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
         }
         if (tid == SAMPLE_WGS - 1) cpre[SAMPLE_WGS] = inc;
     }
+    // this call's candidate stripes start empty
+    if (tid <= SAE_STRIPES) c.stripe_n[iq * (SAE_STRIPES + 1) + tid] = 0;
     if (tid == SEL_THREADS - 1) {
-        c.spill_n[iq] = 0;  // this call's spill list starts empty
         nsp_s = 0;
         nb_s = 0;
         bound_s = 0;
@@ -1004,13 +996,16 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
 // The blocks that remain (about the bound's candidates) are queued per wave in
 // LDS with their features; a wave scores its queue exactly once 64 are queued,
 // and at the end the four waves score what is left together.  Blocks with
-// (key, id) <= bound go to the workgroup's own candidate region (one LDS
-// atomic per wave and queue); only a region overflow uses the shared spill
-// list.  Batches of a pool whose size is not a multiple of 4, and the last
-// partial batch, take a path with per-element loads.
+// (key, id) <= bound are buffered in LDS per queue (one LDS atomic per wave
+// and queue); at the end each queue's buffer is appended to one of the
+// queue's candidate stripes with a single device atomic, and what does not fit
+// that stripe, or the buffer, goes to the queue's overflow list.  Batches of a pool whose
+// size is not a multiple of 4, and the last partial batch, take a path with
+// per-element loads.
 #define SCAN_BATCH 256  // blocks per wave per batch: 4 per lane
 #define SCAN_WAVES (SCAN_THREADS / SAE_WAVE)
 #define SCAN_LIST (SAE_WAVE + SCAN_BATCH)  // queued blocks per wave
+#define SCAN_CB 128  // candidates a workgroup buffers per queue before appending to a stripe
 
 // Structural (pn / pd = 1 - o_b / o_max) and recency (pn = pd = 1) blocks:
 // true only if fl(pn awl) > fl(fl(T dt) pd), which implies P > T.  Proof
@@ -1076,6 +1071,9 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
     __shared__ uint32_t st_s;
     __shared__ uint32_t left_s[SCAN_WAVES + 1];
     __shared__ int4 s_lst[SCAN_WAVES][SCAN_LIST];  // queued blocks: last_access, off, meta, id
+    __shared__ unsigned long long cbuf[SAE_MAX_QUEUES][SCAN_CB];  // this workgroup's candidates per queue
+    __shared__ uint32_t res_base[SAE_MAX_QUEUES], res_n[SAE_MAX_QUEUES], ovf_base[SAE_MAX_QUEUES],
+        ovf_n[SAE_MAX_QUEUES];
     const int inst = blockIdx.y;
     const int wg = blockIdx.x;
     const int Q = c.Q;
@@ -1111,13 +1109,13 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
 
     const int now = a.now;
     uint32_t st = 0;
-    const long long rbase = ((long long)inst * c.scan_gx + wg) * Q;
-    unsigned long long *reg = c.creg + rbase * SAE_CAND_REGION;
-    unsigned long long *spill = c.spill + (long long)inst * Q * c.cand_cap;
-    uint32_t *spill_n = c.spill_n + (long long)inst * Q;
+    unsigned long long *cand = c.cand + (long long)inst * Q * 2 * SAE_LCAP;
+    uint32_t *stripe_n = c.stripe_n + (long long)inst * Q * (SAE_STRIPES + 1);
     int4 *lst = s_lst[wave];
 
-    // append (key, id) of an evictable block if it is within its queue's bound
+    // append (key, id) of an evictable block if it is within its queue's bound:
+    // to the workgroup's LDS buffer of the queue, or once that is full, straight
+    // to the queue's overflow list (one device atomic per wave and queue)
     auto emit = [&](bool act, int q, uint32_t key, uint32_t b) {
         const unsigned long long comp = ((unsigned long long)key << 32) | b;
         const bool e = act && (comp <= thr_s[q]);
@@ -1131,17 +1129,16 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
             bp = __shfl(bp, l0, SAE_WAVE);
             const uint32_t pos = bp + (uint32_t)__popcll(mq & lanemask_lt());
             const bool in_e = e && q == qq;
-            if (in_e && pos < SAE_CAND_REGION) reg[(long long)qq * SAE_CAND_REGION + pos] = comp;
-            // beyond the region: one atomic per wave on the queue's spill list
-            const unsigned long long ms = __ballot(in_e && pos >= SAE_CAND_REGION);
+            if (in_e && pos < SCAN_CB) cbuf[qq][pos] = comp;
+            const unsigned long long ms = __ballot(in_e && pos >= SCAN_CB);
             if (ms) {
                 const int ls = __ffsll((long long)ms) - 1;
                 uint32_t sb = 0;
-                if (lane == ls) sb = atomicAdd(&spill_n[qq], (uint32_t)__popcll(ms));
+                if (lane == ls) sb = atomicAdd(&stripe_n[qq * (SAE_STRIPES + 1) + SAE_STRIPES], (uint32_t)__popcll(ms));
                 sb = __shfl(sb, ls, SAE_WAVE);
-                if (in_e && pos >= SAE_CAND_REGION) {
+                if (in_e && pos >= SCAN_CB) {
                     const uint32_t sp = sb + (uint32_t)__popcll(ms & lanemask_lt());
-                    if (sp < (uint32_t)c.cand_cap) spill[(long long)qq * c.cand_cap + sp] = comp;
+                    if (sp < SAE_LCAP) cand[(long long)qq * 2 * SAE_LCAP + SAE_LCAP + sp] = comp;
                 }
             }
             em &= ~mq;
@@ -1232,378 +1229,385 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
     }
     if (st) atomicOr(&st_s, st);
     lds_barrier();
-    if (tid < Q) c.creg_n[rbase + tid] = min(cnt_s[tid], (uint32_t)SAE_CAND_REGION);
+    // the buffered candidates go to stripe wg mod SAE_STRIPES of their queue
+    // (one reservation per queue), the part that does not fit it to the
+    // queue's overflow list (a second reservation, rarely); then every thread
+    // stores
+    const uint32_t stripe = (uint32_t)wg % SAE_STRIPES;
+    if (tid < Q) {
+        const uint32_t n = min(cnt_s[tid], (uint32_t)SCAN_CB);
+        const uint32_t b = n ? atomicAdd(&stripe_n[tid * (SAE_STRIPES + 1) + stripe], n) : 0u;
+        const uint32_t fit = b >= SAE_STRIPE_CAP ? 0u : min(n, (uint32_t)SAE_STRIPE_CAP - b);
+        res_n[tid] = n;
+        res_base[tid] = b;
+        ovf_n[tid] = fit;  // buffered candidates that fit the stripe
+        ovf_base[tid] = (n > fit) ? atomicAdd(&stripe_n[tid * (SAE_STRIPES + 1) + SAE_STRIPES], n - fit) : 0u;
+    }
     if (tid == 0) set_status(c.status, st_s);
-}
-
-// Sum over a wave of n words p[0], p[stride], ... (n <= 32 * SAE_WAVE): every
-// load is issued before the first is used.
-__device__ uint32_t wave_sum_strided(const uint32_t *p, int n, long long stride)
-{
-    uint32_t t[32];
-#pragma unroll
-    for (int u = 0; u < 32; ++u) {
-        const int w = u * SAE_WAVE + lane_id();
-        t[u] = (w < n) ? p[(long long)w * stride] : 0u;
-    }
-    uint32_t s = 0;
-#pragma unroll
-    for (int u = 0; u < 32; ++u) s += t[u];
-    for (int d = 32; d > 0; d >>= 1) s += __shfl_xor(s, d, SAE_WAVE);
-    return s;
-}
-
-// Pool-scan engine, step 4: per (instance, queue) and slice, where the
-// candidates in scan order (the workgroups' regions, then the spill list) are
-// cut into SAE_GATHER_S equal slices: stage the slice in LDS, find each
-// candidate's bucket (the first upper end >= it) and write the slice grouped by
-// bucket (counting sort) to its place in cand: slice s starts at g_base[s],
-// its bucket b at g_rel[s][b] with g_cnt[s][b] elements.  Also sums the
-// evictable blocks of a 1 / SAE_GATHER_S share of the scan workgroups.
-#define GATHER_THREADS 256
-#define GATHER_RPT (2048 / GATHER_THREADS)  // scan workgroups per thread (scan_gx <= 2048)
-__global__ void __launch_bounds__(GATHER_THREADS) k_gather(DevCtx c, SelectArgs a)
-{
-    extern __shared__ unsigned long long el[];  // [SAE_LCAP / SAE_GATHER_S + 1]
-    __shared__ unsigned long long spl[SAE_NBUCKET];
-    __shared__ uint32_t offs[2048 + 1];
-    __shared__ uint32_t hist[SAE_NBUCKET], boff[SAE_NBUCKET], wsum[GATHER_THREADS / SAE_WAVE];
-    const int s = blockIdx.x;
-    const int q = blockIdx.y;
-    const int inst = blockIdx.z;
-    const int Q = c.Q;
-    const int gx = c.scan_gx;
-    const int tid = threadIdx.x;
-    const int lane = lane_id();
-    const long long iq = (long long)inst * Q + q;
-    const long long iqs = iq * SAE_GATHER_S + s;
-    // one round of loads: every workgroup's candidate count, the bucket upper ends
-    const int NB = c.nsplit[iq];
-    const uint32_t ns = c.spill_n[iq];
-    uint32_t cv[GATHER_RPT];
-#pragma unroll
-    for (int u = 0; u < GATHER_RPT; ++u) {
-        const int w = tid * GATHER_RPT + u;
-        cv[u] = (w < gx) ? c.creg_n[((long long)inst * gx + w) * Q + q] : 0u;
-    }
-    const unsigned long long sv = c.split[iq * SAE_NBUCKET + tid];
-    hist[tid] = 0;
-    spl[tid] = (tid < NB) ? sv : ~0ull;
-    uint32_t loc = 0;
-#pragma unroll
-    for (int u = 0; u < GATHER_RPT; ++u) loc += cv[u];
-    const uint32_t inc = wave_incl_scan(loc);
-    if (lane == 63) wsum[tid >> 6] = inc;
     lds_barrier();
-    {
-        uint32_t o = inc - loc;
-        for (int w = 0; w < (tid >> 6); ++w) o += wsum[w];
-#pragma unroll
-        for (int u = 0; u < GATHER_RPT; ++u) {
-            const int w = tid * GATHER_RPT + u;
-            if (w < gx) offs[w] = o;
-            o += cv[u];
+    for (int i = tid; i < Q * SCAN_CB; i += SCAN_THREADS) {
+        const int q = i / SCAN_CB;
+        const uint32_t j = (uint32_t)(i - q * SCAN_CB);
+        if (j >= res_n[q]) continue;
+        unsigned long long *cq = cand + (long long)q * 2 * SAE_LCAP;
+        if (j < ovf_n[q]) {
+            cq[stripe * SAE_STRIPE_CAP + res_base[q] + j] = cbuf[q][j];
+        } else {
+            const uint32_t p = ovf_base[q] + (j - ovf_n[q]);
+            if (p < SAE_LCAP) cq[SAE_LCAP + p] = cbuf[q][j];
         }
-        if (tid == GATHER_THREADS - 1) offs[gx] = o;  // cv is 0 beyond gx
+    }
+}
+
+// Pool-scan engine, step 4: the sorted lists and the Algorithm 1 decision, in
+// one launch of FIN_THREADS-thread workgroups per instance (the commit, a
+// chain of scattered accesses per victim, follows in a kernel that spreads the
+// victims over many compute units):
+//  * every workgroup first reads each queue's stripe counts, bound and bucket
+//    count (one round of loads) and derives the same facts from them: the
+//    candidates C_q, the list size need_q = min(k, evictable), whether the
+//    queue's candidates are complete (C_q >= need_q, no stripe over its
+//    capacity, not forced to the exact path), and the decision's size;
+//  * "group" workgroups, FIN_G buckets of one queue each: stream the queue's
+//    candidates, count those at or below the group's lower end, rank the
+//    ones inside by bucket and write the part within the first need_q
+//    positions (the evict-first queue's list also fills the decision's first
+//    positions, Algorithm 1 stage 1);
+//  * "union" workgroups, FIN_GU buckets each of the reference queue (the
+//    queue other than evict-first with the smallest bound): the decision's
+//    stage 2 is the first k - n1 of all other queues' blocks by (P, id), and
+//    every one of them is a candidate of its queue (each lies among its own
+//    queue's first k), so ranking the union of those candidates up to the
+//    reference bound gives it exactly;
+//  * one finisher workgroup writes the list sizes and the decision size and
+//    updates the eviction count.  If any queue's candidates are incomplete,
+//    every other workgroup stops and the finisher alone computes everything
+//    by the exact path (radix select streaming the pool) and merges.
+#define FIN_THREADS 1024
+#define FIN_G 16                             // buckets per group workgroup
+#define FIN_GPQ (SAE_NBUCKET / FIN_G)        // group workgroups per queue
+#define FIN_GU 4                             // reference-queue buckets per union workgroup
+#define FIN_NU (SAE_NBUCKET / FIN_GU)        // union workgroups
+#define FIN_GCAP 4096                        // candidates a workgroup ranks at once
+#define FIN_U (SAE_LCAP / FIN_THREADS)       // candidates per thread of one streamed queue
+#define FIN_STACK 80                         // pending ranges (a range splits into two)
+#define FIN_SB 64                            // sub-bins per bucket in the ranking
+static_assert(SAE_STRIPES == SAE_WAVE, "one stripe per lane");
+static_assert(FIN_G <= 16 && FIN_GU <= FIN_G, "bucket indices fit the bucket histogram");
+
+struct FinInfo {
+    uint32_t C[SAE_MAX_QUEUES];     // candidates held (stripes, then the overflow list)
+    uint32_t over[SAE_MAX_QUEUES];  // candidates lost beyond the overflow list's capacity
+    uint32_t need[SAE_MAX_QUEUES];  // list size min(k, evictable)
+    int32_t nb[SAE_MAX_QUEUES];
+    int32_t fail[SAE_MAX_QUEUES];
+    unsigned long long thr[SAE_MAX_QUEUES];
+    uint32_t spre[SAE_MAX_QUEUES][SAE_STRIPES + 1];  // position of each stripe's first candidate in queue
+                                                     // order; [SAE_STRIPES]: the overflow list's
+    int32_t any_fail, n1, rest, d;
+};
+
+struct FinRange {
+    unsigned long long lo, hi;  // range (lo, hi], or [0, hi] when !has_lo
+    int32_t has_lo, e0, e1;     // bucket upper ends e0 .. e1 - 1 of the range (e1 - 1 ends at hi), or none
+};
+
+// Per-instance facts from the scan's counts (all threads; ends with a barrier).
+__device__ void fin_info(const DevCtx &c, const SelectArgs &a, int inst, uint32_t kq, FinInfo &f)
+{
+    const int Q = c.Q, tid = threadIdx.x, lane = lane_id(), wave = tid / SAE_WAVE;
+    if (wave < Q) {
+        const long long iq = (long long)inst * Q + wave;
+        const uint32_t *sn = c.stripe_n + iq * (SAE_STRIPES + 1);
+        const uint32_t raw = sn[lane];
+        const uint32_t ovr = sn[SAE_STRIPES];
+        const int32_t nb = c.nsplit[iq];
+        const unsigned long long thr = c.thr[iq];
+        const uint32_t capd = raw < SAE_STRIPE_CAP ? raw : (uint32_t)SAE_STRIPE_CAP;
+        const uint32_t inc = wave_incl_scan(capd);
+        f.spre[wave][lane] = inc - capd;
+        const uint32_t S = __shfl(inc, SAE_WAVE - 1, SAE_WAVE);
+        const uint32_t ovk = ovr < SAE_LCAP ? ovr : (uint32_t)SAE_LCAP;
+        if (lane == 0) {
+            f.spre[wave][SAE_STRIPES] = S;
+            f.C[wave] = S + ovk;
+            f.over[wave] = ovr - ovk;
+            f.nb[wave] = nb;
+            f.thr[wave] = thr;
+        }
     }
     lds_barrier();
-    const uint32_t total_r = offs[gx];
-    const uint32_t nsp = ns < (uint32_t)c.cand_cap ? ns : (uint32_t)c.cand_cap;
-    const uint32_t C = total_r + nsp;
-    const uint32_t lo = (uint32_t)(((unsigned long long)s * C) / SAE_GATHER_S);
-    const uint32_t hi = (uint32_t)(((unsigned long long)(s + 1) * C) / SAE_GATHER_S);
-    const uint32_t n = hi - lo;
     if (tid == 0) {
-        c.g_base[iqs] = lo;
-        c.g_tot[iqs] = (NB <= 0) ? 0u : (C > SAE_LCAP ? (uint32_t)SAE_LCAP + 1u : n);
-    }
-    if (NB <= 0 || C > SAE_LCAP) return;  // uniform: nothing wanted, exact path, or too many candidates
-    // stage the slice: index math first, then every load in flight
-    const unsigned long long *reg = c.creg + (long long)inst * gx * Q * SAE_CAND_REGION;
-    const unsigned long long *spill = c.spill + iq * c.cand_cap;
-    for (uint32_t i0 = 0; i0 < n; i0 += 4 * GATHER_THREADS) {
-        unsigned long long ev[4];
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const uint32_t i = lo + i0 + tid + (uint32_t)m * GATHER_THREADS;
-            const int l = last_le<11>(offs, gx, i);  // the workgroup holding candidate i
-            ev[m] = (i < total_r) ? reg[((long long)l * Q + q) * SAE_CAND_REGION + (i - offs[l])]
-                                  : ((i < hi) ? spill[i - total_r] : ~0ull);
+        int any = 0;
+        uint32_t other = 0, n_ef = 0;
+        for (int q = 0; q < Q; ++q) {
+            const bool all = f.thr[q] == ~0ull;
+            const uint32_t need = (all && f.C[q] < kq) ? f.C[q] : kq;
+            const bool fail = need > 0 && ((a.flags & SAE_SS_FORCE_FALLBACK) || f.nb[q] <= 0 || f.C[q] < need ||
+                                           f.over[q] > 0 || f.C[q] > SAE_LCAP);
+            f.need[q] = need;
+            f.fail[q] = fail ? 1 : 0;
+            any |= fail ? 1 : 0;
+            if (q == c.ef_queue) n_ef = need;
+            else other += need;
         }
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const uint32_t i = i0 + tid + (uint32_t)m * GATHER_THREADS;
-            if (i < n) {
-                el[i] = ev[m];
-                atomicAdd(&hist[count_lt256(spl, NB, ev[m])], 1u);
-            }
-        }
+        f.any_fail = any;
+        f.n1 = (int32_t)n_ef;
+        f.rest = (int32_t)(kq - n_ef);
+        f.d = (int32_t)(n_ef + ((uint32_t)f.rest < other ? (uint32_t)f.rest : other));
     }
     lds_barrier();
-    {
-        const uint32_t v = hist[tid];
-        const uint32_t inc2 = wave_incl_scan(v);
-        if (lane == 63) wsum[tid >> 6] = inc2;
-        lds_barrier();
-        uint32_t pre = 0;
-        for (int w = 0; w < (tid >> 6); ++w) pre += wsum[w];
-        boff[tid] = pre + inc2 - v;
-        c.g_rel[iqs * SAE_NBUCKET + tid] = pre + inc2 - v;
-        c.g_cnt[iqs * SAE_NBUCKET + tid] = v;
-    }
-    lds_barrier();
-    unsigned long long *out = c.cand + iq * SAE_LCAP + lo;
-    for (uint32_t i = tid; i < n; i += GATHER_THREADS) {
-        const unsigned long long e = el[i];
-        out[atomicAdd(&boff[count_lt256(spl, NB, e)], 1u)] = e;
-    }
 }
 
-// Pool-scan engine, step 5: one workgroup per bucket of one (instance, queue).
-// The bucket's elements are its pieces in the slices; its offset in the
-// queue's sorted list is the sum over slices of the elements below it.  It is
-// sorted (rank counting; sort_lds when larger than a workgroup) and the part
-// that falls within the first need = min(k, evictable) positions is written
-// (for the evict-first queue also to the decision, whose first positions it
-// fills: Algorithm 1, stage 1).  Nothing is written when the queue needs the
-// exact path (too few or too many candidates, a full spill list, a bucket too
-// large to sort): the merge kernel then recomputes that queue's whole list.
-#define BUCKET_THREADS 256
-__global__ void __launch_bounds__(BUCKET_THREADS) k_bucket(DevCtx c, SelectArgs a)
+// Where candidate i (< C) of a queue lies: the stripes in order, then the
+// overflow list.  Computed without a branch, so that the loads of all of a
+// thread's candidates can be in flight together (a load inside a divergent
+// branch is waited for at the branch's end).
+__device__ __forceinline__ uint32_t fin_slot(const uint32_t *spre, uint32_t i)
 {
-    extern __shared__ unsigned long long bel[];  // [2 * SAE_BSORT]
-    __shared__ uint32_t base_v[SAE_GATHER_S], rel_v[SAE_GATHER_S], pre_v[SAE_GATHER_S + 1];
-    __shared__ uint32_t C_s, off_s;
-    const int j = blockIdx.x;
-    const int q = blockIdx.y;
-    const int inst = blockIdx.z;
-    const int Q = c.Q;
-    const int tid = threadIdx.x;
-    const long long iq = (long long)inst * Q + q;
-    // one round of loads; the first wave sums the slices
-    const int NB = c.nsplit[iq];
-    const uint32_t ns = c.spill_n[iq];
-    const bool all = c.thr[iq] == ~0ull;
-    if (tid < SAE_WAVE) {
-        const bool in = tid < SAE_GATHER_S;
-        const long long iqs = iq * SAE_GATHER_S + tid;
-        uint32_t tv = in ? c.g_tot[iqs] : 0u;
-        const uint32_t bv = in ? c.g_base[iqs] : 0u;
-        uint32_t rv = in ? c.g_rel[iqs * SAE_NBUCKET + j] : 0u;
-        const uint32_t cv = in ? c.g_cnt[iqs * SAE_NBUCKET + j] : 0u;
-        const uint32_t inc = wave_incl_scan(cv);
-        if (in) {
-            base_v[tid] = bv;
-            rel_v[tid] = rv;
-            pre_v[tid] = inc - cv;
-        }
-        if (tid == SAE_GATHER_S - 1) pre_v[SAE_GATHER_S] = inc;
-        for (int d = 32; d > 0; d >>= 1) {
-            tv += __shfl_xor(tv, d, SAE_WAVE);
-            rv += __shfl_xor(rv, d, SAE_WAVE);
-        }
+    const int s = last_le<6>(spre, SAE_STRIPES, i);
+    const uint32_t in_stripe = (uint32_t)s * SAE_STRIPE_CAP + (i - spre[s]);
+    const uint32_t ov = spre[SAE_STRIPES];
+    return i >= ov ? (uint32_t)SAE_LCAP + (i - ov) : in_stripe;
+}
+
+// Ranks the candidates of the queues in `src` (a bit mask) that lie in
+// (first range's lo, ends[e1 - 1]]: out(r, e) is called for every one of them
+// whose rank r among all those queues' candidates is below `need`.
+// Streaming: wave w reads stripes w, w + 16, w + 32, w + 48 of a queue, every
+// load issued before any is used, and keeps the candidates inside the range
+// in a region of its own (a register count, no atomics).  Ranking, over those
+// only: each candidate's bucket, the buckets' smallest and largest values, a
+// counting sort by sub-bin (FIN_SB equal value ranges between a bucket's
+// smallest and largest value; monotone in the value, so the sub-bins are
+// ordered), and inside its sub-bin (a handful of candidates) each one's rank
+// by comparison.  A range holding more than fits is split in two (by its
+// bucket ends, or by value once it has a single bucket) and the halves are
+// ranked in order.  All threads call; `ends` is in LDS.
+template <typename Out>
+__device__ void fin_rank(const DevCtx &c, int inst, const FinInfo &f, uint32_t src, const unsigned long long *ends,
+                         FinRange first, uint32_t need, unsigned long long *st1, unsigned long long *st2,
+                         Out out)
+{
+    constexpr int NW = FIN_THREADS / SAE_WAVE;
+    constexpr int NSB = 16 * FIN_SB;
+    constexpr int WCAP = FIN_GCAP / NW;  // staging slots per wave
+    constexpr int PER = FIN_GCAP / FIN_THREADS;
+    static_assert(NSB == FIN_THREADS, "one sub-bin per thread in the scan");
+    static_assert(SAE_STRIPES == 4 * NW && SAE_STRIPE_CAP == 4 * SAE_WAVE, "four stripes of four slots per lane");
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid / SAE_WAVE;
+    __shared__ FinRange stack[FIN_STACK];
+    __shared__ int32_t sp_s, stop_s, go_s, full_s;
+    __shared__ uint32_t below_s, wsum[NW], wcnt[NW], wpre[NW + 1];
+    __shared__ uint32_t hist[NSB], soff[NSB + 1];
+    __shared__ unsigned long long bmin[16], bmax[16];
+    __shared__ float sbmul[16];
+    __shared__ FinRange cur;
+    if (tid == 0) {
+        stack[0] = first;
+        sp_s = 1;
+        stop_s = 0;
+    }
+    lds_barrier();
+    while (true) {
         if (tid == 0) {
-            C_s = tv;
-            off_s = rv;
+            cur = stack[--sp_s];
+            below_s = 0;
+            full_s = 0;
         }
-    }
-    lds_barrier();
-    if (j >= NB) return;  // uniform per workgroup
-    const uint32_t C = C_s, off = off_s, n = pre_v[SAE_GATHER_S];
-    if (tid == 0) {
-        c.bsize[iq * SAE_NBUCKET + j] = n;
-        c.bbelow[iq * SAE_NBUCKET + j] = off;
-    }
-    const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
-    // a bound that admits every block makes the candidates the evictable blocks
-    const uint32_t need = (all && C < kq) ? C : kq;
-    if ((a.flags & SAE_SS_FORCE_FALLBACK) || C > SAE_LCAP || ns > (uint32_t)c.cand_cap || C < need) return;
-    if (off >= need || n == 0 || n > SAE_BSORT) return;
-    const unsigned long long *cand = c.cand + iq * SAE_LCAP;
-    const uint32_t m = (need - off) < n ? (need - off) : n;
-    const long long ob = iq * c.max_k + off;
-    int32_t *dec = (q == c.ef_queue) ? a.decision + (long long)inst * c.max_k + off : nullptr;
-    auto elem = [&](uint32_t t) {
-        const int sl = last_le<4>(pre_v, SAE_GATHER_S, t);  // the slice holding element t
-        return cand[base_v[sl] + rel_v[sl] + (t - pre_v[sl])];
-    };
-    if (n <= BUCKET_THREADS) {
-        const unsigned long long e0 = (tid < (int)n) ? elem((uint32_t)tid) : ~0ull;
-        if (tid < (int)n) bel[tid] = e0;
+        hist[tid] = 0;
+        if (tid < 16) {
+            bmin[tid] = ~0ull;
+            bmax[tid] = 0;
+        }
         lds_barrier();
-        if (tid < (int)n) {
-            uint32_t rank = 0, i = 0;
-            for (; i + 8 <= n; i += 8) {
+        const FinRange r = cur;
+        const bool has_ends = r.e1 > r.e0;
+        const int nbk = has_ends ? r.e1 - r.e0 : 1;
+        uint32_t below = 0, wn = 0;  // wn: this wave's staged candidates (wave-uniform)
+        bool full = false;
+        const unsigned long long lt = lanemask_lt();
+        unsigned long long *wst = st1 + wave * WCAP;
+        auto take = [&](unsigned long long e, bool ok) {
+            const bool under = ok && r.has_lo && e <= r.lo;
+            below += under ? 1u : 0u;
+            const bool inr = ok && !under && e <= r.hi;
+            const unsigned long long m = __ballot(inr);
+            const uint32_t p = wn + (uint32_t)__popcll(m & lt);
+            if (inr && p < WCAP) wst[p] = e;
+            wn += (uint32_t)__popcll(m);
+        };
+        for (int q = 0; q < c.Q; ++q) {
+            if (!((src >> q) & 1u)) continue;
+            const uint32_t C = f.C[q];
+            if (C == 0) continue;  // uniform
+            const unsigned long long *cq = c.cand + ((long long)inst * c.Q + q) * 2 * SAE_LCAP;
+            const uint32_t *spre = f.spre[q];
+            unsigned long long ev[16];
+            uint32_t okm = 0;
 #pragma unroll
-                for (int u = 0; u < 8; ++u) rank += (bel[i + u] < e0) ? 1u : 0u;  // LDS broadcast reads
+            for (int r4 = 0; r4 < 4; ++r4) {
+                const int st = wave + NW * r4;
+                const uint32_t cnt = spre[st + 1] - spre[st];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const uint32_t j = (uint32_t)(lane + SAE_WAVE * v);
+                    ev[r4 * 4 + v] = cq[st * SAE_STRIPE_CAP + (j < cnt ? j : 0u)];
+                    okm |= (j < cnt) ? (1u << (r4 * 4 + v)) : 0u;
+                }
             }
-            for (; i < n; ++i) rank += (bel[i] < e0) ? 1u : 0u;
-            if (rank < m) {
-                const int32_t id = (int32_t)(uint32_t)(e0 & 0xFFFFFFFFull);
-                a.victims[ob + rank] = id;
-                if (a.scores) a.scores[ob + rank] = __uint_as_float((uint32_t)(e0 >> 32));
-                c.sel[ob + rank] = e0;
-                if (dec) dec[rank] = id;
+#pragma unroll
+            for (int u = 0; u < 16; ++u) take(ev[u], (okm >> u) & 1u);
+            // the overflow list (usually empty), split over the waves
+            const uint32_t ov = C - spre[SAE_STRIPES];
+            for (uint32_t b0 = 0; b0 < ov; b0 += FIN_THREADS) {
+                const uint32_t i = b0 + (uint32_t)tid;
+                take(cq[SAE_LCAP + (i < ov ? i : ov - 1)], i < ov);
             }
         }
-        return;
-    }
-    // a larger bucket: sample sort inside it -- SEL_PIVOTS pivots from evenly
-    // spaced positions, sub-buckets by counting, rank counting within each
-    __shared__ unsigned long long piv[SEL_PIVOTS];
-    __shared__ uint32_t sh[SEL_PIVOTS + 2], sfill[SEL_PIVOTS + 1];
-    __shared__ uint8_t sk[SAE_BSORT];
-    unsigned long long *bel2 = bel + SAE_BSORT;
-    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) bel[t] = elem(t);
-    if (tid <= SEL_PIVOTS) {
-        sh[tid] = 0;
-        sfill[tid] = 0;
-    }
-    lds_barrier();
-    __shared__ unsigned long long praw[SEL_PIVOTS];
-    if (tid < SAE_WAVE) {
-        const unsigned long long p = bel[(uint32_t)(((unsigned long long)tid * n) / SEL_PIVOTS)];
-        praw[tid] = p;
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        uint32_t rk = 0;
-#pragma unroll
-        for (int i = 0; i < SEL_PIVOTS; ++i) rk += (praw[i] < p) ? 1u : 0u;
-        piv[rk] = p;
-    }
-    lds_barrier();
-    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
-        const unsigned long long e = bel[t];
-        int k = 0;  // pivots below e
-#pragma unroll
-        for (int st = 32; st > 0; st >>= 1)
-            if (piv[k + st - 1] < e) k += st;
-        k += (k == SEL_PIVOTS - 1 && piv[SEL_PIVOTS - 1] < e) ? 1 : 0;
-        sk[t] = (uint8_t)k;
-        atomicAdd(&sh[k], 1u);
-    }
-    lds_barrier();
-    if (tid < SAE_WAVE) {
-        // exclusive offsets of the SEL_PIVOTS + 1 sub-buckets (lane 63 also owns the last one)
-        const uint32_t v = sh[tid] + ((tid == SAE_WAVE - 1) ? sh[SEL_PIVOTS] : 0u);
-        const uint32_t inc = wave_incl_scan(v);
-        const uint32_t ex = inc - v;
-        const uint32_t h0 = sh[tid];
-        __builtin_amdgcn_wave_barrier();
-        sh[tid] = ex;
-        if (tid == SAE_WAVE - 1) {
-            sh[SEL_PIVOTS] = ex + h0;
-            sh[SEL_PIVOTS + 1] = inc;
+        full = wn > WCAP;
+        for (int o = 32; o > 0; o >>= 1) below += __shfl_xor(below, o, SAE_WAVE);
+        if (lane == 0) {
+            if (below) atomicAdd(&below_s, below);
+            wcnt[wave] = wn < WCAP ? wn : WCAP;
+            if (full) full_s = 1;
         }
-    }
-    lds_barrier();
-    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
-        const int k = sk[t];
-        bel2[sh[k] + atomicAdd(&sfill[k], 1u)] = bel[t];
-    }
-    lds_barrier();
-    for (uint32_t t = tid; t < n; t += BUCKET_THREADS) {
-        // position t of the sub-bucket order: rank within its sub-bucket
-        const unsigned long long e = bel2[t];
-        int k = 0;
-#pragma unroll
-        for (int st = 32; st > 0; st >>= 1)
-            if (sh[k + st] <= t) k += st;
-        k += (k == SEL_PIVOTS - 1 && sh[SEL_PIVOTS] <= t) ? 1 : 0;
-        const uint32_t lo = sh[k], hi = sh[k + 1];
-        uint32_t rk = lo, i = lo;
-        for (; i + 8 <= hi; i += 8) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) rk += (bel2[i + u] < e) ? 1u : 0u;
+        lds_barrier();
+        if (tid == 0) {
+            uint32_t o = 0;
+            for (int w = 0; w < NW; ++w) {
+                wpre[w] = o;
+                o += wcnt[w];
+            }
+            wpre[NW] = o;
         }
-        for (; i < hi; ++i) rk += (bel2[i] < e) ? 1u : 0u;
-        if (rk < m) {
-            const int32_t id = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
-            a.victims[ob + rk] = id;
-            if (a.scores) a.scores[ob + rk] = __uint_as_float((uint32_t)(e >> 32));
-            c.sel[ob + rk] = e;
-            if (dec) dec[rk] = id;
+        lds_barrier();
+        const uint32_t bl = below_s, n = wpre[NW];
+        if (bl >= need) {
+            // this range and every later one lie beyond the first `need`
+        } else if (full_s) {
+            if (tid == 0) {
+                FinRange a1 = r, a2 = r;
+                if (r.e1 - r.e0 >= 2) {
+                    const int mid = (r.e0 + r.e1) / 2;
+                    a1.e1 = mid;
+                    a1.hi = ends[mid - 1];
+                    a2.e0 = mid;
+                    a2.lo = ends[mid - 1];
+                    a2.has_lo = 1;
+                } else {
+                    const unsigned long long lo = r.has_lo ? r.lo : 0ull;
+                    const unsigned long long m = lo + (r.hi - lo) / 2;
+                    a1.e0 = a1.e1 = a2.e0 = a2.e1 = 0;
+                    a1.hi = m;
+                    a2.lo = m;
+                    a2.has_lo = 1;
+                }
+                if (sp_s + 2 <= FIN_STACK) {
+                    stack[sp_s++] = a2;
+                    stack[sp_s++] = a1;
+                } else {
+                    stop_s = 1;  // cannot happen: each split at least halves a 64-bit range
+                }
+            }
+        } else {
+            // this thread's staged candidates (position p of the waves' regions in order)
+            unsigned long long e4[PER];
+            int b4[PER];
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                const uint32_t p = (uint32_t)(tid + u * FIN_THREADS);
+                b4[u] = -1;
+                if (p < n) {
+                    const int w = last_le<4>(wpre, NW, p);
+                    e4[u] = st1[w * WCAP + (p - wpre[w])];
+                    int b = 0;  // the bucket: ends below e
+                    if (has_ends) {
+#pragma unroll
+                        for (int st = 8; st > 0; st >>= 1)
+                            if (b + st < nbk && ends[r.e0 + b + st - 1] < e4[u]) b += st;
+                    }
+                    b4[u] = b;
+                    atomicMin(&bmin[b], e4[u]);
+                    atomicMax(&bmax[b], e4[u]);
+                }
+            }
+            lds_barrier();
+            if (tid < nbk) sbmul[tid] = (float)FIN_SB / ((float)(bmax[tid] - bmin[tid]) + 1.0f);
+            lds_barrier();
+            int k4[PER];
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                k4[u] = -1;
+                if (b4[u] >= 0) {
+                    int sb = (int)((float)(e4[u] - bmin[b4[u]]) * sbmul[b4[u]]);
+                    sb = sb < FIN_SB - 1 ? sb : FIN_SB - 1;
+                    k4[u] = b4[u] * FIN_SB + sb;
+                    atomicAdd(&hist[k4[u]], 1u);
+                }
+            }
+            lds_barrier();
+            // counting sort by sub-bin: offsets by a workgroup scan (one sub-bin per thread)
+            const uint32_t v = hist[tid];
+            const uint32_t inc = wave_incl_scan(v);
+            if (lane == SAE_WAVE - 1) wsum[wave] = inc;
+            lds_barrier();
+            uint32_t pre = 0;
+            for (int w = 0; w < wave; ++w) pre += wsum[w];
+            soff[tid] = pre + inc - v;
+            if (tid == FIN_THREADS - 1) soff[NSB] = pre + inc;
+            hist[tid] = 0;  // from here the fill count of the sub-bin
+            lds_barrier();
+#pragma unroll
+            for (int u = 0; u < PER; ++u)
+                if (k4[u] >= 0) st2[soff[k4[u]] + atomicAdd(&hist[k4[u]], 1u)] = e4[u];
+            lds_barrier();
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                if (k4[u] < 0) continue;
+                const uint32_t lo = soff[k4[u]], hi = soff[k4[u] + 1];
+                uint32_t rk = 0, i = lo;
+                for (; i + 4 <= hi; i += 4) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) rk += (st2[i + t] < e4[u]) ? 1u : 0u;
+                }
+                for (; i < hi; ++i) rk += (st2[i] < e4[u]) ? 1u : 0u;
+                const uint32_t rank = bl + lo + rk;
+                if (rank < need) out(rank, e4[u]);
+            }
         }
+        // thread 0 alone changes the stack, so it decides whether to go on
+        if (tid == 0) go_s = !(bl >= need || sp_s == 0 || stop_s);
+        lds_barrier();
+        if (!go_s) break;  // uniform
     }
 }
 
-// Pool-scan engine, step 6, per instance: the final list size of every queue;
-// the exact path for a queue whose buckets cannot give its list (or when
-// forced): stream the instance's pool, radix-select the need smallest
-// (key, id) and sort them; then the Algorithm 1 decision.
-__global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, int P, long long lds_bytes)
+// The exact path of one instance, run by the finisher alone when some queue's
+// candidates are incomplete (or when forced): every queue's list by a radix
+// select that streams the pool (its evictable blocks counted first), the
+// decision by merging the lists (Algorithm 1).
+__device__ void fin_exact(const DevCtx &c, const SelectArgs &a, int inst, uint32_t kq, const FinInfo &f, int P,
+                          long long lds_bytes, unsigned long long *el)
 {
-    extern __shared__ unsigned long long el[];  // exact path [2 * max(P, 256)]; sorted lists
     __shared__ SelState st;
     __shared__ ScoreTab tab;
     __shared__ int32_t cnt[SAE_MAX_QUEUES];
-    __shared__ uint32_t need_s[SAE_MAX_QUEUES], nev_s[SAE_MAX_QUEUES], cand_s[SAE_MAX_QUEUES];
-    __shared__ int32_t fb_s[SAE_MAX_QUEUES];
     __shared__ uint32_t lcount, st_s;
-    const int inst = blockIdx.x;
     const int Q = c.Q;
     const int tid = threadIdx.x;
-    const int wave = tid / SAE_WAVE;
     const int lane = lane_id();
     const long long N = c.N;
     const long long base = (long long)inst * N;
-    const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
     load_score_tab(tab, c.state[inst], c);
-    if (tid == 0) st_s = 0;
-    // one wave per queue: candidates, list size, whether the buckets suffice
-    if (wave < Q) {
-        const int q = wave;
-        const long long iq = (long long)inst * Q + q;
-        // every load of this wave in one round
-        const int NB = c.nsplit[iq];
-        const uint32_t ns = c.spill_n[iq];
-        const bool all = c.thr[iq] == ~0ull;
-        const uint32_t gt = (lane < SAE_GATHER_S) ? c.g_tot[iq * SAE_GATHER_S + lane] : 0u;
-        uint32_t bb[SAE_NBUCKET / SAE_WAVE], bz[SAE_NBUCKET / SAE_WAVE];
-#pragma unroll
-        for (int u = 0; u < SAE_NBUCKET / SAE_WAVE; ++u) {
-            bb[u] = c.bbelow[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
-            bz[u] = c.bsize[iq * SAE_NBUCKET + u * SAE_WAVE + lane];
-        }
-        uint32_t C = gt;
-        for (int d = 32; d > 0; d >>= 1) C += __shfl_xor(C, d, SAE_WAVE);
-        // a bound that admits every block makes the candidates the evictable
-        // blocks; otherwise fewer than k candidates send the queue to the exact path
-        const uint32_t need = (all && C < kq) ? C : kq;
-        const uint32_t nev = all ? C : 0xFFFFFFFFu;
-        // a bucket that holds some of the first `need` positions but is too big to sort
-        bool big = false;
-#pragma unroll
-        for (int u = 0; u < SAE_NBUCKET / SAE_WAVE; ++u)
-            big |= (u * SAE_WAVE + lane < NB) && bb[u] < need && bz[u] > SAE_BSORT;
-        const bool anybig = __ballot(big) != 0ull;
-        if (lane == 0) {
-            const bool fb = (a.flags & SAE_SS_FORCE_FALLBACK) || NB < 0 ||
-                            (need > 0 && (NB == 0 || C < need || C > SAE_LCAP || ns > (uint32_t)c.cand_cap ||
-                                          anybig));
-            need_s[q] = need;
-            nev_s[q] = nev;
-            cand_s[q] = C;
-            fb_s[q] = (fb && need > 0) ? 1 : 0;
-            uint32_t *dbg = c.sel_stats + iq * 4;
-            dbg[0] = nev;
-            dbg[1] = C;
-            dbg[2] = ns;
-            dbg[3] = fb_s[q];
-            cnt[q] = (int32_t)need;
-            a.count[iq] = (int32_t)need;
-            c.sel_count[iq] = (int32_t)need;
-        }
+    if (tid == 0) {
+        st_s = 0;
+        set_status(c.status, SAE_ST_SELECT_FALLBACK);
     }
     __syncthreads();
     uint32_t dummy = 0;
     for (int q = 0; q < Q; ++q) {
-        if (!fb_s[q]) continue;  // uniform
-        if (tid == 0) {
-            set_status(c.status, SAE_ST_SELECT_FALLBACK);
-            lcount = 0;
-        }
-        // the exact path counts the queue's evictable blocks itself
+        if (tid == 0) lcount = 0;
         __syncthreads();
         {
             uint32_t n = 0;
@@ -1615,20 +1619,21 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
             if (lane == 0 && n) atomicAdd(&lcount, n);
         }
         __syncthreads();
+        const uint32_t nev = lcount;
+        const uint32_t need = nev < kq ? nev : kq;
         if (tid == 0) {
-            const uint32_t nev = lcount;
-            const uint32_t nd = nev < kq ? nev : kq;
             const long long iq = (long long)inst * Q + q;
-            nev_s[q] = nev;
-            need_s[q] = nd;
-            cnt[q] = (int32_t)nd;
-            a.count[iq] = (int32_t)nd;
-            c.sel_count[iq] = (int32_t)nd;
-            c.sel_stats[iq * 4] = nev;
+            cnt[q] = (int32_t)need;
+            a.count[iq] = (int32_t)need;
+            c.sel_count[iq] = (int32_t)need;
+            uint32_t *dbg = c.sel_stats + iq * 4;
+            dbg[0] = nev;
+            dbg[1] = f.C[q];
+            dbg[2] = f.over[q];
+            dbg[3] = 1;
             lcount = 0;
         }
         __syncthreads();
-        const uint32_t need = need_s[q];
         if (need == 0) continue;  // uniform
         auto for_each = [&](auto &&fn) {
             for (long long b = tid; b < N; b += blockDim.x) {
@@ -1640,7 +1645,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
         };
         uint32_t needv[SAE_MAX_QUEUES], nevv[SAE_MAX_QUEUES];
         needv[0] = need;
-        nevv[0] = nev_s[q];
+        nevv[0] = nev;
         sel_init(st, 1, needv, nevv);
         for (int p = 0; p < 6 && st.any_active; ++p) {
             const int s = (p < 5) ? 53 - 11 * p : 0;
@@ -1683,7 +1688,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
     // stage 2 searches the sorted lists: from LDS when they fit
     const unsigned long long *lists = c.sel + (long long)inst * Q * c.max_k;
     int stride = c.max_k;
-    int n1 = (c.ef_queue >= 0) ? min((int)kq, cnt[c.ef_queue]) : 0;
+    const int n1 = (c.ef_queue >= 0) ? min((int)kq, cnt[c.ef_queue]) : 0;
     int maxc = 0;
     for (int q = 0; q < Q; ++q) maxc = max(maxc, (int)cnt[q]);
     if ((int)kq > n1 && (long long)Q * maxc * 8 <= lds_bytes) {
@@ -1695,16 +1700,113 @@ __global__ void __launch_bounds__(SEL_THREADS) k_merge(DevCtx c, SelectArgs a, i
         lists = el;
         stride = maxc;
     }
-    // stage 1 (the evict-first list) is already in the decision unless that list took the exact path
-    const bool copy1 = c.ef_queue >= 0 && fb_s[c.ef_queue];
-    const int d = merge_decision(lists, stride, cnt, Q, c.ef_queue, (int)kq, a.decision + (long long)inst * c.max_k,
-                                 copy1);
+    int32_t *dec = a.decision + (long long)inst * c.max_k;
+    const int d = merge_decision(lists, stride, cnt, Q, c.ef_queue, (int)kq, dec, true);
     if (tid == 0) {
         a.decision_count[inst] = d;
         // a cascading decision is completed (and counted) by k_cascade
         if (!(a.flags & SAE_SS_CASCADE)) commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
         set_status(c.status, st_s);
     }
+}
+
+__global__ void __launch_bounds__(FIN_THREADS) k_final(DevCtx c, SelectArgs a, int P, long long lds_bytes)
+{
+    extern __shared__ unsigned long long fdyn[];  // staging (group / union) or the exact path's sort
+    __shared__ FinInfo f;
+    __shared__ unsigned long long ends[FIN_G + 1];
+    __shared__ int32_t ref_s;
+    const int inst = blockIdx.y;
+    const int unit = blockIdx.x;
+    const int Q = c.Q;
+    const int tid = threadIdx.x;
+    const uint32_t kq = (uint32_t)inst_k(a, inst, c.max_k);
+    const int n_group = Q * FIN_GPQ;
+    if (unit < n_group && tid <= FIN_G) {
+        // a group's bucket ends go out with the first round of loads
+        const int b0 = (unit % FIN_GPQ) * FIN_G;
+        const unsigned long long *spl = c.split + ((long long)inst * Q + unit / FIN_GPQ) * SAE_NBUCKET;
+        ends[tid] = (b0 + tid - 1 >= 0) ? spl[b0 + tid - 1] : 0ull;
+    }
+    fin_info(c, a, inst, kq, f);
+    unsigned long long *st1 = fdyn, *st2 = fdyn + FIN_GCAP;
+    int32_t *dec = a.decision + (long long)inst * c.max_k;
+    if (unit < n_group + FIN_NU) {
+        if (f.any_fail) return;  // uniform: the finisher computes everything
+        const bool group = unit < n_group;
+        const int q = group ? unit / FIN_GPQ : 0;
+        if (!group && tid == 0) {
+            // the reference queue: smallest bound among the other queues with a list
+            int ref = -1;
+            for (int qq = 0; qq < Q; ++qq)
+                if (qq != c.ef_queue && f.need[qq] > 0 && (ref < 0 || f.thr[qq] < f.thr[ref])) ref = qq;
+            ref_s = ref;
+        }
+        lds_barrier();
+        const int rq = group ? q : ref_s;
+        const int per = group ? FIN_G : FIN_GU;
+        const int g = group ? unit % FIN_GPQ : unit - n_group;
+        const uint32_t need = group ? f.need[q] : (uint32_t)f.rest;
+        if (rq < 0 || need == 0) return;  // uniform
+        const int nb = f.nb[rq];
+        const int b0 = g * per;
+        if (b0 >= nb) return;  // uniform
+        const int b1 = b0 + per < nb ? b0 + per : nb;
+        if (!group) {  // the reference queue's ends (ends[0]: the lower end)
+            const unsigned long long *spl = c.split + ((long long)inst * Q + rq) * SAE_NBUCKET;
+            if (tid <= b1 - b0) ends[tid] = (b0 + tid - 1 >= 0) ? spl[b0 + tid - 1] : 0ull;
+            lds_barrier();
+        }
+        FinRange first;
+        first.has_lo = b0 > 0;
+        first.lo = ends[0];
+        first.hi = ends[b1 - b0];
+        first.e0 = 1;
+        first.e1 = 1 + (b1 - b0);
+        uint32_t src = 0;
+        if (group) {
+            src = 1u << q;
+        } else {
+            for (int qq = 0; qq < Q; ++qq)
+                if (qq != c.ef_queue && f.need[qq] > 0) src |= 1u << qq;
+        }
+        const long long ob = ((long long)inst * Q + q) * c.max_k;
+        const bool is_ef = group && q == c.ef_queue;
+        const int n1 = f.n1;
+        auto out = [&](uint32_t rank, unsigned long long e) {
+            const int32_t id = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
+            if (group) {
+                a.victims[ob + rank] = id;
+                if (a.scores) a.scores[ob + rank] = __uint_as_float((uint32_t)(e >> 32));
+                c.sel[ob + rank] = e;
+                if (is_ef) dec[rank] = id;
+            } else {
+                dec[n1 + (int)rank] = id;
+            }
+        };
+        fin_rank(c, inst, f, src, ends, first, need, st1, st2, out);
+        return;
+    }
+    // the finisher
+    if (!f.any_fail) {
+        if (tid < Q) {
+            const long long iq = (long long)inst * Q + tid;
+            a.count[iq] = (int32_t)f.need[tid];
+            c.sel_count[iq] = (int32_t)f.need[tid];
+            uint32_t *dbg = c.sel_stats + iq * 4;
+            dbg[0] = (f.thr[tid] == ~0ull) ? f.C[tid] : 0xFFFFFFFFu;
+            dbg[1] = f.C[tid];
+            dbg[2] = f.over[tid];
+            dbg[3] = 0;
+        }
+        if (tid == 0) {
+            a.decision_count[inst] = f.d;
+            // a cascading decision is completed (and counted) by k_cascade
+            if (!(a.flags & SAE_SS_CASCADE)) commit_bookkeeping(c.state[inst], f.d, (a.flags & SAE_SS_COMMIT) != 0);
+        }
+        return;
+    }
+    fin_exact(c, a, inst, kq, f, P, lds_bytes, fdyn);
 }
 
 // ---------------------------------------------------------------------------
@@ -1782,8 +1884,18 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
         find_crossing(hist, Q, st.rem, st.active, st.cr, st.seg_tot);
         sel_step(st, Q, s, w, p == 4);
     }
-    // collect (the histogram area is reused for the lists)
-    for (int i = tid; i < Q * P; i += blockDim.x) lists[i] = ~0ull;
+    // collect (the histogram area is reused for the lists); only the first
+    // Pe = pow2 >= the largest need of each segment is filled and sorted
+    __shared__ int32_t pe_s;
+    if (tid == 0) {
+        uint32_t mx = 1;
+        for (int q = 0; q < Q; ++q) mx = need_s[q] > mx ? need_s[q] : mx;
+        pe_s = pow2_ge((int)mx) < P ? pow2_ge((int)mx) : P;
+    }
+    __syncthreads();
+    const int Pe = pe_s;
+    const int lpe = 31 - __clz(Pe);
+    for (int i = tid; i < Q * Pe; i += blockDim.x) lists[(long long)(i >> lpe) * P + (i & (Pe - 1))] = ~0ull;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < BATCH_IPT; ++j) {
@@ -1799,7 +1911,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
         }
     }
     __syncthreads();
-    bitonic_sort_segments(lists, Q, P);
+    bitonic_sort_segments(lists, Q, Pe, P);
     if (tid < Q) cnt_s[tid] = (int32_t)min(need_s[tid], (uint32_t)P);
     __syncthreads();
     for (int q = 0; q < Q; ++q) {
@@ -2210,14 +2322,15 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
     else
         hipLaunchKernelGGL(k_scan, dim3(c.scan_gx, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 4: group the candidates by bucket
-    const size_t lds_c = (size_t)(SAE_LCAP / SAE_GATHER_S + 1) * sizeof(unsigned long long);
-    if ((e = allow_lds((const void *)k_gather, lds_c)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_gather, dim3(SAE_GATHER_S, c.Q, c.n_inst), dim3(GATHER_THREADS), lds_c, s, c, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 5: sort the buckets
-    const size_t lds_b = (size_t)2 * SAE_BSORT * sizeof(unsigned long long);
-    hipLaunchKernelGGL(k_bucket, dim3(SAE_NBUCKET, c.Q, c.n_inst), dim3(BUCKET_THREADS), lds_b, s, c, a);
+    // step 4: lists, decision and commit
+    const int P = pow2_at_least(c.max_k);
+    size_t lds = (size_t)2 * FIN_GCAP * sizeof(unsigned long long);  // staging of a range
+    const size_t ex = (size_t)2 * (P < 256 ? 256 : P) * sizeof(unsigned long long);  // the exact path's sort
+    if (ex > lds) lds = ex;
+    if (lds < (size_t)SAE_BINS * sizeof(uint32_t)) lds = (size_t)SAE_BINS * sizeof(uint32_t);
+    if ((e = allow_lds((const void *)k_final, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_final, dim3(c.Q * FIN_GPQ + FIN_NU + 1, c.n_inst), dim3(FIN_THREADS), lds, s, c, a, P,
+                       (long long)lds);
     return hipGetLastError();
 }
 
@@ -2234,20 +2347,6 @@ int scan_grid_x(int n_inst, int N)
     if (gx < 1) gx = 1;
     if (gx > 2048) gx = 2048;
     return (int)gx;
-}
-
-hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s)
-{
-    const int P = pow2_at_least(c.max_k);
-    // the exact path's sort (and histogram), or the sorted lists of stage 2 when they fit
-    size_t lds = (size_t)2 * (P < 256 ? 256 : P) * sizeof(unsigned long long);
-    if (lds < (size_t)SAE_BINS * sizeof(uint32_t)) lds = (size_t)SAE_BINS * sizeof(uint32_t);
-    const size_t lists = (size_t)c.Q * P * sizeof(unsigned long long);
-    if (lists > lds) lds = lists < (size_t)128 * 1024 ? lists : (size_t)128 * 1024;
-    hipError_t e = allow_lds((const void *)k_merge, lds);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_merge, dim3(c.n_inst), dim3(SEL_THREADS), lds, s, c, a, P, (long long)lds);
-    return hipGetLastError();
 }
 
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s)

@@ -168,25 +168,13 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     d.index_mask = (uint32_t)(c->index_slots - 1);
     d.ghost_mask = (uint32_t)(c->ghost_slots - 1);
 
-    long long cc = 8ll * d.max_k;
-    if (cc < 32768) cc = 32768;
-    if (cc > d.N) cc = d.N;
-    d.cand_cap = (int32_t)cc;
-
     const long long I = d.n_inst, Q = d.Q;
     d.scan_gx = scan_grid_x(d.n_inst, d.N);
-    const long long GX = d.scan_gx;
     bool ok = dev_alloc(c, &d.state, I) && dev_alloc(c, &d.status, 1) &&
               dev_alloc(c, &d.index, I * c->index_slots) && dev_alloc(c, &d.ring, I * d.ring_cap) &&
               dev_alloc(c, &d.gtab, I * c->ghost_slots) && dev_alloc(c, &d.thr, I * Q) && dev_alloc(c, &d.sent, I * 64) && dev_alloc(c, &d.eflim, I * 16) &&
-              dev_alloc(c, &d.creg, I * GX * Q * SAE_CAND_REGION) &&
-              dev_alloc(c, &d.creg_n, I * GX * Q) && dev_alloc(c, &d.spill, I * Q * d.cand_cap) &&
-              dev_alloc(c, &d.spill_n, I * Q) && dev_alloc(c, &d.split, I * Q * SAE_NBUCKET) &&
-              dev_alloc(c, &d.nsplit, I * Q) && dev_alloc(c, &d.bsize, I * Q * SAE_NBUCKET) &&
-              dev_alloc(c, &d.bbelow, I * Q * SAE_NBUCKET) && dev_alloc(c, &d.cand, I * Q * SAE_LCAP) &&
-              dev_alloc(c, &d.g_base, I * Q * SAE_GATHER_S) && dev_alloc(c, &d.g_tot, I * Q * SAE_GATHER_S) &&
-              dev_alloc(c, &d.g_rel, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
-              dev_alloc(c, &d.g_cnt, I * Q * SAE_GATHER_S * SAE_NBUCKET) &&
+              dev_alloc(c, &d.split, I * Q * SAE_NBUCKET) && dev_alloc(c, &d.nsplit, I * Q) &&
+              dev_alloc(c, &d.cand, I * Q * 2 * SAE_LCAP) && dev_alloc(c, &d.stripe_n, I * Q * (SAE_STRIPES + 1)) &&
               dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
               dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
               dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&
@@ -570,7 +558,6 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
             e1 = pr.second;
         }
         e = launch_select_scan(c->dc, a, s, e0, e1);
-        if (e == hipSuccess) e = launch_merge(c->dc, a, s);
     }
     if (e == hipSuccess && (flags & SAE_SS_CASCADE)) {
         e = launch_cascade(c->dc, a, s, c->casc_set);

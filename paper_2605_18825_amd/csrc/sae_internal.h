@@ -22,13 +22,16 @@
 // Sampling of the pool-scan engine: chunks per instance and blocks per chunk.
 #define SAE_SAMPLE_WGS 64
 #define SAE_SAMPLE_CHUNK 256
-#define SAE_GATHER_S 16       // slices of the scan workgroups, per (instance, queue), in the gather
-#define SAE_CAND_REGION 128  // candidate slots per (scan workgroup, queue)
 // Candidate buckets of the pool-scan engine, per (instance, queue): the bucket
 // upper ends are sampled (key, id) values at or below the candidate bound.
 #define SAE_NBUCKET 256  // buckets
-#define SAE_BSORT 2048   // largest bucket one workgroup sorts
 #define SAE_LCAP 16384   // candidates kept per (instance, queue)
+// The scan appends a queue's candidates to one of SAE_STRIPES stripes of
+// SAE_LCAP / SAE_STRIPES slots (one device atomic per workgroup and queue,
+// spread over the stripes so that few workgroups meet on one counter); what
+// does not fit a stripe goes to the queue's overflow list of SAE_LCAP slots.
+#define SAE_STRIPES 64
+#define SAE_STRIPE_CAP (SAE_LCAP / SAE_STRIPES)
 
 // Feedback counters are added into one of SAE_CSLOTS striped copies (chosen by
 // the adding workgroup) and folded into InstState by the learner kernel:
@@ -108,7 +111,6 @@ struct DevCtx {
     int32_t W;         // ghost window
     int32_t ring_cap;  // W + max_k
     uint32_t index_mask, ghost_mask;
-    int32_t cand_cap;  // spilled candidates per (instance, queue), scan engine
     // pool (caller-owned)
     int32_t *la;
     uint16_t *meta;
@@ -129,20 +131,13 @@ struct DevCtx {
     int32_t *eflim;            // [n_inst][16] evict-first queue: largest candidate id per num_tokens - 1 (-1: none)
     unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
     uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
-    uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, spilled, slow path
-    unsigned long long *creg;  // [n_inst][scan_gx][Q][SAE_CAND_REGION] candidates per scan workgroup
-    uint32_t *creg_n;          // [n_inst][scan_gx][Q]
-    unsigned long long *spill; // [n_inst][Q][cand_cap] candidates beyond a region
-    uint32_t *spill_n;         // [n_inst][Q]
+    uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, beyond a stripe, slow path
     unsigned long long *split; // [n_inst][Q][SAE_NBUCKET] bucket upper ends, ascending; the last is thr
-    int32_t *nsplit;           // [n_inst][Q] buckets (0: no candidates; -1: exact path)
-    unsigned long long *cand;  // [n_inst][Q][SAE_LCAP] candidates, per slice grouped by bucket
-    uint32_t *g_base;          // [n_inst][Q][SAE_GATHER_S] where each slice starts in cand
-    uint32_t *g_tot;           // [n_inst][Q][SAE_GATHER_S] candidates per slice (all slices: > SAE_LCAP = too many)
-    uint32_t *g_rel;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket start within its slice
-    uint32_t *g_cnt;           // [n_inst][Q][SAE_GATHER_S][SAE_NBUCKET] bucket size within its slice
-    uint32_t *bsize;           // [n_inst][Q][SAE_NBUCKET] candidates per bucket
-    uint32_t *bbelow;          // [n_inst][Q][SAE_NBUCKET] candidates below the bucket
+    int32_t *nsplit;           // [n_inst][Q] buckets (0: no candidates)
+    unsigned long long *cand;  // [n_inst][Q][2 SAE_LCAP] candidates, unordered: the stripes
+                               // (SAE_STRIPES x SAE_STRIPE_CAP), then the overflow list
+    uint32_t *stripe_n;        // [n_inst][Q][SAE_STRIPES + 1] slots taken in each stripe (may exceed its
+                               // capacity: the rest went to the overflow list), then in the overflow list
     int32_t scan_gx;           // scan workgroups per instance
     int32_t *cpart;            // [n_inst][SAE_CSLOTS][SAE_CF_STRIDE] feedback counters, striped
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
@@ -229,6 +224,90 @@ __device__ __forceinline__ uint32_t hash_home(unsigned long long h, uint32_t mas
     unsigned long long z = h ^ (h >> 31);
     z *= 0x9E3779B97F4A7C15ull;
     return (uint32_t)(z >> 32) & mask;
+}
+
+// index_erase and ghost_insert continued from the home slot s0 whose hash v0
+// the caller has already loaded (so that several first probes can be in
+// flight together): linear probing from the home slot, as every lookup of
+// the block index and of recently_evicted does.
+__device__ __forceinline__ void index_erase_from(IndexSlot *tab, uint32_t mask, unsigned long long h, uint32_t s0,
+                                                 unsigned long long v0)
+{
+    uint32_t s = s0;
+    unsigned long long v = v0;
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        if (p > 0) v = tab[s].hash;
+        if (v == h) {
+            tab[s].hash = SAE_TOMB_HASH;
+            return;
+        }
+        if (v == SAE_EMPTY_HASH) return;
+        s = (s + 1) & mask;
+    }
+}
+
+__device__ __forceinline__ bool ghost_insert_from(GhostSlot *tab, uint32_t mask, unsigned long long h,
+                                                  uint32_t ring_pos, uint32_t s0, unsigned long long v0)
+{
+    uint32_t s = s0;
+    unsigned long long v = v0;
+    bool fresh = true;  // v holds slot s's hash as loaded
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        if (!fresh) v = tab[s].hash;
+        fresh = false;
+        if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
+            unsigned long long old = atomicCAS(&tab[s].hash, v, h);
+            if (old == v) {
+                tab[s].ring = ring_pos;
+                return true;
+            }
+            continue;
+        }
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+// Commit of victim v at decision position j (of d) of instance inst: free the
+// block, erase its index entry, count it into the LDS sums (Algorithm 3's
+// evicted[tau], Algorithm 2's queue_evictions[q], the queue's cached
+// blocks), take it from its parent (a parent left without a cached child
+// becomes a leaf) and record it in recently_evicted at ring position
+// evb + j, stamped evb + d (evb: eviction_count before the decision).
+__device__ __forceinline__ void commit_victim(const DevCtx &c, int inst, int j, int32_t v, long long evb, int d,
+                                              int32_t *sums)
+{
+    const long long g = (long long)inst * c.N + v;
+    // one round trip for the block's fields, then one for the parent's
+    // count and the first probes of both tables together
+    const uint32_t m = c.meta[g];
+    const unsigned long long h = c.hash[g];
+    const int32_t p = c.parent[g];
+    const uint32_t off = c.off[g];
+    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
+    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    const uint32_t si = hash_home(h, c.index_mask), sg = hash_home(h, c.ghost_mask);
+    const unsigned long long vi = tab[si].hash, vg = gt[sg].hash;
+    const bool has_p = p >= 0 && p < c.N;
+    const long long gp = (long long)inst * c.N + (has_p ? p : 0);
+    const int before = has_p ? atomicSub(&c.child_count[gp], 1) : 0;
+    atomicAdd(&sums[SAE_CF_EVICTED + meta_type(m) % SAE_N_TYPES], 1);
+    atomicAdd(&sums[SAE_CF_EVICTIONS + meta_queue(m)], 1);
+    atomicSub(&sums[SAE_CF_RES + meta_queue(m)], 1);
+    meta_and(c.meta, g, (uint32_t)(~SAE_META_VALID) & 0xFFFFu);
+    const bool hashed = !SAE_HASH_RESERVED(h);  // a reserved hash was never indexed
+    if (hashed) index_erase_from(tab, c.index_mask, h, si, vi);
+    if (has_p && before == 1) meta_or(c.meta, gp, SAE_META_LEAF);
+    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    const uint32_t rp = (uint32_t)((evb + j) % c.ring_cap);
+    GhostEntry e;
+    e.hash = hashed ? h : SAE_EMPTY_HASH;  // an empty entry is never found
+    e.stamp = evb + d;
+    e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
+           (pos_bin(off) << SAE_TQ_BIN_SHIFT);
+    e.pad_ = 0;
+    ring[rp] = e;
+    if (hashed && !ghost_insert_from(gt, c.ghost_mask, h, rp, sg, vg)) set_status(c.status, SAE_ST_GHOST_FULL);
 }
 
 // ----------------------------------------------------------------------------
@@ -471,7 +550,6 @@ hipError_t launch_index_rebuild(const DevCtx &c, hipStream_t s);
 hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s,
                               hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
-hipError_t launch_merge(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s, int set);
 hipError_t launch_predict(int n, int d, const uint16_t *h, const uint16_t *w1, const float *b1, const float *w2,
                           const float *b2, const float *w3, const float *b3, float *work, float *logit,

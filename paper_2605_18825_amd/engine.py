@@ -119,18 +119,28 @@ class DeviceBackend:
             api.sae_ref_blocks(self.ctx, d[1], delta, inst=d[0])
 
     def evict(self, now, k):
-        kd = self.st.put("k", np.asarray(k, np.int32), torch.int32)
-        self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd)
+        k = np.asarray(k, np.int32)
+        if self.n_inst == 1:  # one cache: k goes by value
+            self.out.run(self.ctx, now, int(k[0]), self.select_flags)
+        else:
+            kd = self.st.put("k", k, torch.int32)
+            self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd)
+        self.select_calls += 1
+        small = self.n_inst * self.max_k <= 16384
         cnt = self.st.get("cnt", self.out.decision_count)
+        if small:  # the whole decision buffer comes back with the counts
+            dec = self.st.get("dec", self.out.decision)
         self.stream.synchronize()
         cnt = cnt.view(np.int32)[:self.n_inst].copy()
         m = int(cnt.max()) if len(cnt) else 0
-        self.select_calls += 1
         if m == 0:
             return [np.zeros(0, np.int32) for _ in range(self.n_inst)]
-        dec = self.st.get("dec", self.out.decision[:, :m])
-        self.stream.synchronize()
-        dec = dec.view(np.int32)[:self.n_inst * m].reshape(self.n_inst, m)
+        if small:
+            dec = dec.view(np.int32)[:self.n_inst * self.max_k].reshape(self.n_inst, self.max_k)
+        else:
+            dec = self.st.get("dec", self.out.decision[:, :m])
+            self.stream.synchronize()
+            dec = dec.view(np.int32)[:self.n_inst * m].reshape(self.n_inst, m)
         return [dec[i, :cnt[i]].copy() for i in range(self.n_inst)]
 
     def insert(self, now, f):

@@ -22,7 +22,7 @@ def pool_of(kinds, mix, seed):
 
 
 def stats(pair):
-    return [dict(zip(("evictable", "candidates", "spilled", "slow"), s)) for s in api.sae_select_stats(pair.ctx, 0, pair.Q)]
+    return [dict(zip(("evictable", "candidates", "beyond_stripes", "slow"), s)) for s in api.sae_select_stats(pair.ctx, 0, pair.Q)]
 
 
 def run(pair, pool, k, rounds=3, commit=False, expect_fallback=False):
