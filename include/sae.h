@@ -15,7 +15,10 @@
  *    Pointers documented "host" are read or written before the call returns.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream).  A context is not thread-safe: use it from one stream at a
- *    time.  Calls that overlap on one context race.
+ *    time.  Calls that overlap on one context race, with one exception: a
+ *    read-only sae_prefix_match (no flags) may run on another stream while a
+ *    sae_score_select without SAE_SS_COMMIT runs, since neither writes what
+ *    the other reads (the pool, the index, the parameters).
  *  - The context allocates all of its internal device memory in sae_create();
  *    the hot calls (sae_prefix_match, sae_score_select, sae_feedback_update)
  *    never allocate.
@@ -293,6 +296,9 @@ enum { SAE_PM_TOUCH = 1u << 0, SAE_PM_STATS = 1u << 1, SAE_PM_INTERVALS = 1u << 
  * SAE_LEARN_DECAY_POWER bit is set, to the hits of its positional bin
  * floor(8 o_b / o_max) (decay-power learner, App. B); with SAE_LEARN_TOKEN_EMA
  * set, to type_hits[its type].
+ * The queue, type and positional bin counted for a block are the ones it had
+ * when it entered the index (sae_insert_blocks or sae_index_build): a caller
+ * that rewrites those pool fields of a valid block rebuilds the index.
  * SAE_PM_INTERVALS records Algorithm 4's reuse intervals: for every request
  * and every log-normal queue among its matched blocks, dt = now - last_access
  * of its deepest matched block of that queue, as it was before the call,

@@ -26,7 +26,7 @@ constexpr int kThreads = 256;
 // flight together, so a lookup usually costs one memory round trip.  Tables
 // hold at least 64 slots, a multiple of IDX_GROUP.
 #define IDX_GROUP 8
-__device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h)
+__device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h, uint32_t *tq)
 {
     const uint4 *t4 = reinterpret_cast<const uint4 *>(tab);
     if (SAE_HASH_RESERVED(h)) return -1;
@@ -43,7 +43,10 @@ __device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, u
             if ((uint32_t)t < s - g || seen >= lim) continue;
             ++seen;
             const unsigned long long vh = (unsigned long long)v[t].x | ((unsigned long long)v[t].y << 32);
-            if (vh == h) return (int32_t)v[t].z;
+            if (vh == h) {
+                *tq = v[t].w;
+                return (int32_t)v[t].z;
+            }
             if (vh == SAE_EMPTY_HASH) return -1;
         }
         s = (g + IDX_GROUP) & mask;
@@ -51,7 +54,8 @@ __device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, u
     return -1;
 }
 
-__device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsigned long long h, int32_t id)
+__device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsigned long long h, int32_t id,
+                                             uint32_t tq)
 {
     uint32_t s = hash_home(h, mask);
     for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
@@ -59,7 +63,7 @@ __device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsi
         if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
             unsigned long long old = atomicCAS(&tab[s].hash, v, h);
             if (old == v) {
-                tab[s].id = id;
+                *reinterpret_cast<uint2 *>(&tab[s].id) = make_uint2((uint32_t)id, tq);
                 return true;
             }
             continue;  // lost the slot: look at it again
@@ -170,6 +174,7 @@ __global__ void k_clear_all(DevCtx c, int clear_ghost_and_counters)
     if (i < nidx) {
         c.index[i].hash = SAE_EMPTY_HASH;
         c.index[i].id = -1;
+        c.index[i].tq = 0;
     }
     if (!clear_ghost_and_counters) return;
     long long ngt = (long long)c.n_inst * ((long long)c.ghost_mask + 1);
@@ -223,7 +228,8 @@ __global__ void k_index_fill(DevCtx c, int census)
             IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
             const unsigned long long h = c.hash[g];
             if (SAE_HASH_RESERVED(h)) set_status(c.status, SAE_ST_BAD_HASH);
-            else if (!index_insert(tab, c.index_mask, h, b)) set_status(c.status, SAE_ST_INDEX_FULL);
+            else if (!index_insert(tab, c.index_mask, h, b, slot_tq(m, c.off[g])))
+                set_status(c.status, SAE_ST_INDEX_FULL);
             if (census) {
                 if (one_inst) atomicAdd(&cnt[meta_queue(m)], 1);
                 else atomicAdd(counter_slot(c, inst, blockIdx.x) + SAE_CF_RES + meta_queue(m), 1);
@@ -294,7 +300,7 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     c.ref_count[g] = 0;
     c.access_count[g] = 0;
     IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    if (!index_insert(tab, c.index_mask, h, b)) set_status(c.status, SAE_ST_INDEX_FULL);
+    if (!index_insert(tab, c.index_mask, h, b, slot_tq(m, off[i]))) set_status(c.status, SAE_ST_INDEX_FULL);
     int32_t *cs = counter_slot(c, inst, i);
     atomicAdd(cs + SAE_CF_RES + meta_queue(m), 1);
     if (c.state[inst].learn & SAE_LEARN_TOKEN_EMA) atomicAdd(cs + SAE_CF_TADD + meta_type(m) % SAE_N_TYPES, 1);
@@ -422,11 +428,11 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
             const uint64_t *hr = hashes + (long long)r * max_len;
             int m = 0;
             int j0 = 0;
-            // software-pipelined over chunks of 64 hashes: the next chunk's
-            // hashes are fetched with this chunk's probe, and its probe goes
-            // out right after this chunk's block fields are requested, so a
-            // matched chunk costs no extra round trip for its fields
-            int32_t id = (lane < len) ? index_find(tab, c.index_mask, hr[lane]) : -1;
+            // Chunks of 64 hashes.  The index slot carries the block's queue,
+            // type and positional bin, so a chunk costs one round trip (its
+            // probe); the next chunk's hashes come with this chunk's probe.
+            uint32_t tq = 0;
+            int32_t id = (lane < len) ? index_find(tab, c.index_mask, hr[lane], &tq) : -1;
             unsigned long long hnext = (SAE_WAVE + lane < len) ? hr[SAE_WAVE + lane] : 0ull;
             for (; j0 < len; j0 += SAE_WAVE) {
                 const int j = j0 + lane;
@@ -437,22 +443,11 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                 const bool hit = lane < lim;
                 int q = 0, ty = 0;
                 uint32_t bin = 0;
-                // unconditional (block 0 for lanes without a hit): a load in a
-                // divergent block would be waited for at its end
-                const long long gh = base + (hit ? id : 0);
-                const uint32_t off = bins ? c.off[gh] : 0u;  // loaded beside meta, not after it
-                const uint32_t mt = c.meta[gh];
-                int32_t idn = -1;
-                if (!mm && j0 + SAE_WAVE < len) {  // uniform: this chunk matched whole
-                    const int jn = j + SAE_WAVE;
-                    idn = (jn < len) ? index_find(tab, c.index_mask, hnext) : -1;
-                    hnext = (jn + SAE_WAVE < len) ? hr[jn + SAE_WAVE] : 0ull;
-                }
                 if (hit) {
                     const long long g = base + id;
-                    q = meta_queue(mt);
-                    ty = meta_type(mt) % SAE_N_TYPES;
-                    if (bins && ((c.struct_mask >> q) & 1u)) bin = pos_bin(off);
+                    q = (int)((tq >> 3) & 7u);
+                    ty = (int)(tq & 7u);
+                    if (bins && ((c.struct_mask >> q) & 1u)) bin = tq >> SAE_TQ_BIN_SHIFT;
                     if (touch) {
                         c.la[g] = now;
                         atomicAdd(&c.access_count[g], 1);
@@ -486,11 +481,14 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                     }
                 }
                 m = j0 + lim;
-                if (mm) {
+                if (mm || j0 + SAE_WAVE >= len) {  // uniform
                     j0 += SAE_WAVE;
                     break;
                 }
-                id = idn;
+                // this chunk matched whole: probe the next one
+                const int jn = j + SAE_WAVE;
+                id = (jn < len) ? index_find(tab, c.index_mask, hnext, &tq) : -1;
+                hnext = (jn + SAE_WAVE < len) ? hr[jn + SAE_WAVE] : 0ull;
             }
             if (mid)
                 for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;

@@ -159,13 +159,16 @@ __device__ void sel_init(SelState &st, int nq, const uint32_t *need, const uint3
 }
 
 // One refinement step after the histogram of digit (shift, width) was built.
+// The selection is complete when the elements below the crossing bin and the
+// bin itself are exactly the ones still needed: then every element whose
+// digits up to this one are at most the bin's is taken.
 __device__ void sel_step(SelState &st, int nq, int shift, int width, bool last)
 {
     int tid = threadIdx.x;
     if (tid < nq && st.active[tid]) {
         Crossing c = st.cr[tid];
         unsigned long long pb = (st.prefix[tid] << width) | (unsigned long long)c.bin;
-        if (c.cnt == st.rem[tid] || last) {
+        if (c.below + c.cnt == st.rem[tid] || last) {
             st.mode[tid] = 2;
             st.shift[tid] = shift;
             st.bound[tid] = pb;

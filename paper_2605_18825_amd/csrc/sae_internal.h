@@ -83,11 +83,14 @@ struct InstState {
     long long ivl_start[SAE_MAX_QUEUES];  // first interval still in the buffer (before the cap)
 };
 
-// Open-addressing slot of the block index: content hash -> block id.
+// Open-addressing slot of the block index: content hash -> block id, with the
+// block's type, queue and positional bin as of its insertion (the layout of
+// GhostEntry.tq without the consumed bit), so a prefix match counts its hits
+// without reading the pool.
 struct IndexSlot {
     unsigned long long hash;  // SAE_EMPTY_HASH, SAE_TOMB_HASH or a content hash
     int32_t id;
-    int32_t pad_;
+    uint32_t tq;  // tau | queue << 3 | pos_bin << SAE_TQ_BIN_SHIFT
 };
 
 // recently_evicted: a ring in eviction order plus a hash table into it.
@@ -188,6 +191,15 @@ __device__ __forceinline__ uint32_t pos_bin(uint32_t off)
 // Meta field access.
 __device__ __forceinline__ int meta_queue(uint32_t m) { return (int)(m & 7u); }
 __device__ __forceinline__ int meta_type(uint32_t m) { return (int)((m >> 3) & 7u); }
+
+// Type, queue and positional bin of a block (meta m, offsets off) packed as
+// tau | queue << 3 | pos_bin << SAE_TQ_BIN_SHIFT: the recently_evicted entry
+// and the index slot of the block carry it.
+__device__ __forceinline__ uint32_t slot_tq(uint32_t m, uint32_t off)
+{
+    return (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
+           (pos_bin(off) << SAE_TQ_BIN_SHIFT);
+}
 __device__ __forceinline__ int meta_ntok(uint32_t m) { return (int)((m >> 9) & 15u) + 1; }
 __device__ __forceinline__ bool meta_evictable(uint32_t m)
 {
@@ -303,8 +315,7 @@ __device__ __forceinline__ void commit_victim(const DevCtx &c, int inst, int j, 
     GhostEntry e;
     e.hash = hashed ? h : SAE_EMPTY_HASH;  // an empty entry is never found
     e.stamp = evb + d;
-    e.tq = (uint32_t)(meta_type(m) % SAE_N_TYPES) | ((uint32_t)meta_queue(m) << 3) |
-           (pos_bin(off) << SAE_TQ_BIN_SHIFT);
+    e.tq = slot_tq(m, off);
     e.pad_ = 0;
     ring[rp] = e;
     if (hashed && !ghost_insert_from(gt, c.ghost_mask, h, rp, sg, vg)) set_status(c.status, SAE_ST_GHOST_FULL);

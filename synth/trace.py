@@ -47,7 +47,7 @@ import subprocess
 
 import numpy as np
 
-from .pools import M64, ROOT, mix64
+from .pools import M64, MU_AGENT_MS, MU_CHAT_MS, ROOT, SIGMA_AGENT, SIGMA_CHAT, mix64
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "chain.c")
@@ -268,3 +268,28 @@ TRACE_CONFIGS = {
     "batched_sweep": dict(mixes=("single_turn_dominant", "multi_turn_dominant"), n_requests=10_000, n_inst=256,
                           capacity=65536, k_min=256, max_k=4096, K=32, seed=1005, concurrency=4),
 }
+
+
+# The paper's four queues of the trace configurations (Sec. 3.1): evict-first,
+# structural, chat and agent (kinds 0 evict-first, 1 structural, 2 log-normal),
+# their starting timing parameters, and the Classify roles.
+TRACE_KINDS = [0, 1, 2, 2]
+TRACE_ROLES = [0, 1, 2, 3]
+TRACE_MU = [0.0, 0.0, MU_CHAT_MS, MU_AGENT_MS]
+TRACE_SIGMA = [1.0, 1.0, SIGMA_CHAT, SIGMA_AGENT]
+
+
+def trace_gen(name, inst, n_inst=None, **over):
+    """Request generator of instance `inst` of trace configuration `name`."""
+    cfg = TRACE_CONFIGS[name]
+    n_inst = cfg["n_inst"] if n_inst is None else n_inst
+    if "mixes" in cfg:
+        mix = cfg["mixes"][0 if inst < n_inst // 2 else 1]
+    else:
+        mix = cfg["mix"]
+    return TraceGen(mix, cfg["seed"] * 1000 + inst, **over)
+
+
+def trace_gens(name, n_inst, **over):
+    return [trace_gen(name, i, n_inst, **over) for i in range(n_inst)]
+

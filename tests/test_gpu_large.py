@@ -29,6 +29,40 @@ def test_large_select_no_commit(large):
     assert not p.status()
 
 
+def test_large_select_with_concurrent_prefix_match(large):
+    """The large-pool configuration's concurrent case: a read-only prefix match
+    of 4,096 requests x 128 hashes on a second stream overlaps the
+    score+select pass on the first; both results equal the oracle's."""
+    import torch
+    p, pool, cfg = large
+    R, L = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], 5)
+    now = pool["now"] + 1
+    hd = torch.as_tensor(np.asarray(R, np.uint64).view(np.int64)).cuda()
+    ld = torch.as_tensor(np.asarray(L, np.int32)).cuda()
+    ml = torch.full((len(L),), -7, dtype=torch.int32, device="cuda")
+    mid = torch.full(hd.shape, -7, dtype=torch.int32, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    say("large: score_select on stream A, read-only prefix match on stream B")
+    p.out.run(p.ctx, now, cfg["k"], 0, stream=sa)
+    api.sae_prefix_match(p.ctx, hd, ld, now, 0, ml, matched_ids=mid, stream=sb)
+    torch.cuda.synchronize()
+    om, omid = p.oc.prefix_match(R, L, now, touch=False, stats=False)
+    assert np.array_equal(ml.cpu().numpy(), om), "match lengths differ"
+    assert np.array_equal(mid.cpu().numpy(), omid), "matched ids differ"
+    lists, key, dec = p.oc.score_select(now, cfg["k"])
+    cnt = p.out.count[0].cpu().numpy()
+    vic = p.out.victims[0].cpu().numpy()
+    sc = p.out.scores[0].cpu().numpy().view(np.uint32)
+    for q in range(p.Q):
+        c = int(cnt[q])
+        assert c == len(lists[q]) and np.array_equal(vic[q, :c], lists[q]), "queue %d differs" % q
+        assert np.array_equal(sc[q, :c], key[lists[q]]), "queue %d: score bits differ" % q
+    d = int(p.out.decision_count[0])
+    assert d == len(dec) and np.array_equal(p.out.decision[0, :d].cpu().numpy(), dec)
+    assert not p.status()
+
+
 def test_large_fallback_path(large):
     p, pool, cfg = large
     say("large: exact slow path")

@@ -46,6 +46,48 @@ def test_score_select(tiny, engine):
     assert set(st) <= {"SELECT_FALLBACK"}, st
 
 
+def _early_stops(e, need, digits):
+    """Digit steps of a most-significant-digit radix select of the `need`
+    smallest of the distinct composites e where the crossing bin alone holds
+    `need` elements while smaller bins hold others: a selection that stopped
+    there on the bin's count alone would take too many."""
+    n, rem = 0, need
+    for i, (s, w) in enumerate(digits):
+        d = ((e >> np.uint64(s)) & np.uint64((1 << w) - 1)).astype(np.int64)
+        h = np.bincount(d, minlength=1 << w)
+        cum = np.cumsum(h)
+        b = int(np.searchsorted(cum, rem))
+        below, cnt = int(cum[b] - h[b]), int(h[b])
+        n += int(cnt == rem and below > 0 and i < len(digits) - 1)
+        if below + cnt == rem:
+            break
+        e, rem = e[d == b], rem - below
+    return n
+
+
+def test_score_select_k_sweep(tiny):
+    """k = 1 .. 64 on every engine: among these, some k put exactly k keys of a
+    queue in the crossing bin of a digit with smaller keys below it (checked
+    here for both composite layouts: (key, id) in 48 bits for the batched
+    engine, 64 bits for the exact path)."""
+    p, pool, cfg = tiny
+    key, _ = p.oc.keys(pool["now"])
+    ev = p.oc.evictable()
+    layouts = {48: ([(37, 11), (26, 11), (15, 11), (4, 11), (0, 4)], 16),
+               64: ([(53, 11), (42, 11), (31, 11), (20, 11), (9, 11), (0, 9)], 32)}
+    for bits, (digits, sh) in layouts.items():
+        hits = 0
+        for q in range(p.Q):
+            ids = np.nonzero(ev & (p.oc.queue == q))[0].astype(np.uint64)
+            e = (key[ids].astype(np.uint64) << np.uint64(sh)) | ids
+            hits += sum(_early_stops(e, k, digits) for k in range(1, 65) if k < len(ids))
+        assert hits > 0, "no k in the sweep exercises the %d-bit case" % bits
+    for flags in (api.SS_ENGINE_BATCHED, api.SS_ENGINE_SCAN, api.SS_FORCE_FALLBACK):
+        say("tiny k sweep flags %d" % flags)
+        for k in range(1, 65):
+            p.select(pool["now"], k, flags)
+
+
 def test_prefix_match_and_stats(tiny):
     p, pool, cfg = tiny
     R, L = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], 77)
