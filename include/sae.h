@@ -444,6 +444,24 @@ typedef struct {
 sae_status sae_predict_sessions(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, float *work,
                                 float *logit, uint8_t *pred, sae_stream_t stream);
 
+/*
+ * Session predictor for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and results as sae_predict_sessions, with
+ * no `work` argument.  Layer 1's partial sums go to a buffer of the library's
+ * own, one per GPU, of SAE_PRED_NOALLOC_MAX_N rows (16 MiB), held by each GPU
+ * the library runs on until the process ends; the call allocates nothing.
+ * Every call on a GPU shares that buffer, so calls that overlap on one GPU
+ * (several streams, threads or processes' contexts in flight at once) race;
+ * calls in stream order do not.  Nothing in the buffer needs to start at zero:
+ * every partial sum read is written first by the same call.
+ * SAE_ERR_ARG (nothing launched) for n > SAE_PRED_NOALLOC_MAX_N and the
+ * conditions of sae_predict_sessions.
+ */
+#define SAE_PRED_NOALLOC_MAX_N 4096
+sae_status sae_predict_sessions_noalloc(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w,
+                                        float *logit, uint8_t *pred, sae_stream_t stream);
+
 /* Device realisation of the fp32 recipe's elementary functions (the ones
  * Eq. 1 and Eq. 2 are built from), element-wise, for checking it:
  *  fn = SAE_FN_LN    y = ln x    (x a positive normal float)

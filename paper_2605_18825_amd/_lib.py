@@ -97,6 +97,7 @@ SIGNATURES = {
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
     "sae_get_intervals": (_I32, [_P, _I32, _I32, _P, _I32, ctypes.POINTER(_I32), _P]),
     "sae_predict_sessions": (_I32, [_I32, _I32, _P, ctypes.POINTER(SaePredictor), _P, _P, _P, _P]),
+    "sae_predict_sessions_noalloc": (_I32, [_I32, _I32, _P, ctypes.POINTER(SaePredictor), _P, _P, _P]),
     "sae_select_stats": (_I32, [_P, _I32, _P, _P]),
     "sae_profile_enable": (_I32, [_P, _I32]),
     "sae_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),

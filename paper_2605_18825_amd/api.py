@@ -248,5 +248,19 @@ def sae_predict_sessions(h_bf16, w, work, logit, pred=None, stream=None):
                                                   _ptr(pred), _stream(stream)))
 
 
+PRED_NOALLOC_MAX_N = 4096
+
+
+def sae_predict_sessions_noalloc(h_bf16, w, logit, pred=None, stream=None):
+    """As sae_predict_sessions, with the library's own per-GPU buffer in place
+    of `work` (n <= PRED_NOALLOC_MAX_N); allocates nothing."""
+    n, d = h_bf16.shape
+    p = SaePredictor()
+    for name in ("w1", "b1", "w2", "b2", "w3", "b3"):
+        setattr(p, name, _ptr(w[name]).value)
+    _check(None, _lib.load().sae_predict_sessions_noalloc(n, d, _ptr(h_bf16), ctypes.byref(p), _ptr(logit),
+                                                          _ptr(pred), _stream(stream)))
+
+
 def status_names(bits):
     return [v for k, v in ST_NAMES.items() if bits & k]

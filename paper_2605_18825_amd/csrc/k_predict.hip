@@ -20,6 +20,8 @@
 // and fed to the four 16-column blocks, every load of a wave issued at once,
 // the eighths summed in a fixed order), then the 64-term layer 3 by shuffles.  Layer 1's four k
 // slices are added here, in slice order, before b1 and the ReLU.
+#include <mutex>
+
 #include "sae_internal.h"
 
 namespace {
@@ -287,6 +289,36 @@ k_pred_l23(int n, const float *part, const float *b1, const float *w2, const flo
 }
 
 }  // namespace
+
+// Layer 1's partial sums for sae_predict_sessions_noalloc: device memory of the
+// library's own (each GPU holds its own copy of the array until the process
+// ends).  Host code never passes `scratch` itself to a kernel (on the host it
+// is only a stand-in for the symbol); it passes the device address that
+// hipGetSymbolAddress returned for the current device.
+static __device__ __align__(256) float scratch[(size_t)KSPLIT * SAE_PRED_NOALLOC_MAX_N * SAE_PRED_H1];
+
+// The device address of `scratch` on the current device, looked up with that
+// device current on its first use and kept per device.
+hipError_t predict_scratch(float **out)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = static_cast<float *>(addr[dev]);
+    return hipSuccess;
+}
 
 hipError_t launch_predict(int n, int d, const uint16_t *h, const uint16_t *w1, const float *b1, const float *w2,
                           const float *b2, const float *w3, const float *b3, float *work, float *logit,

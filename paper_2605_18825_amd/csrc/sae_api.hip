@@ -386,19 +386,44 @@ sae_status sae_get_intervals(sae_ctx *c, int32_t inst, int32_t queue, int32_t *o
     return SAE_OK;
 }
 
-sae_status sae_predict_sessions(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, float *work,
-                                float *logit, uint8_t *pred, sae_stream_t stream)
+// Argument checks shared by both predictor entry points (work may be NULL for
+// the one that brings its own buffer).
+static sae_status predict_args(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, const float *work,
+                               bool need_work, const float *logit)
 {
     if (n < 0) return fail(nullptr, SAE_ERR_ARG, "n must be >= 0");
     if (d < 256 || d > 16384 || d % 256 != 0)
         return fail(nullptr, SAE_ERR_ARG, "d must be a multiple of 256 in 256..16384");
     if (n == 0) return SAE_OK;
-    if (!h || !w || !w->w1 || !w->b1 || !w->w2 || !w->b2 || !w->w3 || !w->b3 || !work || !logit)
+    if (!h || !w || !w->w1 || !w->b1 || !w->w2 || !w->b2 || !w->w3 || !w->b3 || (need_work && !work) || !logit)
         return fail(nullptr, SAE_ERR_ARG, "h, every weight, work and logit must be non-NULL");
-    if (!aligned(h, 16) || !aligned(w->w1, 16) || !aligned(w->w2, 16) || !aligned(work, 16))
+    if (!aligned(h, 16) || !aligned(w->w1, 16) || !aligned(w->w2, 16) || (need_work && !aligned(work, 16)))
         return fail(nullptr, SAE_ERR_ARG, "h, w1, w2 and work must be 16-byte aligned");
+    return SAE_OK;
+}
+
+sae_status sae_predict_sessions(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w, float *work,
+                                float *logit, uint8_t *pred, sae_stream_t stream)
+{
+    sae_status st = predict_args(n, d, h, w, work, true, logit);
+    if (st != SAE_OK || n == 0) return st;
     hipError_t e = launch_predict(n, d, h, w->w1, w->b1, w->w2, w->b2, w->w3, w->b3, work, logit, pred, S(stream));
     if (e != hipSuccess) return hip_fail(nullptr, e, "sae_predict_sessions");
+    return SAE_OK;
+}
+
+sae_status sae_predict_sessions_noalloc(int32_t n, int32_t d, const uint16_t *h, const sae_predictor *w,
+                                        float *logit, uint8_t *pred, sae_stream_t stream)
+{
+    if (n > SAE_PRED_NOALLOC_MAX_N)
+        return fail(nullptr, SAE_ERR_ARG, "n exceeds SAE_PRED_NOALLOC_MAX_N (4096) rows");
+    sae_status st = predict_args(n, d, h, w, nullptr, false, logit);
+    if (st != SAE_OK || n == 0) return st;
+    float *work = nullptr;
+    hipError_t e = predict_scratch(&work);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "sae_predict_sessions_noalloc: library buffer");
+    e = launch_predict(n, d, h, w->w1, w->b1, w->w2, w->b2, w->w3, w->b3, work, logit, pred, S(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "sae_predict_sessions_noalloc");
     return SAE_OK;
 }
 

@@ -562,6 +562,8 @@ hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t 
                               hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s, int set);
+// Device address of the no-allocation predictor's buffer on the current device.
+hipError_t predict_scratch(float **out);
 hipError_t launch_predict(int n, int d, const uint16_t *h, const uint16_t *w1, const float *b1, const float *w2,
                           const float *b2, const float *w3, const float *b3, float *work, float *logit,
                           uint8_t *pred, hipStream_t s);
