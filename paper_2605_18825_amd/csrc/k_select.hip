@@ -1276,12 +1276,13 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
 //    ones inside by bucket and write the part within the first need_q
 //    positions (the evict-first queue's list also fills the decision's first
 //    positions, Algorithm 1 stage 1);
-//  * "union" workgroups, FIN_GU buckets each of the reference queue (the
-//    queue other than evict-first with the smallest bound): the decision's
-//    stage 2 is the first k - n1 of all other queues' blocks by (P, id), and
-//    every one of them is a candidate of its queue (each lies among its own
-//    queue's first k), so ranking the union of those candidates up to the
-//    reference bound gives it exactly;
+//  * "union" workgroups: the decision's stage 2 is the first k - n1 of all
+//    other queues' blocks by (P, id), and every one of them is a candidate of
+//    its queue (each lies among its own queue's first k), so ranking the
+//    union of those candidates up to the reference bound (the smallest bound
+//    among those queues) gives it exactly; the union's ranges are cut at the
+//    bucket ends of all those queues merged, so that each holds about the
+//    same number of candidates however the queues' keys interleave;
 //  * one finisher workgroup writes the list sizes and the decision size and
 //    updates the eviction count.  If any queue's candidates are incomplete,
 //    every other workgroup stops and the finisher alone computes everything
@@ -1289,14 +1290,16 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan(DevCtx c, SelectArgs a)
 #define FIN_THREADS 1024
 #define FIN_G 16                             // buckets per group workgroup
 #define FIN_GPQ (SAE_NBUCKET / FIN_G)        // group workgroups per queue
-#define FIN_GU 4                             // reference-queue buckets per union workgroup
-#define FIN_NU (SAE_NBUCKET / FIN_GU)        // union workgroups
+#define FIN_NU 64                            // union workgroups
 #define FIN_GCAP 4096                        // candidates a workgroup ranks at once
 #define FIN_U (SAE_LCAP / FIN_THREADS)       // candidates per thread of one streamed queue
 #define FIN_STACK 80                         // pending ranges (a range splits into two)
 #define FIN_SB 64                            // sub-bins per bucket in the ranking
+#define FIN_T 64                             // largest segment ranked by comparison alone
+#define FIN_RSTACK (FIN_GCAP / FIN_T)        // pending segments (disjoint, each above FIN_T)
+#define FIN_MAXREF 48                        // refinements of one range before comparison takes over
 static_assert(SAE_STRIPES == SAE_WAVE, "one stripe per lane");
-static_assert(FIN_G <= 16 && FIN_GU <= FIN_G, "bucket indices fit the bucket histogram");
+static_assert(FIN_G <= 16, "bucket indices fit the bucket histogram");
 
 struct FinInfo {
     uint32_t C[SAE_MAX_QUEUES];     // candidates held (stripes, then the overflow list)
@@ -1384,9 +1387,15 @@ __device__ __forceinline__ uint32_t fin_slot(const uint32_t *spre, uint32_t i)
 // counting sort by sub-bin (FIN_SB equal value ranges between a bucket's
 // smallest and largest value; monotone in the value, so the sub-bins are
 // ordered), and inside its sub-bin (a handful of candidates) each one's rank
-// by comparison.  A range holding more than fits is split in two (by its
-// bucket ends, or by value once it has a single bucket) and the halves are
-// ranked in order.  All threads call; `ends` is in LDS.
+// by comparison.  Equal keys of many blocks (blocks added together share
+// last_access, so a queue's keys repeat in clusters of hundreds) put whole
+// clusters into one sub-bin; a sub-bin of more than FIN_T candidates is
+// therefore refined by a counting sort of its own over FIN_THREADS sub-bins
+// between its smallest and largest value (each refinement puts those two in
+// different sub-bins, so segments shrink), until every segment is small.  A
+// range holding more than fits is split in two (by its bucket ends, or by
+// value once it has a single bucket) and the halves are ranked in order.  All
+// threads call; `ends` is in LDS.
 template <typename Out>
 __device__ void fin_rank(const DevCtx &c, int inst, const FinInfo &f, uint32_t src, const unsigned long long *ends,
                          FinRange first, uint32_t need, unsigned long long *st1, unsigned long long *st2,
@@ -1406,6 +1415,11 @@ __device__ void fin_rank(const DevCtx &c, int inst, const FinInfo &f, uint32_t s
     __shared__ unsigned long long bmin[16], bmax[16];
     __shared__ float sbmul[16];
     __shared__ FinRange cur;
+    __shared__ uint32_t segbits[FIN_GCAP / 32];  // bit p: a segment starts at position p
+    __shared__ uint2 rstack[FIN_RSTACK];
+    __shared__ int32_t rsp_s;
+    __shared__ uint32_t rlo_s, rhi_s;
+    __shared__ unsigned long long rmin_s, rmax_s;
     if (tid == 0) {
         stack[0] = first;
         sp_s = 1;
@@ -1564,19 +1578,105 @@ __device__ void fin_rank(const DevCtx &c, int inst, const FinInfo &f, uint32_t s
 #pragma unroll
             for (int u = 0; u < PER; ++u)
                 if (k4[u] >= 0) st2[soff[k4[u]] + atomicAdd(&hist[k4[u]], 1u)] = e4[u];
+            if (tid < FIN_GCAP / 32) segbits[tid] = 0;
+            if (tid == 0) rsp_s = 0;
             lds_barrier();
-#pragma unroll
-            for (int u = 0; u < PER; ++u) {
-                if (k4[u] < 0) continue;
-                const uint32_t lo = soff[k4[u]], hi = soff[k4[u] + 1];
+            // segments: the non-empty sub-bins; the large ones wait for refinement
+            {
+                const uint32_t s0 = soff[tid], cnt = soff[tid + 1] - s0;
+                if (cnt) atomicOr(&segbits[s0 >> 5], 1u << (s0 & 31));
+                if (cnt > FIN_T) rstack[atomicAdd(&rsp_s, 1)] = make_uint2(s0, s0 + cnt);
+            }
+            lds_barrier();
+            // every thread reads the stack size between two barriers, before
+            // thread 0 pops, so all of them take the same branch
+            bool more = rsp_s > 0;
+            for (int nref = 0; more && nref < FIN_MAXREF; ++nref) {  // uniform
+                lds_barrier();
+                if (tid == 0) {
+                    const uint2 sg = rstack[--rsp_s];
+                    rlo_s = sg.x;
+                    rhi_s = sg.y;
+                    rmin_s = ~0ull;
+                    rmax_s = 0;
+                }
+                hist[tid] = 0;
+                lds_barrier();
+                const uint32_t lo = rlo_s, hi = rhi_s;
+                unsigned long long mn = ~0ull, mx = 0;
+                for (uint32_t p = lo + tid; p < hi; p += FIN_THREADS) {
+                    const unsigned long long e = st2[p];
+                    mn = e < mn ? e : mn;
+                    mx = e > mx ? e : mx;
+                }
+                for (int o = 32; o > 0; o >>= 1) {
+                    const unsigned long long a2 = shfl_xor_u64(mn, o), b2 = shfl_xor_u64(mx, o);
+                    mn = a2 < mn ? a2 : mn;
+                    mx = b2 > mx ? b2 : mx;
+                }
+                if (lane == 0 && lo + (uint32_t)wave * SAE_WAVE < hi) {
+                    atomicMin(&rmin_s, mn);
+                    atomicMax(&rmax_s, mx);
+                }
+                lds_barrier();
+                const unsigned long long smn = rmin_s;
+                const float mul = (float)FIN_THREADS / ((float)(rmax_s - smn) + 1.0f);
+                auto sub = [&](unsigned long long e) {
+                    const int x = (int)((float)(e - smn) * mul);
+                    return x < FIN_THREADS - 1 ? x : FIN_THREADS - 1;
+                };
+                for (uint32_t p = lo + tid; p < hi; p += FIN_THREADS) atomicAdd(&hist[sub(st2[p])], 1u);
+                lds_barrier();
+                const uint32_t hv = hist[tid];
+                const uint32_t hinc = wave_incl_scan(hv);
+                if (lane == SAE_WAVE - 1) wsum[wave] = hinc;
+                lds_barrier();
+                uint32_t hpre = 0;
+                for (int w = 0; w < wave; ++w) hpre += wsum[w];
+                soff[tid] = lo + hpre + hinc - hv;
+                hist[tid] = 0;
+                lds_barrier();
+                for (uint32_t p = lo + tid; p < hi; p += FIN_THREADS) {
+                    const unsigned long long e = st2[p];
+                    const int x = sub(e);
+                    st1[soff[x] + atomicAdd(&hist[x], 1u)] = e;
+                }
+                lds_barrier();
+                for (uint32_t p = lo + tid; p < hi; p += FIN_THREADS) st2[p] = st1[p];
+                if (hv) {
+                    const uint32_t s0 = soff[tid];
+                    atomicOr(&segbits[s0 >> 5], 1u << (s0 & 31));
+                    if (hv > FIN_T) rstack[atomicAdd(&rsp_s, 1)] = make_uint2(s0, s0 + hv);
+                }
+                lds_barrier();
+                more = rsp_s > 0;
+            }
+            // rank inside the final segments by comparison
+            for (uint32_t p = tid; p < n; p += FIN_THREADS) {
+                const unsigned long long e = st2[p];
+                uint32_t lo = p, hi = p + 1;
+                {  // the segment's first position: the last set bit at or below p
+                    int w = (int)(p >> 5);
+                    uint32_t bits = segbits[w] & (0xFFFFFFFFu >> (31 - (p & 31)));
+                    while (!bits && w > 0) bits = segbits[--w];
+                    lo = bits ? (uint32_t)(w * 32 + 31 - __clz(bits)) : 0u;
+                }
+                if (bl + lo >= need) continue;  // the whole segment lies beyond the first `need`
+                {  // its end: the next set bit above p, or n
+                    int w = (int)(p >> 5);
+                    uint32_t bits = (p & 31) == 31 ? 0u : (segbits[w] & (0xFFFFFFFFu << ((p & 31) + 1)));
+                    while (!bits && w + 1 < FIN_GCAP / 32 && (uint32_t)(w + 1) * 32 < n) bits = segbits[++w];
+                    hi = bits ? (uint32_t)(w * 32 + __ffs(bits) - 1) : n;
+                    hi = hi < n ? hi : n;
+                }
                 uint32_t rk = 0, i = lo;
                 for (; i + 4 <= hi; i += 4) {
 #pragma unroll
-                    for (int t = 0; t < 4; ++t) rk += (st2[i + t] < e4[u]) ? 1u : 0u;
+                    for (int t = 0; t < 4; ++t) rk += (st2[i + t] < e) ? 1u : 0u;
                 }
-                for (; i < hi; ++i) rk += (st2[i] < e4[u]) ? 1u : 0u;
+                for (; i < hi; ++i) rk += (st2[i] < e) ? 1u : 0u;
                 const uint32_t rank = bl + lo + rk;
-                if (rank < need) out(rank, e4[u]);
+                if (rank < need) out(rank, e);
             }
         }
         // thread 0 alone changes the stack, so it decides whether to go on
@@ -1731,6 +1831,17 @@ __global__ void __launch_bounds__(FIN_THREADS) k_final(DevCtx c, SelectArgs a, i
         const unsigned long long *spl = c.split + ((long long)inst * Q + unit / FIN_GPQ) * SAE_NBUCKET;
         ends[tid] = (b0 + tid - 1 >= 0) ? spl[b0 + tid - 1] : 0ull;
     }
+    // a union workgroup's: every queue's bucket ends (2 per thread, Q <= 8)
+    static_assert(SAE_MAX_QUEUES * SAE_NBUCKET == 2 * FIN_THREADS, "two bucket ends per thread");
+    unsigned long long uend[2] = {0ull, 0ull};
+    if (unit >= n_group && unit < n_group + FIN_NU) {
+        const unsigned long long *spl = c.split + (long long)inst * Q * SAE_NBUCKET;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i = tid + h * FIN_THREADS;
+            uend[h] = (i < Q * SAE_NBUCKET) ? spl[i] : 0ull;
+        }
+    }
     fin_info(c, a, inst, kq, f);
     unsigned long long *st1 = fdyn, *st2 = fdyn + FIN_GCAP;
     int32_t *dec = a.decision + (long long)inst * c.max_k;
@@ -1747,31 +1858,98 @@ __global__ void __launch_bounds__(FIN_THREADS) k_final(DevCtx c, SelectArgs a, i
         }
         lds_barrier();
         const int rq = group ? q : ref_s;
-        const int per = group ? FIN_G : FIN_GU;
-        const int g = group ? unit % FIN_GPQ : unit - n_group;
         const uint32_t need = group ? f.need[q] : (uint32_t)f.rest;
         if (rq < 0 || need == 0) return;  // uniform
-        const int nb = f.nb[rq];
-        const int b0 = g * per;
-        if (b0 >= nb) return;  // uniform
-        const int b1 = b0 + per < nb ? b0 + per : nb;
-        if (!group) {  // the reference queue's ends (ends[0]: the lower end)
-            const unsigned long long *spl = c.split + ((long long)inst * Q + rq) * SAE_NBUCKET;
-            if (tid <= b1 - b0) ends[tid] = (b0 + tid - 1 >= 0) ? spl[b0 + tid - 1] : 0ull;
-            lds_barrier();
-        }
-        FinRange first;
-        first.has_lo = b0 > 0;
-        first.lo = ends[0];
-        first.hi = ends[b1 - b0];
-        first.e0 = 1;
-        first.e1 = 1 + (b1 - b0);
         uint32_t src = 0;
         if (group) {
             src = 1u << q;
         } else {
             for (int qq = 0; qq < Q; ++qq)
                 if (qq != c.ef_queue && f.need[qq] > 0) src |= 1u << qq;
+        }
+        FinRange first;
+        if (group) {
+            const int nb = f.nb[q];
+            const int b0 = (unit % FIN_GPQ) * FIN_G;
+            if (b0 >= nb) return;  // uniform
+            const int b1 = b0 + FIN_G < nb ? b0 + FIN_G : nb;
+            first.has_lo = b0 > 0;
+            first.lo = ends[0];
+            first.hi = ends[b1 - b0];
+            first.e0 = 1;
+            first.e1 = 1 + (b1 - b0);
+        } else {
+            // The union's ranges follow the bucket ends of all its queues
+            // merged, up to the reference bound: a range between consecutive
+            // merged ends holds at most one bucket's worth of each queue,
+            // wherever each queue's keys lie.  Union workgroup g takes
+            // consecutive merged ends g S .. g S + S - 1, S = ceil(M / FIN_NU).
+            unsigned long long *mend = st1, *mer = st2;  // [queue][SAE_NBUCKET], merged
+            __shared__ uint32_t mcnt[SAE_MAX_QUEUES], mtot;
+            const unsigned long long rb = f.thr[rq];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = tid + h * FIN_THREADS, qq = i / SAE_NBUCKET, j = i % SAE_NBUCKET;
+                const bool ok = qq < Q && ((src >> qq) & 1u) && j < f.nb[qq];
+                mend[i] = ok ? uend[h] : ~0ull;  // ascending per queue, unused slots last
+            }
+            lds_barrier();
+            if (tid < SAE_MAX_QUEUES) {  // each queue's ends at or below the reference bound
+                const int nq = (tid < Q && ((src >> tid) & 1u)) ? f.nb[tid] : 0;
+                const unsigned long long *eq = mend + tid * SAE_NBUCKET;
+                int l = 0;
+#pragma unroll
+                for (int st = SAE_NBUCKET; st > 0; st >>= 1)
+                    if (l + st <= nq && eq[l + st - 1] <= rb) l += st;
+                mcnt[tid] = (uint32_t)l;
+            }
+            lds_barrier();
+            if (tid == 0) {
+                uint32_t m = 0;
+                for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) m += mcnt[qq];
+                mtot = m;
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = tid + h * FIN_THREADS, qq = i / SAE_NBUCKET, j = i % SAE_NBUCKET;
+                if ((uint32_t)j < mcnt[qq]) {
+                    // rank in the merge, equal ends ordered by queue
+                    const unsigned long long v = mend[i];
+                    uint32_t r = (uint32_t)j;
+                    for (int q2 = 0; q2 < SAE_MAX_QUEUES; ++q2) {
+                        if (q2 == qq || mcnt[q2] == 0) continue;
+                        const unsigned long long *e2 = mend + q2 * SAE_NBUCKET;
+                        const int n2 = (int)mcnt[q2];
+                        int l = 0;
+#pragma unroll
+                        for (int st = SAE_NBUCKET; st > 0; st >>= 1)
+                            if (l + st <= n2 && (q2 < qq ? e2[l + st - 1] <= v : e2[l + st - 1] < v)) l += st;
+                        r += (uint32_t)l;
+                    }
+                    mer[r] = v;
+                }
+            }
+            lds_barrier();
+            const uint32_t M = mtot;
+            const uint32_t S = (M + FIN_NU - 1) / FIN_NU;
+            const uint32_t g = (uint32_t)(unit - n_group);
+            const uint32_t r0 = g * S;
+            if (r0 >= M) return;  // uniform
+            const uint32_t r1 = r0 + S < M ? r0 + S : M;
+            const uint32_t cnt = r1 - r0;
+            const uint32_t stride = (cnt + FIN_G - 1) / FIN_G;
+            const int nbk = (int)((cnt + stride - 1) / stride);
+            if (tid == 0) ends[0] = r0 > 0 ? mer[r0 - 1] : 0ull;
+            if (tid < nbk) {
+                const uint32_t pos = r0 + (uint32_t)(tid + 1) * stride - 1;
+                ends[1 + tid] = mer[pos < r1 ? pos : r1 - 1];
+            }
+            lds_barrier();
+            first.has_lo = r0 > 0;
+            first.lo = ends[0];
+            first.hi = ends[nbk];
+            first.e0 = 1;
+            first.e1 = 1 + nbk;
         }
         const long long ob = ((long long)inst * Q + q) * c.max_k;
         const bool is_ef = group && q == c.ef_queue;

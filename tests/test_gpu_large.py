@@ -85,3 +85,24 @@ def test_large_match_commit_feedback(large):
     say("large: second decision")
     p.select(pool["now"] + 30, cfg["k"], commit=True)
     p.check_counters()
+
+
+def test_large_equal_key_clusters():
+    """Blocks added together share last_access, so their keys repeat: here
+    last_access takes 400 values, which makes clusters of about 2,000 equal
+    keys per (queue, type), and every queue's candidates hold whole clusters.
+    Every list and the decision equal the oracle's on the pool-scan engine,
+    with no fallback."""
+    cfg = synth.pool_config("large")
+    pool = synth.make_pool(cfg, seed=1234)
+    rng = np.random.default_rng(9)
+    la = pool["now"] - 1000 * rng.integers(1, 401, pool["n_blocks"])
+    pool["last_access"] = la.astype(pool["last_access"].dtype)
+    p = Pair(cfg["kinds"], pool, cfg["k"], mu=cfg["mu"], sigma=cfg["sigma"], K=cfg["k"])
+    try:
+        for now, k in ((pool["now"], cfg["k"]), (pool["now"] + 500, 1000), (pool["now"] + 900, 4000)):
+            say("large clusters: score_select k=%d" % k)
+            p.select(now, k, api.SS_ENGINE_SCAN)
+            assert not p.status()
+    finally:
+        p.close()
