@@ -8,7 +8,9 @@ eviction decisions.  No policy step runs here.
 Host arrays go to the device through pinned staging buffers with
 asynchronous copies, and results come back the same way with one stream
 synchronisation per call that returns them, so a replay step costs few
-host-device round trips.
+host-device round trips.  Everything runs on the stream that was current when
+the backend was made (library calls name it; torch's copies use the current
+stream), so the caller keeps that stream current.
 """
 import numpy as np
 import torch
@@ -18,30 +20,35 @@ from .pool import DevicePool, SelectBuffers
 
 
 class _Staging:
-    """Pinned host buffers and device buffers, reused call after call.
+    """Pinned host buffers and device buffers, reused call after call, on one
+    stream.
 
     put(name, array) copies a host array into the pinned buffer `name` and
-    from there, asynchronously on the current stream, into the device buffer
-    `name`; it returns the device view.  Before a pinned buffer is written
+    from there, asynchronously on the stream, into the device buffer `name`;
+    it returns the device view.  Before a pinned input buffer is written
     again, the copy that last read it must have finished (its event); the
-    device buffer needs no such wait, since everything runs on one stream."""
+    device buffer needs no such wait, since everything runs on one stream.
+    get(name, t) starts the copy of t into a pinned output buffer; its caller
+    synchronises the stream before reading it and before the next get."""
 
-    def __init__(self):
+    def __init__(self, stream):
+        self.stream = stream
         self.host = {}
         self.dev = {}
         self.ev = {}
 
-    def _bufs(self, name, nbytes):
+    def _bufs(self, name, nbytes, device=True):
         h = self.host.get(name)
         if h is None or h.numel() < nbytes:
             n = max(nbytes, 2 * (h.numel() if h is not None else 0), 4096)
             if name in self.ev:
                 self.ev[name].synchronize()
             self.host[name] = torch.empty(n, dtype=torch.uint8, pin_memory=True)
-            self.dev[name] = torch.empty(n, dtype=torch.uint8, device="cuda")
-            self.ev[name] = torch.cuda.Event()
-            self.ev[name].record()
-        return self.host[name], self.dev[name]
+            if device:
+                self.dev[name] = torch.empty(n, dtype=torch.uint8, device="cuda")
+                self.ev[name] = torch.cuda.Event()
+                self.ev[name].record(self.stream)
+        return self.host[name], self.dev.get(name)
 
     def put(self, name, a, dtype):
         a = np.ascontiguousarray(a)
@@ -50,7 +57,7 @@ class _Staging:
         self.ev[name].synchronize()
         h.numpy()[:nb] = a.view(np.uint8).ravel()
         d[:nb].copy_(h[:nb], non_blocking=True)
-        self.ev[name].record()
+        self.ev[name].record(self.stream)
         return d[:nb].view(dtype).view(a.shape) if nb else d[:0].view(dtype)
 
     def get(self, name, t):
@@ -58,10 +65,8 @@ class _Staging:
         numpy view is valid after the stream has been synchronised."""
         t = t.contiguous()
         nb = t.numel() * t.element_size()
-        h, _ = self._bufs("out_" + name, max(nb, 1))
-        self.ev["out_" + name].synchronize()
+        h, _ = self._bufs("out_" + name, max(nb, 1), device=False)
         h[:nb].copy_(t.view(-1).view(torch.uint8), non_blocking=True)
-        self.ev["out_" + name].record()
         return h[:nb].numpy()
 
 
@@ -81,8 +86,8 @@ class DeviceBackend:
         api.sae_set_params(self.ctx, -1, api.make_params(self.Q, w=w, alpha=alpha, mu=mu, sigma=sigma, gamma=gamma,
                                                          eta=eta, temperature=T, beta=beta, K=K, learn=learn))
         self.out = SelectBuffers(n_inst, self.Q, max_k)
-        self.st = _Staging()
         self.stream = torch.cuda.current_stream()
+        self.st = _Staging(self.stream)
         self.select_calls = 0
 
     def close(self):
@@ -104,7 +109,7 @@ class DeviceBackend:
         ml = torch.empty(n, dtype=torch.int32, device="cuda")
         mid = torch.empty((n, L), dtype=torch.int32, device="cuda")
         flags = api.PM_TOUCH | api.PM_STATS | (api.PM_INTERVALS if self.intervals else 0)
-        api.sae_prefix_match(self.ctx, hd, ld, now, flags, ml, matched_ids=mid, inst=idv)
+        api.sae_prefix_match(self.ctx, hd, ld, now, flags, ml, matched_ids=mid, inst=idv, stream=self.stream)
         mlh = self.st.get("pm_ml", ml)
         midh = self.st.get("pm_mid", mid)
         self.stream.synchronize()
@@ -116,15 +121,15 @@ class DeviceBackend:
         if len(ids):
             both = np.stack([np.asarray(inst, np.int32), np.asarray(ids, np.int32)])
             d = self.st.put("ref%d" % (delta > 0), both, torch.int32)
-            api.sae_ref_blocks(self.ctx, d[1], delta, inst=d[0])
+            api.sae_ref_blocks(self.ctx, d[1], delta, inst=d[0], stream=self.stream)
 
     def evict(self, now, k):
         k = np.asarray(k, np.int32)
         if self.n_inst == 1:  # one cache: k goes by value
-            self.out.run(self.ctx, now, int(k[0]), self.select_flags)
+            self.out.run(self.ctx, now, int(k[0]), self.select_flags, stream=self.stream)
         else:
             kd = self.st.put("k", k, torch.int32)
-            self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd)
+            self.out.run(self.ctx, now, self.max_k, self.select_flags, k_per_inst=kd, stream=self.stream)
         self.select_calls += 1
         small = self.n_inst * self.max_k <= 16384
         cnt = self.st.get("cnt", self.out.decision_count)
@@ -161,14 +166,14 @@ class DeviceBackend:
         counts = cb[:, :5].contiguous()
         hints = cb[:, 5].contiguous()
         tau = torch.empty(n, dtype=torch.uint8, device="cuda")
-        api.sae_block_type(counts, tau)
+        api.sae_block_type(counts, tau, stream=self.stream)
         # meta before Classify: type, num_tokens - 1 = 15 (the queue bits are Classify's)
         meta = ((tau.to(torch.int32) << 3) | (15 << 9)).to(torch.int16)
-        api.sae_classify_blocks(self.ctx, hints, meta, self.roles)
-        api.sae_insert_blocks(self.ctx, ci[1], hd, ci[2], ci[3], meta, ci[4], inst=ci[0])
+        api.sae_classify_blocks(self.ctx, hints, meta, self.roles, stream=self.stream)
+        api.sae_insert_blocks(self.ctx, ci[1], hd, ci[2], ci[3], meta, ci[4], inst=ci[0], stream=self.stream)
 
     def feedback(self):
-        api.sae_feedback_update(self.ctx, 0)
+        api.sae_feedback_update(self.ctx, 0, stream=self.stream)
 
     # -------------------------------------------------------------- read-back
     def counters(self, i):

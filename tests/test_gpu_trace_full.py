@@ -15,7 +15,8 @@ bits of the learned parameters.  The HIP replay computes the same digests; the
 first step whose digest differs is named, and every checkpoint must be equal.
 The four replays run side by side, each in a process of its own
 (tests/trace_full_run.py), since the host side of a replay step is what takes
-the time.
+the time: about 8 minutes in all on one MI355X (each balanced replay makes
+about 7.6 million eviction decisions, one host round trip each).
 """
 import json
 import os
@@ -32,7 +33,7 @@ from harness import say  # noqa: E402
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 RUNS = ["balanced_alg23", "balanced_all", "sweep_fixed", "sweep_learned"]
-LIMIT_S = 600
+LIMIT_S = 900
 
 
 def test_full_length_replays():
