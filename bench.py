@@ -51,10 +51,10 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per launch of the pass's kernels from rocprofv3 counters, if
+def measured_traffic(name="score_select_large_pool_traffic.json"):
+    """HBM bytes per launch of a pass's kernels from rocprofv3 counters, if
     the committed measurement was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", "score_select_large_pool_traffic.json")
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -331,8 +331,11 @@ def leg_sweep_batched(api, DevicePool, SelectBuffers, stream, with_cpu):
     alg = BYTES_PER_BLOCK * n_inst * N
     res = dict(workload="256 caches x 65,536 blocks, 4 queues, k=256 per cache, batched engine (one workgroup "
                         "per cache)", gpu_decision_us=us, gpu_blocks_per_s=n_inst * N / (us * 1e-6),
-               roofline={"bound": "hbm", "achieved": alg / (us * 1e-6) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, "bytes_alg": alg})
+               roofline={"kernel": "k_batched", "bound": "hbm", "achieved": alg / (us * 1e-6) / 1e9,
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                         "bytes_alg": alg})
+    tr = measured_traffic("k_batched_sweep_traffic.json")
+    res["roofline"]["traffic"] = tr.get("bytes_per_launch") if tr else None
     if with_cpu:
         n_proc = min(16, cores())
         jobs = [(cfg, 1005, k)] * n_proc
@@ -397,6 +400,79 @@ def leg_sweep_comparison():
 
 
 # ---------------------------------------------------------------------------- main
+def predictor_leg(api, args, R, stream):
+    """Session predictor (Sec. 3.3) on 4,096 last-token hidden states of
+    d = 4,096, rotating over R batches (256 MB, beyond the last-level cache)."""
+    import numpy as np
+    import torch
+    from synth import predictor as SP
+    PN, PD = 4096, 4096
+    h0 = SP.hidden_states(PN, PD, 5).view(np.int16)
+    hbat = [torch.as_tensor(h0).cuda() for _ in range(R)]
+    wnp = SP.weights(PD, 6)
+    wp = {kk: torch.as_tensor(v.view(np.int16) if kk == "w1" else v).cuda() for kk, v in wnp.items()}
+    pwork = torch.empty((4, PN, 256), dtype=torch.float32, device="cuda")
+    plogit = torch.empty(PN, dtype=torch.float32, device="cuda")
+    ppred = torch.empty(PN, dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
+        with Timer(stream) as tp:
+            for i in range(args.steps):
+                api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
+    ms_pred = tp.ms / args.steps
+    pred_bytes = PN * PD * 2 + 256 * PD * 2 + PN * 5  # hidden states, W1, logits and predictions
+    pred_flops = 2.0 * PN * PD * 256 + 2.0 * PN * 256 * 64 + 2.0 * PN * 64
+    del hbat
+    return ms_pred, pred_bytes, pred_flops, PN, PD
+
+
+def calib_copy(mib):
+    """A plain device-to-device copy of `mib` MiB, 4 times: the known-size
+    kernel that HBM byte counters are scaled by."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return n * 4
+
+
+def extra_legs(v):
+    """JSON entries of the legs beside the headline, from main()'s measurements `v`."""
+    N, HBM_PEAK = v["N"], HBM_PEAK_GBS
+    ms_casc, ms_all, ms_ss, ss_steps, ss_per, dc_min = (v[x] for x in ("ms_casc", "ms_all", "ms_ss", "ss_steps",
+                                                                         "ss_per", "dc_min"))
+    ms_pred, pred_bytes, pred_flops, PN, PD = (v[x] for x in ("ms_pred", "pred_bytes", "pred_flops", "PN", "PD"))
+    return {
+        "score_select_cascade": {
+            "value": N / (ms_casc * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_casc,
+            "decision": "Algorithm 1 one victim at a time (SAE_SS_CASCADE)",
+        },
+        "all_learners": {
+            "value": N / (ms_all * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_all,
+            "step": "the same step with Algorithms 2, 3, 4 and the decay-power learner on "
+                    "(prefix match records reuse intervals)",
+        },
+        "steady_state": {
+            "value": N / (ms_ss * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_ss, "steps": ss_steps,
+            "last_decision_size": dc_min,
+            "note": "the step plus Add() of k fresh blocks into the freed slots (the pool stays full); %d steps "
+                    "per cache, so each cache's index is rebuilt from its deleted slots %d times and its "
+                    "recently-evicted table as often as its size calls for" % (ss_per, ss_per // 256),
+        },
+        "predictor": {
+            "value": PN / (ms_pred * 1e-3), "unit": "predictions/s", "ms_per_call": ms_pred,
+            "batch": PN, "d": PD,
+            "roofline": {"bound": "hbm", "achieved": pred_bytes / (ms_pred * 1e-3) / 1e9, "peak": HBM_PEAK,
+                         "unit": "GB/s", "frac": pred_bytes / (ms_pred * 1e-3) / 1e9 / HBM_PEAK,
+                         "mfma_tflops_bf16": pred_flops / (ms_pred * 1e-3) / 1e12, "mfma_peak_bf16": 2500.0},
+        },
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -407,6 +483,12 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the other configurations' legs")
     ap.add_argument("--no-sweep", action="store_true", help="skip the full-length fixed/learned sweep comparison")
+    ap.add_argument("--main-only", action="store_true",
+                    help="time only the full steps and the score+select pass (for profiler runs)")
+    ap.add_argument("--batched-only", action="store_true",
+                    help="time only the batched-sweep decision (for profiler runs)")
+    ap.add_argument("--predictor-only", action="store_true",
+                    help="time only the session predictor (for profiler runs)")
     ap.add_argument("--sweep-run", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed region, copy this many MiB device-to-device 4 times "
@@ -428,6 +510,22 @@ def main():
     from paper_2605_18825_amd.pool import DevicePool, SelectBuffers
 
     torch.cuda.set_device(0)
+    if args.predictor_only:
+        stream = torch.cuda.Stream()  # default priority
+        ms_pred, pred_bytes, pred_flops, PN, PD = predictor_leg(api, args, max(1, args.replicas), stream)
+        out = {"predictor": {"ms_per_call": ms_pred, "batch": PN, "d": PD, "bytes_alg": pred_bytes}}
+        if args.calib_copy_mib > 0:
+            out["calib_copy_bytes"] = calib_copy(args.calib_copy_mib)
+        print(json.dumps(out), flush=True)
+        return
+    if args.batched_only:
+        stream = torch.cuda.Stream()  # default priority
+        out = {"batched_sweep": leg_sweep_batched(api, DevicePool, SelectBuffers, stream, False)}
+        if args.calib_copy_mib > 0:
+            out["calib_copy_bytes"] = calib_copy(args.calib_copy_mib)
+        print(json.dumps(out), flush=True)
+        return
+    extra = not args.main_only
     cfg = synth.pool_config("large")
     pool = synth.make_pool(cfg)
     N, Q, k = pool["n_blocks"], len(cfg["kinds"]), cfg["k"]
@@ -502,78 +600,62 @@ def main():
         torch.cuda.synchronize()
         s1 = time.perf_counter()
         pass_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
-        # --- the same pass with a read-only prefix match on a second stream
-        def pair(i, sel=True, pm=True):
-            c = caches[i % R]
-            if sel:
-                c["out"].run(c["ctx"], c["now"], k, 0, stream=stream)
-            if pm:
-                api.sae_prefix_match(c["ctx"], d_reqs, d_lens, c["now"], 0, d_ml2, stream=stream_b)
+        if extra:
+            # --- the same pass with a read-only prefix match on a second stream
+            def pair(i, sel=True, pm=True):
+                c = caches[i % R]
+                if sel:
+                    c["out"].run(c["ctx"], c["now"], k, 0, stream=stream)
+                if pm:
+                    api.sae_prefix_match(c["ctx"], d_reqs, d_lens, c["now"], 0, d_ml2, stream=stream_b)
+            note("score+select alone: %.3f ms/pass" % pass_ms)
+            ms_pm_alone = timed_loop(lambda i: pair(i, sel=False), args.steps, args.warmup)
+            ms_pair = timed_loop(pair, args.steps, args.warmup)
+            # --- cascading decision (Algorithm 1 one victim at a time)
+            ms_casc = timed_loop(lambda i: caches[i % R]["out"].run(caches[i % R]["ctx"], caches[i % R]["now"], k,
+                                                                    api.SS_CASCADE, stream=stream), args.steps, args.warmup)
+            # --- every learner on: Algorithms 2, 3, 4 and the decay power, the prefix match recording reuse intervals
+            for c in caches:
+                api.sae_set_params(c["ctx"], -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k, learn=15),
+                                   stream=stream)
+            ms_all = timed_loop(step_all_learners, args.steps, args.warmup)
+            for c in caches:
+                api.sae_set_params(c["ctx"], -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k), stream=stream)
+            note("pair, cascade, all learners done")
+            # --- steady state: each step also inserts k fresh blocks into the slots its decision freed
+            # (Add(), so the pool stays full), over enough steps per cache that the index (rebuilt
+            # every 256 commits of k) and recently-evicted tables are rebuilt as in a long run
+            ss_per = 1040
+            ss_steps = R * ss_per
+            now0 = max(c["now"] for c in caches)
+            for c in caches:
+                c["now"] = now0
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(7)
+            ins_hash = torch.randint(1, 1 << 62, (ss_per, k), dtype=torch.int64, device="cuda", generator=gen)
+            ins_la = (now0 + 1000 * torch.arange(ss_per, dtype=torch.int32, device="cuda"))[:, None].expand(
+                ss_per, k).contiguous()
+            ins_meta = caches[0]["dp"].meta[:k].clone()  # queue, type and num_tokens of k pool blocks
+            ins_off = caches[0]["dp"].off[:k].clone()
+            ins_parent = torch.full((k,), -1, dtype=torch.int32, device="cuda")
+            torch.cuda.synchronize()
+
+            def step_insert(i):
+                c = caches[i % R]
+                n = i // R
+                step(i)
+                api.sae_insert_blocks(c["ctx"], c["out"].decision[0, :k], ins_hash[n], ins_parent, ins_la[n], ins_meta,
+                                      ins_off, stream=stream)
+                if (i + 1) % 2000 == 0:
+                    note("steady state: %d of %d steps issued" % (i + 1, ss_steps))
+
+            ms_ss = timed_loop(step_insert, ss_steps, 0)
+            dc_min = min(int(c["out"].decision_count[0]) for c in caches)
+    if extra:
+        note("steady state: %.3f ms/step over %d steps" % (ms_ss, ss_steps))
+        ms_pred, pred_bytes, pred_flops, PN, PD = predictor_leg(api, args, R, stream)
+    else:
         note("score+select alone: %.3f ms/pass" % pass_ms)
-        ms_pm_alone = timed_loop(lambda i: pair(i, sel=False), args.steps, args.warmup)
-        ms_pair = timed_loop(pair, args.steps, args.warmup)
-        # --- cascading decision (Algorithm 1 one victim at a time)
-        ms_casc = timed_loop(lambda i: caches[i % R]["out"].run(caches[i % R]["ctx"], caches[i % R]["now"], k,
-                                                                api.SS_CASCADE, stream=stream), args.steps, args.warmup)
-        # --- every learner on: Algorithms 2, 3, 4 and the decay power, the prefix match recording reuse intervals
-        for c in caches:
-            api.sae_set_params(c["ctx"], -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k, learn=15),
-                               stream=stream)
-        ms_all = timed_loop(step_all_learners, args.steps, args.warmup)
-        for c in caches:
-            api.sae_set_params(c["ctx"], -1, api.make_params(Q, mu=cfg["mu"], sigma=cfg["sigma"], K=k), stream=stream)
-        note("pair, cascade, all learners done")
-        # --- steady state: each step also inserts k fresh blocks into the slots its decision freed
-        # (Add(), so the pool stays full), over enough steps per cache that the index (rebuilt
-        # every 256 commits of k) and recently-evicted tables are rebuilt as in a long run
-        ss_per = 1040
-        ss_steps = R * ss_per
-        now0 = max(c["now"] for c in caches)
-        for c in caches:
-            c["now"] = now0
-        gen = torch.Generator(device="cuda")
-        gen.manual_seed(7)
-        ins_hash = torch.randint(1, 1 << 62, (ss_per, k), dtype=torch.int64, device="cuda", generator=gen)
-        ins_la = (now0 + 1000 * torch.arange(ss_per, dtype=torch.int32, device="cuda"))[:, None].expand(
-            ss_per, k).contiguous()
-        ins_meta = caches[0]["dp"].meta[:k].clone()  # queue, type and num_tokens of k pool blocks
-        ins_off = caches[0]["dp"].off[:k].clone()
-        ins_parent = torch.full((k,), -1, dtype=torch.int32, device="cuda")
-        torch.cuda.synchronize()
-
-        def step_insert(i):
-            c = caches[i % R]
-            n = i // R
-            step(i)
-            api.sae_insert_blocks(c["ctx"], c["out"].decision[0, :k], ins_hash[n], ins_parent, ins_la[n], ins_meta,
-                                  ins_off, stream=stream)
-            if (i + 1) % 2000 == 0:
-                note("steady state: %d of %d steps issued" % (i + 1, ss_steps))
-
-        ms_ss = timed_loop(step_insert, ss_steps, 0)
-        dc_min = min(int(c["out"].decision_count[0]) for c in caches)
-    note("steady state: %.3f ms/step over %d steps" % (ms_ss, ss_steps))
-    # --- session predictor (Sec. 3.3) on 4,096 last-token hidden states of
-    # d = 4,096, rotating over 8 batches (256 MB, beyond the last-level cache)
-    from synth import predictor as SP
-    PN, PD = 4096, 4096
-    h0 = SP.hidden_states(PN, PD, 5).view(np.int16)
-    hbat = [torch.as_tensor(h0).cuda() for _ in range(R)]
-    wnp = SP.weights(PD, 6)
-    wp = {kk: torch.as_tensor(v.view(np.int16) if kk == "w1" else v).cuda() for kk, v in wnp.items()}
-    pwork = torch.empty((4, PN, 256), dtype=torch.float32, device="cuda")
-    plogit = torch.empty(PN, dtype=torch.float32, device="cuda")
-    ppred = torch.empty(PN, dtype=torch.uint8, device="cuda")
-    with torch.cuda.stream(stream):
-        for i in range(args.warmup):
-            api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
-        with Timer(stream) as tp:
-            for i in range(args.steps):
-                api.sae_predict_sessions(hbat[i % R], wp, pwork, plogit, ppred, stream=stream)
-    ms_pred = tp.ms / args.steps
-    pred_bytes = PN * PD * 2 + 256 * PD * 2 + PN * 5  # hidden states, W1, logits and predictions
-    pred_flops = 2.0 * PN * PD * 256 + 2.0 * PN * 256 * 64 + 2.0 * PN * 64
-    del hbat
     st = 0
     for c in caches:
         st |= api.sae_poll_status(c["ctx"])
@@ -620,50 +702,23 @@ def main():
         "score_select": {
             "value": N / (ms_sel * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_sel, "ms_per_pass_events": pass_ms,
             "hbm_frac_at_10B_per_block": alg_bytes / (pass_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "with_concurrent_prefix_match": {
-                "ms_pair": ms_pair, "ms_prefix_match_alone": ms_pm_alone, "ms_score_select_alone": ms_sel,
-                "requests": int(len(lens)), "hashes_per_request": int(reqs.shape[1]),
-                "note": "read-only prefix match on a second stream of the same context",
-            },
-        },
-        "score_select_cascade": {
-            "value": N / (ms_casc * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_call": ms_casc,
-            "decision": "Algorithm 1 one victim at a time (SAE_SS_CASCADE)",
-        },
-        "all_learners": {
-            "value": N / (ms_all * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_all,
-            "step": "the same step with Algorithms 2, 3, 4 and the decay-power learner on "
-                    "(prefix match records reuse intervals)",
-        },
-        "steady_state": {
-            "value": N / (ms_ss * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": ms_ss, "steps": ss_steps,
-            "last_decision_size": dc_min,
-            "note": "the step plus Add() of k fresh blocks into the freed slots (the pool stays full); %d steps "
-                    "per cache, so each cache's index is rebuilt from its deleted slots %d times and its "
-                    "recently-evicted table as often as its size calls for" % (ss_per, ss_per // 256),
-        },
-        "predictor": {
-            "value": PN / (ms_pred * 1e-3), "unit": "predictions/s", "ms_per_call": ms_pred,
-            "batch": PN, "d": PD,
-            "roofline": {"bound": "hbm", "achieved": pred_bytes / (ms_pred * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
-                         "unit": "GB/s", "frac": pred_bytes / (ms_pred * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                         "mfma_tflops_bf16": pred_flops / (ms_pred * 1e-3) / 1e12, "mfma_peak_bf16": 2500.0},
         },
         "device_status": api.status_names(st),
     }
+    if extra:
+        line["score_select"]["with_concurrent_prefix_match"] = {
+            "ms_pair": ms_pair, "ms_prefix_match_alone": ms_pm_alone, "ms_score_select_alone": ms_sel,
+            "requests": int(len(lens)), "hashes_per_request": int(reqs.shape[1]),
+            "note": "read-only prefix match on a second stream of the same context",
+        }
+        line.update(extra_legs(locals()))
     for c in caches:
         api.sae_destroy(c["ctx"])
     del caches
     torch.cuda.synchronize()
     if args.calib_copy_mib > 0:
-        n = args.calib_copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(4):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        line["calib_copy_bytes"] = n * 4
-    if not args.no_configs:
+        line["calib_copy_bytes"] = calib_copy(args.calib_copy_mib)
+    if not args.no_configs and extra:
         line["configs"] = {}
         for name, fn in (("tiny", lambda: leg_tiny(api, DevicePool, SelectBuffers, stream, not args.no_cpu)),
                          ("mid", lambda: leg_mid(api, DevicePool, SelectBuffers, stream, not args.no_cpu)),

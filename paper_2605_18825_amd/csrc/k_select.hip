@@ -22,7 +22,7 @@
 #define SEL_THREADS 1024
 #define SAMPLE_WGS SAE_SAMPLE_WGS
 #define SAMPLE_CHUNK SAE_SAMPLE_CHUNK
-#define BATCH_IPT 64  // keys per thread in the batched engine (64 x 1024 = 65,536 blocks)
+#define BATCH_IPT 64  // blocks per thread of the batched engine (64 x 1024 = 65,536 blocks per instance)
 
 namespace {
 
@@ -308,6 +308,50 @@ __device__ void sort_lds(unsigned long long *a, int P)
     }
     if (src != a) {
         for (int i = tid; i < P; i += blockDim.x) a[i] = src[i];
+        lds_barrier();
+    }
+}
+
+// Sort of T / S independent segments of S (a power of two, 256 <= S) 64-bit
+// keys each, stored back to back in LDS at a[0..T), with a[T..2T) as scratch:
+// the runs of 256 sorted as in sort_lds, then merged pairwise inside each
+// segment (a pair never crosses a segment's end), 4 outputs per thread per
+// round.  All threads call.
+__device__ void sort_segments_lds(unsigned long long *a, int T, int S)
+{
+    const int tid = threadIdx.x;
+    const int wave = tid / SAE_WAVE;
+    const int nwaves = blockDim.x / SAE_WAVE;
+    for (int rI = wave; rI < T / 256; rI += nwaves) wave_sort256(a + rI * 256);
+    lds_barrier();
+    unsigned long long *src = a, *dst = a + T;
+    constexpr int E = 4;
+    for (int run = 256; run < S; run <<= 1) {
+        for (int o0 = tid * E; o0 < T; o0 += (int)blockDim.x * E) {
+            const int pair = o0 / (2 * run);
+            const int d = o0 - pair * 2 * run;
+            const unsigned long long *A = src + pair * 2 * run;
+            const unsigned long long *B = A + run;
+            int lo = d > run ? d - run : 0, hi = d < run ? d : run;
+            while (lo < hi) {  // split: i from A, d - i from B
+                const int mid = (lo + hi) >> 1;
+                if (A[mid] < B[d - mid - 1]) lo = mid + 1;
+                else hi = mid;
+            }
+            int i = lo, jb = d - lo;
+            unsigned long long *D = dst + pair * 2 * run + d;
+            for (int e = 0; e < E; ++e) {
+                const bool takeA = (jb >= run) || (i < run && A[i] < B[jb]);
+                D[e] = takeA ? A[i++] : B[jb++];
+            }
+        }
+        lds_barrier();
+        unsigned long long *t = src;
+        src = dst;
+        dst = t;
+    }
+    if (src != a) {
+        for (int i = tid; i < T; i += blockDim.x) a[i] = src[i];
         lds_barrier();
     }
 }
@@ -1991,114 +2035,285 @@ __global__ void __launch_bounds__(FIN_THREADS) k_final(DevCtx c, SelectArgs a, i
 }
 
 // ---------------------------------------------------------------------------
-// Batched engine: one workgroup per instance, keys held in registers.
-__global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a, int P)
+// Batched engine: one workgroup per instance (N <= 65,536 blocks).  Per
+// queue, composite e = key << 16 | id (48 bits, distinct).
+//  * The first pass reads the pool once, scores every evictable block (Eq.
+//    1-3) and caches its key and queue (5 B per block) for the later passes,
+//    counts each queue's evictable blocks and histograms the top digit of e;
+//    need = min(k, evictable).  A queue whose need is all of its blocks takes
+//    them all; otherwise the bin holding its need-th element gives a range
+//    [lo, hi) of e: every element below lo is selected, and `rem` more from
+//    inside the range.  When the range holds exactly `rem` elements, every
+//    element below hi is selected.
+//  * While the open ranges hold more elements than the candidate buffer, a
+//    pass over the cached keys histograms the next digit inside each range
+//    (equal keys spread on the id digits).
+//  * The collect pass appends every selected element below lo to its queue's
+//    list and every element inside the range to the candidate buffer; a
+//    candidate is selected when fewer than `rem` candidates of its queue are
+//    smaller, and goes straight to list position below + its rank.
+//  * Each queue's list (at most max_k elements) is sorted, written out, and
+//    the decision merged from the lists (Algorithm 1).
+#define BATCH_CAND 2048  // candidate elements beyond the largest lists in LDS
+struct BatchSel {
+    unsigned long long lo[SAE_MAX_QUEUES], hi[SAE_MAX_QUEUES];
+    uint32_t nev[SAE_MAX_QUEUES], need[SAE_MAX_QUEUES], rem[SAE_MAX_QUEUES], remv[SAE_MAX_QUEUES];
+    uint32_t lcnt[SAE_MAX_QUEUES], ccnt[SAE_MAX_QUEUES], coff[SAE_MAX_QUEUES];
+    int32_t mode[SAE_MAX_QUEUES];  // 0: none, 1: all, 2: below lo plus rem from [lo, hi), 3: below hi
+    int32_t active[SAE_MAX_QUEUES];
+    int32_t sh[SAE_MAX_QUEUES], w[SAE_MAX_QUEUES];  // the next digit: bits sh .. sh + w - 1 of e
+    uint32_t mn[SAE_MAX_QUEUES], mx[SAE_MAX_QUEUES];  // smallest and largest key
+    Crossing cr[SAE_MAX_QUEUES];
+    uint32_t seg_tot[16];
+    uint32_t open_cnt, st;
+    int32_t pe;
+};
+
+// A pass over the cached keys of one instance: fn(q, e) for every evictable
+// block, 8 blocks per thread loaded together.
+template <typename Fn>
+__device__ __forceinline__ void batch_cached_pass(const DevCtx &c, int inst, Fn fn)
 {
-    extern __shared__ unsigned long long sh_dyn[];  // hist [Q][SAE_BINS] u32, later lists [Q][P] u64
+    const int N = c.N, tid = threadIdx.x;
+    const long long base = (long long)inst * N;
+    const int nj = (N + SEL_THREADS - 1) / SEL_THREADS;
+    for (int j0 = 0; j0 < nj; j0 += 8) {
+        uint32_t kv[8], qv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int b = tid + (j0 + u) * SEL_THREADS;
+            const bool in = (j0 + u) < nj && b < N;
+            const long long g = base + (in ? b : 0);
+            kv[u] = c.bkey[g];
+            qv[u] = in ? (uint32_t)c.bq[g] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (qv[u]) fn((int)qv[u] - 1, ((unsigned long long)kv[u] << 16) | (uint32_t)(tid + (j0 + u) * SEL_THREADS));
+    }
+}
+
+// After a histogram of every open queue's digit over its range: narrow the
+// range to the crossing bin, and move to the next digit below it.
+__device__ void batch_narrow(BatchSel &bs, int Q)
+{
+    const int tid = threadIdx.x;
+    if (tid < Q && bs.active[tid]) {
+        const Crossing cr = bs.cr[tid];
+        const int sh = bs.sh[tid];
+        const unsigned long long lo = bs.lo[tid] + ((unsigned long long)cr.bin << sh);
+        bs.lo[tid] = lo;
+        bs.hi[tid] = lo + (1ull << sh);
+        bs.rem[tid] -= cr.below;
+        bs.ccnt[tid] = cr.cnt;
+        if (cr.cnt == bs.rem[tid] || sh == 0) {  // the whole bin is selected (a single value when sh = 0)
+            bs.mode[tid] = 3;
+            bs.active[tid] = 0;
+            bs.ccnt[tid] = 0;
+        } else {
+            const int w = sh < SAE_DIGIT_BITS ? sh : SAE_DIGIT_BITS;
+            bs.w[tid] = w;
+            bs.sh[tid] = sh - w;
+        }
+    }
+    lds_barrier();
+    if (tid == 0) {
+        uint32_t n = 0;
+        for (int q = 0; q < Q; ++q) n += bs.active[q] ? bs.ccnt[q] : 0u;
+        bs.open_cnt = n;
+    }
+    lds_barrier();
+}
+
+__global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a, int P, int dyn_elems)
+{
+    extern __shared__ unsigned long long sh_dyn[];  // hist [Q][SAE_BINS] u32, later lists [Q][Pe] + candidates
     uint32_t *hist = reinterpret_cast<uint32_t *>(sh_dyn);
     unsigned long long *lists = sh_dyn;
-    __shared__ SelState st;
+    __shared__ BatchSel bs;
     __shared__ ScoreTab tab;
-    __shared__ uint32_t nev_s[SAE_MAX_QUEUES], need_s[SAE_MAX_QUEUES], lcnt[SAE_MAX_QUEUES];
     __shared__ int32_t cnt_s[SAE_MAX_QUEUES];
-    __shared__ uint32_t st_s;
     const int inst = blockIdx.x;
-    const int Q = c.Q;
-    const int N = c.N;
+    const int Q = c.Q, N = c.N;
+    const int tid = threadIdx.x, lane = lane_id();
     const long long base = (long long)inst * N;
-    const int tid = threadIdx.x;
     load_score_tab(tab, c.state[inst], c);
+    for (int i = tid; i < Q * SAE_BINS; i += blockDim.x) hist[i] = 0;
     if (tid < SAE_MAX_QUEUES) {
-        nev_s[tid] = 0;
-        lcnt[tid] = 0;
+        bs.nev[tid] = 0;
+        bs.lcnt[tid] = 0;
+        bs.active[tid] = 0;
+        bs.mode[tid] = 0;
+        bs.ccnt[tid] = 0;
+        bs.mn[tid] = 0xFFFFFFFFu;
+        bs.mx[tid] = 0;
     }
-    if (tid == 0) st_s = 0;
-    __syncthreads();
+    if (tid == 0) bs.st = 0;
+    lds_barrier();
 
-    uint32_t key[BATCH_IPT];
-    uint32_t info[BATCH_IPT / 8];  // 4 bits per block: 0 = not evictable, else queue + 1
-    uint32_t stbits = 0;
+    // first pass: score, cache, count, smallest and largest key per queue
+    uint32_t cnt_r[SAE_MAX_QUEUES], mn_r[SAE_MAX_QUEUES], mx_r[SAE_MAX_QUEUES];
 #pragma unroll
-    for (int g = 0; g < BATCH_IPT / 8; ++g) info[g] = 0;
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+        cnt_r[q] = 0;
+        mn_r[q] = 0xFFFFFFFFu;
+        mx_r[q] = 0;
+    }
+    uint32_t st = 0;
+    {
+        const int nj = (N + SEL_THREADS - 1) / SEL_THREADS;
+        for (int j0 = 0; j0 < nj; j0 += 4) {
+            uint32_t m[4], off[4];
+            int32_t la[4];
 #pragma unroll
-    for (int j = 0; j < BATCH_IPT; ++j) {
-        int b = tid + j * SEL_THREADS;
-        key[j] = 0;
-        // keep the compiler from hoisting every group's loads (register pressure)
-        if ((j & 7) == 0) __builtin_amdgcn_sched_barrier(0);
-        if (b < N) {
-            uint32_t m = c.meta[base + b];
-            if (meta_evictable(m) && meta_queue(m) < Q) {
-                key[j] = block_key(a.now, c.la[base + b], m, c.off[base + b], tab, stbits);
-                int q = meta_queue(m);
-                info[j >> 3] |= (uint32_t)(q + 1) << (4 * (j & 7));
-                atomicAdd(&nev_s[q], 1u);
+            for (int u = 0; u < 4; ++u) {
+                const int b = tid + (j0 + u) * SEL_THREADS;
+                const bool in = (j0 + u) < nj && b < N;
+                const long long g = base + (in ? b : 0);
+                m[u] = c.meta[g];
+                la[u] = c.la[g];
+                off[u] = c.off[g];
+                m[u] = in ? m[u] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int b = tid + (j0 + u) * SEL_THREADS;
+                const bool ev = meta_evictable(m[u]) && meta_queue(m[u]) < Q;
+                const int q = meta_queue(m[u]);
+                uint32_t key = 0;
+                if (ev) {
+                    key = block_key(a.now, la[u], m[u], off[u], tab, st);
+#pragma unroll
+                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+                        if (qq >= Q) break;  // uniform
+                        cnt_r[qq] += (qq == q) ? 1u : 0u;
+                        mn_r[qq] = (qq == q) ? min(mn_r[qq], key) : mn_r[qq];
+                        mx_r[qq] = (qq == q) ? max(mx_r[qq], key) : mx_r[qq];
+                    }
+                }
+                if ((j0 + u) < nj && b < N) {
+                    c.bkey[base + b] = key;
+                    c.bq[base + b] = ev ? (uint8_t)(q + 1) : (uint8_t)0;
+                }
             }
         }
     }
-    if (stbits) atomicOr(&st_s, stbits);
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
+        uint32_t v = cnt_r[q], lo = mn_r[q], hi = mx_r[q];
+        for (int o = 32; o > 0; o >>= 1) {
+            v += __shfl_xor(v, o, SAE_WAVE);
+            lo = min(lo, (uint32_t)__shfl_xor(lo, o, SAE_WAVE));
+            hi = max(hi, (uint32_t)__shfl_xor(hi, o, SAE_WAVE));
+        }
+        if (lane == 0 && v) {
+            atomicAdd(&bs.nev[q], v);
+            atomicMin(&bs.mn[q], lo);
+            atomicMax(&bs.mx[q], hi);
+        }
+    }
+    lds_barrier();
     if (tid < Q) {
-        int kk = inst_k(a, inst, c.max_k);
-        need_s[tid] = (uint32_t)min((long long)kk, (long long)nev_s[tid]);
-    }
-    __syncthreads();
-    sel_init(st, Q, need_s, nev_s);
-
-    // composite (key << 16 | id): 48 bits, digits of 11, 11, 11, 11 and 4 bits
-    for (int p = 0; p < 5 && st.any_active; ++p) {
-        const int s = (p < 4) ? 37 - 11 * p : 0;
-        const int w = (p < 4) ? 11 : 4;
-        for (int i = tid; i < Q * SAE_BINS; i += blockDim.x) hist[i] = 0;
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < BATCH_IPT; ++j) {
-            int qi = (int)((info[j >> 3] >> (4 * (j & 7))) & 15u);
-            if (qi) {
-                int q = qi - 1;
-                unsigned long long e = ((unsigned long long)key[j] << 16) | (uint32_t)(tid + j * SEL_THREADS);
-                if (st.active[q] && (p == 0 || (e >> (s + w)) == st.prefix[q]))
-                    atomicAdd(&hist[q * SAE_BINS + ((uint32_t)(e >> s) & ((1u << w) - 1u))], 1u);
-            }
+        const int kk = inst_k(a, inst, c.max_k);
+        const uint32_t need = (uint32_t)min((long long)kk, (long long)bs.nev[tid]);
+        bs.need[tid] = need;
+        bs.rem[tid] = need;
+        if (need == 0) bs.mode[tid] = 0;
+        else if (need >= bs.nev[tid]) bs.mode[tid] = 1;
+        else {
+            // the first digit: the highest bits where the queue's keys differ,
+            // or the id bits when every key is equal
+            const uint32_t kx = bs.mn[tid] ^ bs.mx[tid];
+            const int top = kx ? 16 + (32 - __clz(kx)) : 16;  // bits of e below the common prefix
+            const unsigned long long mn = (unsigned long long)bs.mn[tid] << 16;
+            const int w = top < SAE_DIGIT_BITS ? top : SAE_DIGIT_BITS;
+            bs.w[tid] = w;
+            bs.sh[tid] = top - w;
+            bs.lo[tid] = (mn >> top) << top;
+            bs.hi[tid] = bs.lo[tid] + (1ull << top);
+            bs.ccnt[tid] = bs.nev[tid];
+            bs.mode[tid] = 2;
+            bs.active[tid] = 1;
         }
-        __syncthreads();
-        find_crossing(hist, Q, st.rem, st.active, st.cr, st.seg_tot);
-        sel_step(st, Q, s, w, p == 4);
     }
-    // collect (the histogram area is reused for the lists); only the first
-    // Pe = pow2 >= the largest need of each segment is filled and sorted
-    __shared__ int32_t pe_s;
-    if (tid == 0) {
+    lds_barrier();
+    if (tid == 0) {  // list segments of Pe = pow2 >= the largest need
         uint32_t mx = 1;
-        for (int q = 0; q < Q; ++q) mx = need_s[q] > mx ? need_s[q] : mx;
-        pe_s = pow2_ge((int)mx) < P ? pow2_ge((int)mx) : P;
+        for (int q = 0; q < Q; ++q) mx = bs.need[q] > mx ? bs.need[q] : mx;
+        bs.pe = pow2_ge((int)mx) < P ? pow2_ge((int)mx) : P;
     }
+    lds_barrier();
+    if (tid == 0) {
+        uint32_t n = 0;
+        for (int q = 0; q < Q; ++q) n += bs.active[q] ? bs.ccnt[q] : 0u;
+        bs.open_cnt = n;
+    }
+    const int Pe = bs.pe;
+    // the lists take Q x Pe elements at the start of the dynamic LDS, the
+    // candidates follow (ranked by comparison, so their number is bounded)
+    unsigned long long *cand = sh_dyn + (long long)Q * Pe;
+    // every thread's cached keys are visible to the whole workgroup from here
     __syncthreads();
-    const int Pe = pe_s;
-    const int lpe = 31 - __clz(Pe);
-    for (int i = tid; i < Q * Pe; i += blockDim.x) lists[(long long)(i >> lpe) * P + (i & (Pe - 1))] = ~0ull;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < BATCH_IPT; ++j) {
-        int qi = (int)((info[j >> 3] >> (4 * (j & 7))) & 15u);
-        if (qi) {
-            int q = qi - 1;
-            uint32_t id = (uint32_t)(tid + j * SEL_THREADS);
-            unsigned long long e = ((unsigned long long)key[j] << 16) | id;
-            if (sel_take(st, q, e)) {
-                uint32_t pos = atomicAdd(&lcnt[q], 1u);
-                if (pos < (uint32_t)P) lists[q * P + pos] = ((unsigned long long)key[j] << 32) | id;
-            }
+    // digit passes over the cached keys while the open ranges hold more than
+    // the candidate buffer (each narrows every open range by up to 11 bits;
+    // 48-bit composites need at most 5)
+    for (int lev = 0; lev < 5 && bs.open_cnt > BATCH_CAND; ++lev) {  // uniform
+        for (int i = tid; i < Q * SAE_BINS; i += blockDim.x) hist[i] = 0;
+        if (tid < Q) bs.remv[tid] = bs.rem[tid];
+        lds_barrier();
+        batch_cached_pass(c, inst, [&](int q, unsigned long long e) {
+            if (bs.active[q] && e >= bs.lo[q] && e < bs.hi[q])
+                atomicAdd(&hist[q * SAE_BINS + ((uint32_t)(e >> bs.sh[q]) & ((1u << bs.w[q]) - 1u))], 1u);
+        });
+        lds_barrier();
+        find_crossing(hist, Q, bs.remv, bs.active, bs.cr, bs.seg_tot);
+        batch_narrow(bs, Q);
+    }
+    // candidates per open queue
+    if (tid == 0) {
+        uint32_t o = 0;
+        for (int q = 0; q < Q; ++q) {
+            bs.coff[q] = o;
+            o += (bs.mode[q] == 2) ? bs.ccnt[q] : 0u;
         }
     }
-    __syncthreads();
-    bitonic_sort_segments(lists, Q, Pe, P);
-    if (tid < Q) cnt_s[tid] = (int32_t)min(need_s[tid], (uint32_t)P);
-    __syncthreads();
+    for (int i = tid; i < Q * Pe; i += blockDim.x) lists[i] = ~0ull;
+    if (tid < Q) bs.ccnt[tid] = 0;  // from here the fill count of the queue's candidates
+    lds_barrier();
+    // collect
+    batch_cached_pass(c, inst, [&](int q, unsigned long long e) {
+        const int md = bs.mode[q];
+        const bool sel = md == 1 || (md == 3 && e < bs.hi[q]) || (md == 2 && e < bs.lo[q]);
+        const unsigned long long v = ((e >> 16) << 32) | (e & 0xFFFFull);
+        if (sel) lists[(long long)q * Pe + atomicAdd(&bs.lcnt[q], 1u)] = v;
+        else if (md == 2 && e < bs.hi[q]) cand[bs.coff[q] + atomicAdd(&bs.ccnt[q], 1u)] = v;
+    });
+    lds_barrier();
+    // candidates: ranked among their queue's candidates, the first rem join the list
+    {
+        uint32_t tot = 0;
+        for (int q = 0; q < Q; ++q) tot += (bs.mode[q] == 2) ? bs.ccnt[q] : 0u;
+        for (uint32_t i = tid; i < tot; i += blockDim.x) {
+            int q = 0;  // the queue whose candidates hold position i
+            for (int qq = 0; qq < Q; ++qq)
+                if (bs.mode[qq] == 2 && i >= bs.coff[qq] && i < bs.coff[qq] + bs.ccnt[qq]) q = qq;
+            const unsigned long long v = cand[i];
+            const uint32_t lo = bs.coff[q], n = bs.ccnt[q];
+            uint32_t rk = 0;
+            for (uint32_t t = 0; t < n; ++t) rk += (cand[lo + t] < v) ? 1u : 0u;
+            if (rk < bs.rem[q]) lists[(long long)q * Pe + (bs.need[q] - bs.rem[q]) + rk] = v;
+        }
+    }
+    if (st) atomicOr(&bs.st, st);
+    lds_barrier();
+    if (Pe >= 256 && 2 * Q * Pe <= dyn_elems) sort_segments_lds(lists, Q * Pe, Pe);
+    else bitonic_sort_segments(lists, Q, Pe, Pe);
+    if (tid < Q) cnt_s[tid] = (int32_t)min(bs.need[tid], (uint32_t)P);
+    lds_barrier();
     for (int q = 0; q < Q; ++q) {
         const long long ob = ((long long)inst * Q + q) * c.max_k;
         for (int j = tid; j < cnt_s[q]; j += blockDim.x) {
-            unsigned long long e = lists[q * P + j];
+            const unsigned long long e = lists[(long long)q * Pe + j];
             a.victims[ob + j] = (int32_t)(uint32_t)(e & 0xFFFFFFFFull);
             if (a.scores) a.scores[ob + j] = __uint_as_float((uint32_t)(e >> 32));
             c.sel[ob + j] = e;
@@ -2108,12 +2323,12 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
         a.count[(long long)inst * Q + tid] = cnt_s[tid];
         c.sel_count[(long long)inst * Q + tid] = cnt_s[tid];
     }
-    int kk = inst_k(a, inst, c.max_k);
-    int d = merge_decision(lists, P, cnt_s, Q, c.ef_queue, kk, a.decision + (long long)inst * c.max_k);
+    const int kk = inst_k(a, inst, c.max_k);
+    const int d = merge_decision(lists, Pe, cnt_s, Q, c.ef_queue, kk, a.decision + (long long)inst * c.max_k);
     if (tid == 0) {
         a.decision_count[inst] = d;
         if (!(a.flags & SAE_SS_CASCADE)) commit_bookkeeping(c.state[inst], d, (a.flags & SAE_SS_COMMIT) != 0);
-        set_status(c.status, st_s);
+        set_status(c.status, bs.st);
     }
 }
 
@@ -2533,11 +2748,13 @@ int scan_grid_x(int n_inst, int N)
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s)
 {
     int P = pow2_at_least(c.max_k);
-    size_t per = (size_t)P * 8 > (size_t)SAE_BINS * 4 ? (size_t)P * 8 : (size_t)SAE_BINS * 4;
-    size_t lds = (size_t)c.Q * per;
+    // the histograms, then the lists and the candidate buffer
+    const size_t h = (size_t)c.Q * SAE_BINS * 4, l = ((size_t)c.Q * P + BATCH_CAND) * 8;
+    const size_t lds = h > l ? h : l;
+    const int dyn_elems = (int)(lds / 8);
     hipError_t e = allow_lds((const void *)k_batched, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_batched, dim3(c.n_inst), dim3(SEL_THREADS), lds, s, c, a, P);
+    hipLaunchKernelGGL(k_batched, dim3(c.n_inst), dim3(SEL_THREADS), lds, s, c, a, P, dyn_elems);
     return hipGetLastError();
 }
 

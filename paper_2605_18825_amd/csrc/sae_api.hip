@@ -188,6 +188,9 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.casc_prom, I * d.max_k) && dev_alloc(c, &d.casc_pe, I * d.max_k) &&
               dev_alloc(c, &d.casc_aid, I * d.max_k) &&
               dev_alloc(c, &d.casc_n, I * 4);
+    // the batched engine's key cache, where that engine can run
+    const long long nb = batched_engine_fits(d) ? I * d.N : 0;
+    ok = ok && dev_alloc(c, &d.bkey, nb) && dev_alloc(c, &d.bq, nb);
     if (!ok) {
         for (void *p : c->allocs) (void)hipFree(p);
         delete c;

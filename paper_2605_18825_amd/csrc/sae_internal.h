@@ -175,6 +175,11 @@ struct DevCtx {
     int32_t *casc_aid;              // [n_inst][max_k]
     unsigned long long *casc_pe;    // [n_inst][max_k]
     int32_t *casc_n;                // [n_inst][4]: touched, listed, (unused), admitted
+    // Batched engine (instances of at most 65,536 blocks): every block's key
+    // and queue + 1 (0: not evictable) from the call's first pass, read back
+    // by its later passes
+    uint32_t *bkey;  // [n_inst][N]
+    uint8_t *bq;     // [n_inst][N]
 };
 
 // Positional bin of a block (decay-power learner): floor(8 o_b / o_max) with
