@@ -394,6 +394,29 @@ enum { SAE_FB_FORCE = 1u << 0 };
  */
 sae_status sae_feedback_update(sae_ctx *ctx, uint32_t flags, sae_stream_t stream);
 
+/*
+ * Checkpoint and resume of one instance's state held by the context: its
+ * learned parameters and learner settings, every feedback counter, the
+ * eviction count, Algorithm 4's interval buffers and the recently_evicted
+ * ring (Algorithm 1), as one opaque blob.  The pool arrays are the caller's;
+ * the block index is rebuilt from them.
+ *  sae_state_size:  *bytes (host) = the blob size for this context's shape
+ *  sae_save_state:  writes the blob of instance `inst` to buf (host, `bytes`
+ *                   = sae_state_size) and synchronizes `stream`
+ *  sae_load_state:  restores instance `inst` from a blob saved by a context
+ *                   of the same shape (queues and kinds, max_k, ghost window,
+ *                   blocks per instance); SAE_ERR_ARG (nothing changed) for a
+ *                   blob of another shape or size.  It rebuilds the
+ *                   recently_evicted table and synchronizes `stream`.
+ * To resume: copy the pool arrays, sae_create a context of the same shape,
+ * sae_bind_pool, sae_index_build (which clears state), then sae_load_state
+ * for every instance.  The resumed instance then decides, matches and
+ * learns exactly as the saved one would have.
+ */
+sae_status sae_state_size(sae_ctx *ctx, size_t *bytes);
+sae_status sae_save_state(sae_ctx *ctx, int32_t inst, void *buf, size_t bytes, sae_stream_t stream);
+sae_status sae_load_state(sae_ctx *ctx, int32_t inst, const void *buf, size_t bytes, sae_stream_t stream);
+
 /* Algorithm 4's interval buffer of one (instance, log-normal queue), oldest
  * first: out (host int32, cap entries) receives the first min(n, cap)
  * intervals in ticks and *n (host) the number held.  Synchronizes `stream`.

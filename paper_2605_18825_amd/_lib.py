@@ -96,6 +96,9 @@ SIGNATURES = {
     "sae_feedback_update": (_I32, [_P, _U32, _P]),
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
     "sae_get_intervals": (_I32, [_P, _I32, _I32, _P, _I32, ctypes.POINTER(_I32), _P]),
+    "sae_state_size": (_I32, [_P, ctypes.POINTER(ctypes.c_size_t)]),
+    "sae_save_state": (_I32, [_P, _I32, _P, ctypes.c_size_t, _P]),
+    "sae_load_state": (_I32, [_P, _I32, _P, ctypes.c_size_t, _P]),
     "sae_predict_sessions": (_I32, [_I32, _I32, _P, ctypes.POINTER(SaePredictor), _P, _P, _P, _P]),
     "sae_predict_sessions_noalloc": (_I32, [_I32, _I32, _P, ctypes.POINTER(SaePredictor), _P, _P, _P]),
     "sae_select_stats": (_I32, [_P, _I32, _P, _P]),

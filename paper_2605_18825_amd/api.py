@@ -227,6 +227,26 @@ def sae_profile_read(ctx):
     return ms.value, n.value
 
 
+def sae_state_size(ctx):
+    n = ctypes.c_size_t()
+    _check(ctx, _lib.load().sae_state_size(ctx, ctypes.byref(n)))
+    return n.value
+
+
+def sae_save_state(ctx, inst, stream=None):
+    """Instance `inst`'s context-held state as bytes (see include/sae.h)."""
+    n = sae_state_size(ctx)
+    buf = ctypes.create_string_buffer(n)
+    _check(ctx, _lib.load().sae_save_state(ctx, inst, ctypes.cast(buf, ctypes.c_void_p), n, _stream(stream)))
+    return buf.raw
+
+
+def sae_load_state(ctx, inst, blob, stream=None):
+    buf = ctypes.create_string_buffer(bytes(blob), len(blob))
+    _check(ctx, _lib.load().sae_load_state(ctx, inst, ctypes.cast(buf, ctypes.c_void_p), len(blob),
+                                           _stream(stream)))
+
+
 def sae_get_intervals(ctx, inst, queue, cap=IVL_CAP, stream=None):
     """Algorithm 4's interval buffer of (inst, queue), oldest first (host list)."""
     buf = (ctypes.c_int32 * max(cap, 1))()

@@ -359,6 +359,97 @@ sae_status sae_set_counters(sae_ctx *c, int32_t inst, const sae_counters *in, sa
     return SAE_OK;
 }
 
+// Blob of sae_save_state: this header, the instance's InstState (counters
+// folded in), its interval buffers [Q][SAE_IVL_CAP] (when the context has a
+// log-normal queue) and its recently_evicted ring [ring_cap].
+struct StateHeader {
+    uint32_t magic, version;
+    int32_t Q, N, max_k, W, ring_cap, has_ivl;
+    int32_t kind[SAE_MAX_QUEUES];
+    uint64_t state_bytes, ivl_bytes, ring_bytes, total;
+};
+constexpr uint32_t kStateMagic = 0x53414553u;  // "SEAS"
+
+static StateHeader state_header(const sae_ctx *c)
+{
+    StateHeader h;
+    memset(&h, 0, sizeof(h));
+    const DevCtx &d = c->dc;
+    h.magic = kStateMagic;
+    h.version = 1;
+    h.Q = d.Q;
+    h.N = d.N;
+    h.max_k = d.max_k;
+    h.W = d.W;
+    h.ring_cap = d.ring_cap;
+    h.has_ivl = d.ln_mask ? 1 : 0;
+    for (int q = 0; q < SAE_MAX_QUEUES; ++q) h.kind[q] = q < d.Q ? d.kind[q] : -1;
+    h.state_bytes = sizeof(InstState);
+    h.ivl_bytes = h.has_ivl ? (uint64_t)d.Q * SAE_IVL_CAP * sizeof(int32_t) : 0;
+    h.ring_bytes = (uint64_t)d.ring_cap * sizeof(GhostEntry);
+    h.total = sizeof(StateHeader) + h.state_bytes + h.ivl_bytes + h.ring_bytes;
+    return h;
+}
+
+sae_status sae_state_size(sae_ctx *c, size_t *bytes)
+{
+    if (!c || !bytes) return fail(c, SAE_ERR_ARG, "ctx and bytes must be non-NULL");
+    *bytes = (size_t)state_header(c).total;
+    return SAE_OK;
+}
+
+sae_status sae_save_state(sae_ctx *c, int32_t inst, void *buf, size_t bytes, sae_stream_t stream)
+{
+    if (!c || !buf) return fail(c, SAE_ERR_ARG, "ctx and buf must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    const StateHeader h = state_header(c);
+    if (bytes != h.total) return fail(c, SAE_ERR_ARG, "bytes must be sae_state_size()");
+    char *p = static_cast<char *>(buf);
+    memcpy(p, &h, sizeof(h));
+    const DevCtx &d = c->dc;
+    hipError_t e = launch_feedback(d, 0, 0, S(stream));  // fold the striped counters
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(p + sizeof(h), d.state + inst, h.state_bytes, hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess && h.ivl_bytes)
+        e = hipMemcpyAsync(p + sizeof(h) + h.state_bytes, d.ivl + (long long)inst * d.Q * SAE_IVL_CAP, h.ivl_bytes,
+                           hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(p + sizeof(h) + h.state_bytes + h.ivl_bytes, d.ring + (long long)inst * d.ring_cap,
+                           h.ring_bytes, hipMemcpyDeviceToHost, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_save_state");
+    return SAE_OK;
+}
+
+sae_status sae_load_state(sae_ctx *c, int32_t inst, const void *buf, size_t bytes, sae_stream_t stream)
+{
+    if (!c || !buf) return fail(c, SAE_ERR_ARG, "ctx and buf must be non-NULL");
+    if (check_inst(c, inst, false) != SAE_OK) return SAE_ERR_ARG;
+    const StateHeader h = state_header(c);
+    StateHeader got;
+    if (bytes < sizeof(got)) return fail(c, SAE_ERR_ARG, "blob too small");
+    memcpy(&got, buf, sizeof(got));
+    if (bytes != h.total || memcmp(&got, &h, sizeof(h)) != 0)
+        return fail(c, SAE_ERR_ARG, "blob of another context shape, version or size");
+    const char *p = static_cast<const char *>(buf);
+    const DevCtx &d = c->dc;
+    // fold (and so empty) the striped counters first: the blob's totals replace them
+    hipError_t e = launch_feedback(d, 0, 0, S(stream));
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(d.state + inst, p + sizeof(h), h.state_bytes, hipMemcpyHostToDevice, S(stream));
+    if (e == hipSuccess && h.ivl_bytes)
+        e = hipMemcpyAsync(d.ivl + (long long)inst * d.Q * SAE_IVL_CAP, p + sizeof(h) + h.state_bytes, h.ivl_bytes,
+                           hipMemcpyHostToDevice, S(stream));
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(d.ring + (long long)inst * d.ring_cap, p + sizeof(h) + h.state_bytes + h.ivl_bytes,
+                           h.ring_bytes, hipMemcpyHostToDevice, S(stream));
+    if (e == hipSuccess) e = launch_ghost_rebuild(d, S(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "sae_load_state");
+    c->ghost_tombs = 0;
+    return SAE_OK;
+}
+
 sae_status sae_get_intervals(sae_ctx *c, int32_t inst, int32_t queue, int32_t *out, int32_t cap, int32_t *n,
                              sae_stream_t stream)
 {

@@ -22,6 +22,22 @@ def u64(a):
     return np.asarray(a, np.uint64)
 
 
+def gpu_insert(ctx, ids, hashes, parent, la, queue, counts, ntok, ob, omax):
+    """Add() of host arrays on the HIP side; block types from the token counts
+    by sae_block_type."""
+    n = len(ids)
+    if n == 0:
+        return
+    counts = np.asarray(counts, np.uint8)
+    dev = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a)).to(device="cuda", dtype=dt)
+    tau = torch.empty(n, dtype=torch.uint8, device="cuda")
+    api.sae_block_type(dev(counts, torch.uint8).reshape(n, 5).contiguous(), tau)
+    meta = api.meta_to_u16(api.pack_meta(dev(queue, torch.int32), tau.to(torch.int32), dev(ntok, torch.int32)))
+    off = api.off_to_u32(api.pack_off(dev(ob, torch.int64), dev(omax, torch.int64)))
+    api.sae_insert_blocks(ctx, dev(ids, torch.int32), dev(u64(hashes).view(np.int64), torch.int64),
+                          dev(parent, torch.int32), dev(la, torch.int32), meta, off)
+
+
 class Pair:
     """One instance held by both the oracle and a libsae context."""
 
@@ -117,16 +133,7 @@ class Pair:
         counts = np.asarray(counts_or_tau, np.uint8)
         tau_o = oracle.block_type(counts)
         self.oc.insert(ids, hashes, parent, la, queue, tau_o, ntok, ob, omax)
-        n = len(ids)
-        if n == 0:
-            return
-        dev = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a)).to(device="cuda", dtype=dt)
-        tau = torch.empty(n, dtype=torch.uint8, device="cuda")
-        api.sae_block_type(dev(counts, torch.uint8).reshape(n, 5).contiguous(), tau)
-        meta = api.meta_to_u16(api.pack_meta(dev(queue, torch.int32), tau.to(torch.int32), dev(ntok, torch.int32)))
-        off = api.off_to_u32(api.pack_off(dev(ob, torch.int64), dev(omax, torch.int64)))
-        api.sae_insert_blocks(self.ctx, dev(ids, torch.int32), dev(u64(hashes).view(np.int64), torch.int64),
-                              dev(parent, torch.int32), dev(la, torch.int32), meta, off)
+        gpu_insert(self.ctx, ids, hashes, parent, la, queue, counts, ntok, ob, omax)
 
     def feedback(self, force=False):
         api.sae_feedback_update(self.ctx, api.FB_FORCE if force else 0)
