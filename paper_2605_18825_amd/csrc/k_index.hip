@@ -87,17 +87,42 @@ __device__ __forceinline__ void index_erase(IndexSlot *tab, uint32_t mask, unsig
     }
 }
 
-// Live, unconsumed ghost entry of hash h: table slot index, or -1.
-__device__ __forceinline__ int ghost_find(const GhostSlot *tab, uint32_t mask, const GhostEntry *ring,
-                                          unsigned long long h, long long ev_now, int W, uint32_t *ring_pos)
+// index_insert with the home slot's hash already loaded, and the lookup of a
+// live, unconsumed recently_evicted entry of hash h (its table slot index, or
+// -1; *ring_pos its ring position) likewise.
+__device__ __forceinline__ bool index_insert_from(IndexSlot *tab, uint32_t mask, unsigned long long h, int32_t id,
+                                                  uint32_t tq, uint32_t s0, unsigned long long v0)
+{
+    uint32_t s = s0;
+    unsigned long long v = v0;
+    bool fresh = true;  // v holds slot s's hash as loaded
+    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
+        if (!fresh) v = tab[s].hash;
+        fresh = false;
+        if (v == SAE_EMPTY_HASH || v == SAE_TOMB_HASH) {
+            const unsigned long long old = atomicCAS(&tab[s].hash, v, h);
+            if (old == v) {
+                *reinterpret_cast<uint2 *>(&tab[s].id) = make_uint2((uint32_t)id, tq);
+                return true;
+            }
+            continue;  // lost the slot: look at it again
+        }
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+__device__ __forceinline__ int ghost_find_from(const GhostSlot *tab, uint32_t mask, const GhostEntry *ring,
+                                               unsigned long long h, long long ev_now, int W, uint32_t s0,
+                                               unsigned long long v0, uint32_t *ring_pos)
 {
     if (SAE_HASH_RESERVED(h)) return -1;
-    uint32_t s = hash_home(h, mask);
+    uint32_t s = s0;
     for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        unsigned long long v = tab[s].hash;
+        const unsigned long long v = p == 0 ? v0 : tab[s].hash;
         if (v == SAE_EMPTY_HASH) return -1;
         if (v == h) {
-            uint32_t r = tab[s].ring;
+            const uint32_t r = tab[s].ring;
             const GhostEntry &g = ring[r];
             if (g.hash == h && !(g.tq & SAE_TQ_CONSUMED) && ev_now - g.stamp < (long long)W) {
                 *ring_pos = r;
@@ -300,23 +325,26 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     c.ref_count[g] = 0;
     c.access_count[g] = 0;
     IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    if (!index_insert(tab, c.index_mask, h, b, slot_tq(m, off[i]))) set_status(c.status, SAE_ST_INDEX_FULL);
+    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
+    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    // the first probes of the index and of recently_evicted go out together
+    const uint32_t si = hash_home(h, c.index_mask), sg = hash_home(h, c.ghost_mask);
+    const unsigned long long vi = tab[si].hash, vg = gt[sg].hash;
+    if (!index_insert_from(tab, c.index_mask, h, b, slot_tq(m, off[i]), si, vi))
+        set_status(c.status, SAE_ST_INDEX_FULL);
     int32_t *cs = counter_slot(c, inst, i);
     atomicAdd(cs + SAE_CF_RES + meta_queue(m), 1);
     if (c.state[inst].learn & SAE_LEARN_TOKEN_EMA) atomicAdd(cs + SAE_CF_TADD + meta_type(m) % SAE_N_TYPES, 1);
-    // recently_evicted: a hit counts one miss after eviction (Algorithm 1, Add)
-    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
+    // recently_evicted: a hit counts one miss after eviction (Algorithm 1,
+    // Add) and consumes the entry; its table slot then stays stale (a lookup
+    // skips a consumed entry) until the table is rebuilt from the ring
     uint32_t rp = 0;
-    int s = ghost_find(gt, c.ghost_mask, ring, h, c.state[inst].ev_count, c.W, &rp);
-    if (s >= 0) {
-        if (atomicCAS(&gt[s].hash, h, SAE_TOMB_HASH) == h) {
-            uint32_t old = atomicOr(&ring[rp].tq, SAE_TQ_CONSUMED);
-            if (!(old & SAE_TQ_CONSUMED)) {
-                atomicAdd(cs + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
-                if (((c.struct_mask >> ((old >> 3) & 7u)) & 1u) && (c.state[inst].learn & SAE_LEARN_DECAY_POWER))
-                    atomicAdd(cs + SAE_CF_BMISS + ((old >> SAE_TQ_BIN_SHIFT) & (SAE_N_BINS - 1)), 1);
-            }
+    if (ghost_find_from(gt, c.ghost_mask, ring, h, c.state[inst].ev_count, c.W, sg, vg, &rp) >= 0) {
+        const uint32_t old = atomicOr(&ring[rp].tq, SAE_TQ_CONSUMED);
+        if (!(old & SAE_TQ_CONSUMED)) {
+            atomicAdd(cs + SAE_CF_MISSED + (old & 7u) % SAE_N_TYPES, 1);
+            if (((c.struct_mask >> ((old >> 3) & 7u)) & 1u) && (c.state[inst].learn & SAE_LEARN_DECAY_POWER))
+                atomicAdd(cs + SAE_CF_BMISS + ((old >> SAE_TQ_BIN_SHIFT) & (SAE_N_BINS - 1)), 1);
         }
     }
 }

@@ -13,9 +13,23 @@ from paper_2605_18825_amd import api
 from paper_2605_18825_amd.pool import DevicePool, SelectBuffers
 
 
+_capman = None  # pytest's capture manager, set by conftest: progress lines bypass output capture
+
+
+def set_capture_manager(capman):
+    global _capman
+    _capman = capman
+
+
 def say(*a):
-    print(*a, flush=True)
-    sys.stdout.flush()
+    """A progress line, shown as the test runs even when pytest captures
+    output (a long GPU test then keeps printing)."""
+    if _capman is not None:
+        with _capman.global_and_fixture_disabled():
+            print(*a, flush=True)
+    else:
+        print(*a, flush=True)
+        sys.stdout.flush()
 
 
 def u64(a):
