@@ -410,6 +410,10 @@ __device__ __forceinline__ int pm_field(int f)
 // reuse interval, 0 when none) in pm_rec[r]; no block is touched here, so
 // every last_access read is the one from before the call, and k_pm_place
 // touches afterwards.
+#ifndef PM_FIRST
+#define PM_FIRST 8  // hashes of a request's first probe round
+#endif
+static_assert(PM_FIRST >= 1 && PM_FIRST <= SAE_WAVE, "the first round fits a wave");
 __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, int max_len, const uint64_t *hashes,
                                                           const int32_t *lens, const int32_t *inst_a, int32_t now,
                                                           uint32_t flags, int32_t *match_len, int32_t *matched_ids)
@@ -456,17 +460,22 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
             const uint64_t *hr = hashes + (long long)r * max_len;
             int m = 0;
             int j0 = 0;
-            // Chunks of 64 hashes.  The index slot carries the block's queue,
-            // type and positional bin, so a chunk costs one round trip (its
-            // probe); the next chunk's hashes come with this chunk's probe.
+            // Rounds of hashes: the first PM_FIRST, then 64 at a time.  The
+            // index slot carries the block's queue, type and positional bin,
+            // so a round costs one round trip (its probe); the next round's
+            // hashes come with this round's probe.  A short first round spares
+            // the probes past an early miss (most requests that miss, miss
+            // early) for one more round trip on the long matches.
+            int w = PM_FIRST;  // lanes of this round
             uint32_t tq = 0;
-            int32_t id = (lane < len) ? index_find(tab, c.index_mask, hr[lane], &tq) : -1;
-            unsigned long long hnext = (SAE_WAVE + lane < len) ? hr[SAE_WAVE + lane] : 0ull;
-            for (; j0 < len; j0 += SAE_WAVE) {
+            int32_t id = (lane < w && lane < len) ? index_find(tab, c.index_mask, hr[lane], &tq) : -1;
+            unsigned long long hnext = (w + lane < len) ? hr[w + lane] : 0ull;
+            while (j0 < len) {  // uniform
                 const int j = j0 + lane;
-                const bool miss = (j < len) && (id < 0);
+                const bool inr = lane < w && j < len;
+                const bool miss = inr && (id < 0);
                 const unsigned long long mm = __ballot(miss);
-                const int first = mm ? (__ffsll((long long)mm) - 1) : SAE_WAVE;
+                const int first = mm ? (__ffsll((long long)mm) - 1) : w;
                 const int lim = min(first, len - j0);
                 const bool hit = lane < lim;
                 int q = 0, ty = 0;
@@ -481,7 +490,7 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                         atomicAdd(&c.access_count[g], 1);
                     }
                     if (mid) mid[j] = id;
-                } else if (mid && j < max_len) {
+                } else if (mid && lane < w && j < max_len) {
                     mid[j] = -1;
                 }
                 if (flags & SAE_PM_STATS) {
@@ -509,12 +518,11 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
                     }
                 }
                 m = j0 + lim;
-                if (mm || j0 + SAE_WAVE >= len) {  // uniform
-                    j0 += SAE_WAVE;
-                    break;
-                }
-                // this chunk matched whole: probe the next one
-                const int jn = j + SAE_WAVE;
+                j0 += w;
+                if (mm || j0 >= len) break;  // uniform
+                // this round matched whole: probe the next 64
+                w = SAE_WAVE;
+                const int jn = j0 + lane;
                 id = (jn < len) ? index_find(tab, c.index_mask, hnext, &tq) : -1;
                 hnext = (jn + SAE_WAVE < len) ? hr[jn + SAE_WAVE] : 0ull;
             }

@@ -431,6 +431,24 @@ __device__ __forceinline__ int inst_k(const SelectArgs &a, int inst, int max_k)
     return k < 0 ? 0 : (k > max_k ? max_k : k);
 }
 
+// Ascending sort of n distinct elements src[0..n) (LDS) into dst[0..n) (LDS):
+// each element's position is the number of smaller elements, counted with
+// reads that every lane of a wave makes at the same address.  All threads call.
+__device__ void rank_sort(const unsigned long long *src, int n, unsigned long long *dst)
+{
+    for (int t = threadIdx.x; t < n; t += blockDim.x) {
+        const unsigned long long e = src[t];
+        int rank = 0, i = 0;
+        for (; i + 8 <= n; i += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) rank += (src[i + u] < e) ? 1 : 0;
+        }
+        for (; i < n; ++i) rank += (src[i] < e) ? 1 : 0;
+        dst[rank] = e;
+    }
+    lds_barrier();
+}
+
 // LDS working set of the per-(instance, queue) selection kernels.
 #define LCAP 16384  // elements (128 KiB of LDS)
 
@@ -444,7 +462,18 @@ struct BoundScratch {
     uint32_t bin, below, cnt;
     unsigned long long piv[SEL_PIVOTS], tmp[SEL_TMP], res;
     uint32_t pcnt[SEL_PIVOTS + 1], kb, kbelow, kn, fill;
+    uint32_t nsorted;  // when nonzero, the nsorted smallest elements, ascending, at tmp + SEL_HEAD
 };
+#define SEL_HEAD 256  // where the sorted head starts in tmp; at most SEL_HEAD elements
+static_assert(SEL_TMP >= 2 * SEL_HEAD, "a head and its sorted copy fit the scratch");
+
+// The n <= SEL_HEAD elements src[0 .. n) (LDS), sorted into b.tmp + SEL_HEAD
+// (each placed by its count of smaller ones).  All threads call.
+__device__ void lds_sort_head(const unsigned long long *src, int n, BoundScratch &b)
+{
+    if (threadIdx.x == 0) b.nsorted = (uint32_t)n;
+    rank_sort(src, n, b.tmp + SEL_HEAD);
+}
 
 // Among n distinct elements held in LDS, a bound B such that exactly `need`
 // of them are <= B (1 <= need < n).  Radix select with 11-bit digits starting
@@ -534,22 +563,20 @@ __device__ unsigned long long lds_select_bound(const unsigned long long *el, int
 // Sample select: SEL_PIVOTS elements taken at evenly spaced positions are
 // ranked into sorted pivots, every element is counted into the pivot interval
 // it falls in, and only the interval holding the r-th element is ranked
-// exactly.  An interval too large for the scratch falls back to the radix
-// select.  All threads call; blockDim.x a multiple of 64 and >= 128.
+// exactly.  When that interval and the ones below it hold at most SEL_HEAD
+// elements (a small r: the usual case of a candidate bound), all of them are
+// sorted instead, and b.nsorted says how many b.tmp + SEL_HEAD then holds in
+// order (0 otherwise); so are all n elements when n <= SEL_HEAD.  An interval
+// too large for the scratch falls back to the radix select.  All threads
+// call; blockDim.x a multiple of 64 and >= 128.
 __device__ unsigned long long lds_select_rank(const unsigned long long *el, int n, uint32_t r, BoundScratch &b)
 {
     const int tid = threadIdx.x;
     const int nt = blockDim.x;
     const int lane = lane_id();
-    if (n <= SEL_PIVOTS * 2) {
-        for (int t = tid; t < n; t += nt) {
-            const unsigned long long e = el[t];
-            uint32_t rk = 0;
-            for (int i = 0; i < n; ++i) rk += (el[i] < e) ? 1u : 0u;
-            if (rk == r - 1) b.res = e;
-        }
-        lds_barrier();
-        return b.res;
+    if (n <= SEL_HEAD) {
+        lds_sort_head(el, n, b);
+        return b.tmp[SEL_HEAD + r - 1];
     }
     if (tid < SAE_WAVE) {
         // pivots: one element per lane from evenly spaced positions, ranked within the wave
@@ -608,6 +635,22 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
     }
     lds_barrier();
     const uint32_t kb = b.kb, kbelow = b.kbelow, kn = b.kn;
+    if (tid == 0) b.nsorted = 0;
+    if (kbelow + kn <= SEL_HEAD) {
+        // every element up to the interval's upper pivot, sorted
+        const unsigned long long phi = (kb == SEL_PIVOTS) ? ~0ull : b.piv[kb];
+        for (int i0 = tid; i0 < n; i0 += 4 * nt) {
+            unsigned long long e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) e[u] = (i0 + u * nt < n) ? el[i0 + u * nt] : ~0ull;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (i0 + u * nt < n && e[u] <= phi) b.tmp[atomicAdd(&b.fill, 1u)] = e[u];
+        }
+        lds_barrier();
+        lds_sort_head(b.tmp, (int)(kbelow + kn), b);
+        return b.tmp[SEL_HEAD + r - 1];
+    }
     if (kn > SEL_TMP) {
         lds_barrier();
         const unsigned long long B = lds_select_bound(el, n, r, b);  // exactly r elements <= B
@@ -749,24 +792,6 @@ __device__ __forceinline__ int last_le(const uint32_t *a, int n, uint32_t x)
     for (int st = 1 << (LOG - 1); st > 0; st >>= 1)
         if (l + st < n && a[l + st] <= x) l += st;
     return l;
-}
-
-// Ascending sort of n distinct elements src[0..n) (LDS) into dst[0..n) (LDS):
-// each element's position is the number of smaller elements, counted with
-// reads that every lane of a wave makes at the same address.  All threads call.
-__device__ void rank_sort(const unsigned long long *src, int n, unsigned long long *dst)
-{
-    for (int t = threadIdx.x; t < n; t += blockDim.x) {
-        const unsigned long long e = src[t];
-        int rank = 0, i = 0;
-        for (; i + 8 <= n; i += 8) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) rank += (src[i + u] < e) ? 1 : 0;
-        }
-        for (; i < n; ++i) rank += (src[i] < e) ? 1 : 0;
-        dst[rank] = e;
-    }
-    lds_barrier();
 }
 
 // Sample rank r of the candidate bound: with f the sampled fraction and need
@@ -928,19 +953,24 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
         const bool all = (r >= tot) || (est <= ALL_EST);
         const uint32_t K = tot;  // <= SAMPLE_WGS * SAMPLE_CHUNK <= LCAP
         const unsigned long long *sp = c.samp + (long long)inst * SAMPLE_WGS * SAMPLE_CHUNK;
-        for (uint32_t i0 = 0; i0 < K; i0 += 4 * SEL_THREADS) {
-            unsigned long long ev[4];
+        // every load in flight together: a thread's elements past K load
+        // element K - 1 again (in bounds) and are not stored
+        constexpr int SPT = SAMPLE_WGS * SAMPLE_CHUNK / SEL_THREADS;
+        const uint32_t rounds = (K + SEL_THREADS - 1) / SEL_THREADS;  // uniform, <= SPT
+        unsigned long long ev[SPT];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const uint32_t i = i0 + tid + (uint32_t)m * SEL_THREADS;
+        for (int m = 0; m < SPT; ++m) {
+            if ((uint32_t)m < rounds) {
+                uint32_t i = (uint32_t)(tid + m * SEL_THREADS);
+                i = i < K ? i : K - 1;
                 const int ch = last_le<6>(cpre, SAMPLE_WGS, i);  // the chunk holding element i
-                ev[m] = (i < K) ? sp[(long long)ch * SAMPLE_CHUNK + cbase[ch] + (i - cpre[ch])] : ~0ull;
+                ev[m] = sp[(long long)ch * SAMPLE_CHUNK + cbase[ch] + (i - cpre[ch])];
             }
+        }
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const uint32_t i = i0 + tid + (uint32_t)m * SEL_THREADS;
-                if (i < K) el[i] = ev[m];
-            }
+        for (int m = 0; m < SPT; ++m) {
+            const uint32_t i = (uint32_t)(tid + m * SEL_THREADS);
+            if ((uint32_t)m < rounds && i < K) el[i] = ev[m];
         }
         lds_barrier();
         unsigned long long bound;
@@ -948,22 +978,34 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
         if (all) {
             bound = ~0ull;
             rr = K;
+            if (K <= SAE_NBUCKET - 1) lds_sort_head(el, (int)K, bs);
+            else if (tid == 0) bs.nsorted = 0;
+            lds_barrier();
         } else {  // r < K
             bound = lds_select_rank(el, (int)K, r, bs);
             rr = r;
         }
         // upper ends: the elements <= bound, or every stride-th staged one of them
         const uint32_t stride = rr <= SAE_NBUCKET - 1 ? 1u : (rr + SAE_NBUCKET - 3) / (SAE_NBUCKET - 2);
-        for (uint32_t i = tid; i < K; i += blockDim.x) {
-            const unsigned long long e = el[i];
-            if (e <= bound && (stride == 1u || (i % stride) == 0u)) {
-                const uint32_t p = atomicAdd(&nsp_s, 1u);
-                if (p < SAE_NBUCKET - 1) spl_raw[p] = e;
+        const bool sorted = stride == 1u && bs.nsorted >= rr;  // uniform
+        int np;
+        if (sorted) {
+            // the select left the smallest elements in order: the first rr are the ends
+            if (tid < (int)rr) spl[tid] = bs.tmp[SEL_HEAD + tid];
+            np = (int)rr;
+        } else {
+            for (uint32_t i = tid; i < K; i += blockDim.x) {
+                const unsigned long long e = el[i];
+                if (e <= bound && (stride == 1u || (i % stride) == 0u)) {
+                    const uint32_t p = atomicAdd(&nsp_s, 1u);
+                    if (p < SAE_NBUCKET - 1) spl_raw[p] = e;
+                }
             }
+            lds_barrier();
+            np = nsp_s < SAE_NBUCKET - 1 ? (int)nsp_s : SAE_NBUCKET - 1;
+            rank_sort(spl_raw, np, spl);
         }
         lds_barrier();
-        const int np = nsp_s < SAE_NBUCKET - 1 ? (int)nsp_s : SAE_NBUCKET - 1;
-        rank_sort(spl_raw, np, spl);
         if (tid == 0) {
             int nb = np;
             if (nb == 0 || spl[nb - 1] != bound) spl[nb++] = bound;  // the last upper end is the bound
