@@ -1,8 +1,8 @@
 """GPU parity of the session predictor (Sec. 3.3) through the C ABI against
 the fp64 oracle: the first layer's output (its k slices summed) element by
 element and the logits
-within 1e-4 (1 + |y|) (fp32 evaluation in blocked and in sequential order
-stays within a twentieth of it, while a dropped term exceeds it tenfold: both
+within 1e-5 (1 + |y|) (fp32 evaluation in blocked and in sequential order
+stays within a tenth of it, while a dropped term exceeds it tenfold: both
 pinned in tests/test_oracle_predictor.py); predictions
 equal wherever the logit is farther than that from 0.  Sizes: the full
 d = 4,096 of the workload, a ragged batch, the smallest and largest d, one
@@ -18,7 +18,7 @@ from oracle import predictor as P  # noqa: E402
 from paper_2605_18825_amd import api  # noqa: E402
 from synth import predictor as S  # noqa: E402
 
-TOL = 1e-4
+TOL = 1e-5
 
 
 def dev(a, dt):
@@ -47,7 +47,7 @@ def run(n, d, seed):
 def test_predictor_matches_oracle(n, d):
     y, h1, eb, g1, gy, gp = run(n, d, 900 + n + d)
     assert np.all(np.isfinite(g1)) and np.all(np.isfinite(gy))
-    assert np.all(np.abs(g1 - h1) <= 5e-5 * (1 + np.abs(h1))), np.max(np.abs(g1 - h1))
+    assert np.all(np.abs(g1 - h1) <= TOL * (1 + np.abs(h1))), np.max(np.abs(g1 - h1))
     tol = TOL * (1 + np.abs(y))
     err = np.abs(gy.astype(np.float64) - y)
     assert np.all(err <= tol), (float(err.max()), int(np.argmax(err / tol)))
@@ -55,7 +55,8 @@ def test_predictor_matches_oracle(n, d):
     sure = np.abs(y) > tol
     assert np.array_equal(gp[sure], (y[sure] > 0).astype(np.uint8))
     assert set(np.unique(gp).tolist()) <= {0, 1}
-    say("predictor n %d d %d: max |dy| %.3g, %.1f %% predicted to continue" % (n, d, err.max(), 100 * gp.mean()))
+    say("predictor n %d d %d: max |dy| %.3g, max |dh1| / (1 + |h1|) %.3g, %.1f %% predicted to continue"
+        % (n, d, err.max(), float(np.max(np.abs(g1 - h1) / (1 + np.abs(h1)))), 100 * gp.mean()))
 
 
 def test_predictor_argument_checks():

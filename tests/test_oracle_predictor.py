@@ -12,7 +12,7 @@ from synth import predictor as S
 
 # parity tolerance of the predictor's logit, relative to 1 + |y|: the rigorous fp32
 # bound is far too loose here, so the tests below pin this one instead
-TOL = 1e-4
+TOL = 1e-5
 
 
 def test_bf16_decoding_and_rounding():
@@ -78,10 +78,11 @@ def test_error_bound_holds_and_catches_mistakes():
     y32 = b @ w["w3"] + w["b3"][0]
     assert np.all(np.abs(y32 - y) <= eb), (np.abs(y32 - y), eb)
     # the worst-case bound is loose (sums of absolute terms); the parity
-    # tolerance TOL (1 + |y|) holds for fp32 evaluations in blocked and in
-    # plain sequential order, and planted mistakes land far outside it
+    # tolerance TOL (1 + |y|) holds with a tenfold margin for fp32 evaluations
+    # in blocked and in plain sequential order (the sequential one, the worst,
+    # stays below 1e-6 here), and planted mistakes land far outside it
     tol = TOL * (1 + np.abs(y))
-    assert np.all(np.abs(y32 - y) <= tol / 20)
+    assert np.all(np.abs(y32 - y) <= tol / 10)
     h1s = x32[:, 0:1] * W132[:, 0][None, :]
     for i in range(1, d):
         h1s = h1s + x32[:, i:i + 1] * W132[:, i][None, :]
@@ -94,7 +95,7 @@ def test_error_bound_holds_and_catches_mistakes():
     for k in range(1, 64):
         y2 = y2 + b2[:, k] * w["w3"][k]
     y2 = y2 + w["b3"][0]
-    assert np.all(np.abs(y2 - y) <= tol / 20)
+    assert np.all(np.abs(y2 - y) <= tol / 10)
     y_nob2, _, _ = P.forward(h, w["w1"], w["b1"], w["w2"], np.zeros(64), w["w3"], w["b3"])
     y_norelu = (P.bf16_to_f64(h) @ P.bf16_to_f64(w["w1"]).T + w["b1"]) @ w["w2"].T.astype(np.float64)
     y_norelu = np.maximum(y_norelu + w["b2"], 0) @ w["w3"] + w["b3"][0]
