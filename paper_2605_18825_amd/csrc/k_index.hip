@@ -444,6 +444,12 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
     for (int q = 0; q < SAE_MAX_QUEUES; ++q) deep[q] = -1;
     if (active) {
         int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
+        // the first two rounds' hashes are loaded with the length (indices
+        // clamped into the row, so in bounds whatever the length): one round
+        // trip before the first probe instead of two
+        const uint64_t *hr = hashes + (long long)r * max_len;
+        const unsigned long long h0 = hr[lane < max_len ? lane : max_len - 1];
+        const unsigned long long h1 = hr[PM_FIRST + lane < max_len ? PM_FIRST + lane : max_len - 1];
         int len = lens[r];
         if (len > max_len) len = max_len;
         if (len < 0) len = 0;
@@ -457,7 +463,6 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
         } else {
             const IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
             const long long base = (long long)inst * c.N;
-            const uint64_t *hr = hashes + (long long)r * max_len;
             int m = 0;
             int j0 = 0;
             // Rounds of hashes: the first PM_FIRST, then 64 at a time.  The
@@ -468,8 +473,8 @@ __global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, 
             // early) for one more round trip on the long matches.
             int w = PM_FIRST;  // lanes of this round
             uint32_t tq = 0;
-            int32_t id = (lane < w && lane < len) ? index_find(tab, c.index_mask, hr[lane], &tq) : -1;
-            unsigned long long hnext = (w + lane < len) ? hr[w + lane] : 0ull;
+            int32_t id = (lane < w && lane < len) ? index_find(tab, c.index_mask, h0, &tq) : -1;
+            unsigned long long hnext = (w + lane < len) ? h1 : 0ull;
             while (j0 < len) {  // uniform
                 const int j = j0 + lane;
                 const bool inr = lane < w && j < len;
@@ -686,8 +691,11 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(DevCtx c, const int32
     if (threadIdx.x < SAE_CF_N) sums[threadIdx.x] = 0;
     __syncthreads();
     const InstState &s = c.state[inst];
+    // the decision entry is loaded with the decision size (j < max_k: in
+    // bounds either way), so that both arrive in one round trip
+    const int32_t vj = decision[(long long)inst * c.max_k + (j < c.max_k ? j : 0)];
     const int d = s.last_d;
-    int32_t v = (j < d) ? decision[(long long)inst * c.max_k + j] : -1;
+    int32_t v = (j < d) ? vj : -1;
     if (j < d && (v < 0 || v >= c.N)) {
         set_status(c.status, SAE_ST_BAD_BLOCK);
         v = -1;
