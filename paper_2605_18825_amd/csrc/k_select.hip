@@ -2097,6 +2097,8 @@ __global__ void __launch_bounds__(FIN_THREADS) k_final(DevCtx c, SelectArgs a, i
 //  * Each queue's list (at most max_k elements) is sorted, written out, and
 //    the decision merged from the lists (Algorithm 1).
 #define BATCH_CAND 2048  // candidate elements beyond the largest lists in LDS
+#define BATCH_LQ 128     // blocks a wave's scoring list holds: < 64 left + 64 pushed
+#define BATCH_LQ_BYTES (SEL_THREADS / SAE_WAVE * 2 * 3 * BATCH_LQ * 4)  // the first pass's lists (48 KiB)
 struct BatchSel {
     unsigned long long lo[SAE_MAX_QUEUES], hi[SAE_MAX_QUEUES];
     uint32_t nev[SAE_MAX_QUEUES], need[SAE_MAX_QUEUES], rem[SAE_MAX_QUEUES], remv[SAE_MAX_QUEUES];
@@ -2118,6 +2120,37 @@ __device__ __forceinline__ void batch_cached_pass(const DevCtx &c, int inst, Fn 
 {
     const int N = c.N, tid = threadIdx.x;
     const long long base = (long long)inst * N;
+    if ((N & 3) == 0) {
+        // four consecutive blocks per thread and load (16 bytes of keys, 4 of
+        // queues), four such groups in flight: a quarter of the load
+        // instructions of one block per lane
+        const int ng = N / 4;  // groups of four blocks
+        const uint4 *k4 = reinterpret_cast<const uint4 *>(c.bkey + base);
+        const uint32_t *q4 = reinterpret_cast<const uint32_t *>(c.bq + base);
+        for (int g0 = 0; g0 < ng; g0 += 4 * SEL_THREADS) {
+            uint4 kv[4];
+            uint32_t qv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int gi = g0 + u * SEL_THREADS + tid;
+                const bool in = gi < ng;
+                kv[u] = k4[in ? gi : 0];  // clamped: every load unconditional, in flight together
+                qv[u] = q4[in ? gi : 0];
+                qv[u] = in ? qv[u] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t b0 = (uint32_t)(g0 + u * SEL_THREADS + tid) * 4u;
+                const uint32_t kk[4] = {kv[u].x, kv[u].y, kv[u].z, kv[u].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t qb = (qv[u] >> (8 * e)) & 0xFFu;
+                    if (qb) fn((int)qb - 1, ((unsigned long long)kk[e] << 16) | (b0 + (uint32_t)e));
+                }
+            }
+        }
+        return;
+    }
     const int nj = (N + SEL_THREADS - 1) / SEL_THREADS;
     for (int j0 = 0; j0 < nj; j0 += 8) {
         uint32_t kv[8], qv[8];
@@ -2180,7 +2213,6 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
     const int tid = threadIdx.x, lane = lane_id();
     const long long base = (long long)inst * N;
     load_score_tab(tab, c.state[inst], c);
-    for (int i = tid; i < Q * SAE_BINS; i += blockDim.x) hist[i] = 0;
     if (tid < SAE_MAX_QUEUES) {
         bs.nev[tid] = 0;
         bs.lcnt[tid] = 0;
@@ -2203,42 +2235,109 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
     }
     uint32_t st = 0;
     {
+        // A wave's lanes hold blocks of every queue kind, and Eq. 1 (ln,
+        // erfc) and Eq. 2 are long: scored in place, every wave would run
+        // both.  So the blocks of log-normal and structural queues are queued
+        // per wave in LDS with their fields (the dynamic LDS is free until
+        // the digit passes) and scored 64 at a time, one kind per wave-wide
+        // step; the other kinds cost a few operations and are scored in place.
+        // The next step's loads go out before this step is scored.
+        uint32_t *wq = reinterpret_cast<uint32_t *>(sh_dyn) + (tid / SAE_WAVE) * 2 * 3 * BATCH_LQ;
+        uint32_t nq0 = 0, nq1 = 0;  // fill of the log-normal and structural lists (wave-uniform)
+        const unsigned long long lt = lanemask_lt();
+        auto finish = [&](int b, uint32_t m, uint32_t key, bool ev) {
+            const int q = meta_queue(m);
+            if (ev) {
+#pragma unroll
+                for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
+                    if (qq >= Q) break;  // uniform
+                    cnt_r[qq] += (qq == q) ? 1u : 0u;
+                    mn_r[qq] = (qq == q) ? min(mn_r[qq], key) : mn_r[qq];
+                    mx_r[qq] = (qq == q) ? max(mx_r[qq], key) : mx_r[qq];
+                }
+            }
+            c.bkey[base + b] = key;
+            c.bq[base + b] = ev ? (uint8_t)(q + 1) : (uint8_t)0;
+        };
+        // Score the lists: each one that holds 64 (or, at the end, whatever
+        // it holds).  One call site, so that the two long key functions are
+        // compiled once.
+        auto drain = [&](bool final) {
+#pragma unroll 1
+            for (int which = 0; which < 2; ++which) {
+                uint32_t &nq = which == 0 ? nq0 : nq1;
+                const uint32_t n = final ? nq : (nq >= SAE_WAVE ? (uint32_t)SAE_WAVE : 0u);
+                if (n == 0) continue;  // uniform
+                nq -= n;
+                const uint32_t *w = wq + which * 3 * BATCH_LQ;
+                const bool act = (uint32_t)lane < n;
+                const uint32_t p = nq + (act ? (uint32_t)lane : 0u);
+                const int32_t la = (int32_t)w[p];
+                const uint32_t off = w[BATCH_LQ + p], mb = w[2 * BATCH_LQ + p];
+                const uint32_t m = mb & 0xFFFFu;
+                if (act) {
+                    const uint32_t key = which == 0 ? key_lognormal(a.now, la, m, tab, st)
+                                                    : key_structural(a.now, la, m, off, tab, st);
+                    finish((int)(mb >> 16), m, key, true);
+                }
+            }
+        };
+        // Each lane takes blocks tid + 1024 j (consecutive lanes, consecutive
+        // blocks: coalesced loads and key-cache stores), four j per step; the
+        // next step's loads are issued before this step is scored (indices
+        // past the pool load block 0).
         const int nj = (N + SEL_THREADS - 1) / SEL_THREADS;
-        for (int j0 = 0; j0 < nj; j0 += 4) {
-            uint32_t m[4], off[4];
-            int32_t la[4];
+        auto ld = [&](int j0, int32_t (&l)[4], uint32_t (&mm)[4], uint32_t (&o)[4]) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int b = tid + (j0 + u) * SEL_THREADS;
-                const bool in = (j0 + u) < nj && b < N;
-                const long long g = base + (in ? b : 0);
-                m[u] = c.meta[g];
-                la[u] = c.la[g];
-                off[u] = c.off[g];
-                m[u] = in ? m[u] : 0u;
+                const long long g = base + (((j0 + u) < nj && b < N) ? b : 0);
+                l[u] = c.la[g];
+                mm[u] = c.meta[g];
+                o[u] = c.off[g];
+            }
+        };
+        int32_t lc[4], ln[4];
+        uint32_t mc[4], mn2[4], oc[4], on[4];
+        ld(0, lc, mc, oc);
+        for (int j0 = 0; j0 < nj; j0 += 4) {  // uniform
+            ld(j0 + 4, ln, mn2, on);
+#pragma unroll 1
+            for (int e = 0; e < 4; ++e) {
+                // one block per lane: scored in place, or queued
+                const int b = tid + (j0 + e) * SEL_THREADS;
+                const bool in = (j0 + e) < nj && b < N;
+                const int32_t la = e == 0 ? lc[0] : (e == 1 ? lc[1] : (e == 2 ? lc[2] : lc[3]));
+                const uint32_t off = e == 0 ? oc[0] : (e == 1 ? oc[1] : (e == 2 ? oc[2] : oc[3]));
+                const uint32_t m = e == 0 ? mc[0] : (e == 1 ? mc[1] : (e == 2 ? mc[2] : mc[3]));
+                const bool ev = in && meta_evictable(m) && meta_queue(m) < Q;
+                const int kind = ev ? tab.kind[meta_queue(m)] : -1;
+                const bool to0 = kind == SAE_KIND_LOGNORMAL, to1 = kind == SAE_KIND_STRUCTURAL;
+                if (in && !to0 && !to1) finish(b, m, ev ? key_cheap(kind, a.now, la, m, tab, st) : 0u, ev);
+                const unsigned long long m0 = __ballot(to0), m1 = __ballot(to1);
+                if (to0 || to1) {
+                    const uint32_t p = to0 ? nq0 + (uint32_t)__popcll(m0 & lt) : nq1 + (uint32_t)__popcll(m1 & lt);
+                    uint32_t *w = wq + (to0 ? 0 : 3 * BATCH_LQ);
+                    w[p] = (uint32_t)la;
+                    w[BATCH_LQ + p] = off;
+                    w[2 * BATCH_LQ + p] = m | ((uint32_t)b << 16);
+                }
+                nq0 += (uint32_t)__popcll(m0);
+                nq1 += (uint32_t)__popcll(m1);
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                drain(false);
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+                __builtin_amdgcn_wave_barrier();
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int b = tid + (j0 + u) * SEL_THREADS;
-                const bool ev = meta_evictable(m[u]) && meta_queue(m[u]) < Q;
-                const int q = meta_queue(m[u]);
-                uint32_t key = 0;
-                if (ev) {
-                    key = block_key(a.now, la[u], m[u], off[u], tab, st);
-#pragma unroll
-                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
-                        if (qq >= Q) break;  // uniform
-                        cnt_r[qq] += (qq == q) ? 1u : 0u;
-                        mn_r[qq] = (qq == q) ? min(mn_r[qq], key) : mn_r[qq];
-                        mx_r[qq] = (qq == q) ? max(mx_r[qq], key) : mx_r[qq];
-                    }
-                }
-                if ((j0 + u) < nj && b < N) {
-                    c.bkey[base + b] = key;
-                    c.bq[base + b] = ev ? (uint8_t)(q + 1) : (uint8_t)0;
-                }
+                lc[u] = ln[u];
+                mc[u] = mn2[u];
+                oc[u] = on[u];
             }
         }
+        drain(true);  // what the lists still hold
     }
 #pragma unroll
     for (int q = 0; q < SAE_MAX_QUEUES; ++q) {
@@ -2792,7 +2891,8 @@ hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream
     int P = pow2_at_least(c.max_k);
     // the histograms, then the lists and the candidate buffer
     const size_t h = (size_t)c.Q * SAE_BINS * 4, l = ((size_t)c.Q * P + BATCH_CAND) * 8;
-    const size_t lds = h > l ? h : l;
+    size_t lds = h > l ? h : l;
+    if (lds < (size_t)BATCH_LQ_BYTES) lds = BATCH_LQ_BYTES;  // the first pass's scoring lists
     const int dyn_elems = (int)(lds / 8);
     hipError_t e = allow_lds((const void *)k_batched, lds);
     if (e != hipSuccess) return e;
