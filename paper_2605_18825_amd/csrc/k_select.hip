@@ -2245,12 +2245,21 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
         uint32_t *wq = reinterpret_cast<uint32_t *>(sh_dyn) + (tid / SAE_WAVE) * 2 * 3 * BATCH_LQ;
         uint32_t nq0 = 0, nq1 = 0;  // fill of the log-normal and structural lists (wave-uniform)
         const unsigned long long lt = lanemask_lt();
-        auto finish = [&](int b, uint32_t m, uint32_t key, bool ev) {
+        // the queues of each list's kind and of the kinds scored in place
+        // (bit q): a block's counts only touch those
+        uint32_t qm_ln = 0, qm_st = 0;
+        for (int qq = 0; qq < Q; ++qq) {
+            qm_ln |= (tab.kind[qq] == SAE_KIND_LOGNORMAL) ? 1u << qq : 0u;
+            qm_st |= (tab.kind[qq] == SAE_KIND_STRUCTURAL) ? 1u << qq : 0u;
+        }
+        const uint32_t qm_rest = ((1u << Q) - 1u) & ~(qm_ln | qm_st);
+        auto finish = [&](int b, uint32_t m, uint32_t key, bool ev, uint32_t qmask) {
             const int q = meta_queue(m);
             if (ev) {
 #pragma unroll
                 for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
                     if (qq >= Q) break;  // uniform
+                    if (!((qmask >> qq) & 1u)) continue;  // uniform
                     cnt_r[qq] += (qq == q) ? 1u : 0u;
                     mn_r[qq] = (qq == q) ? min(mn_r[qq], key) : mn_r[qq];
                     mx_r[qq] = (qq == q) ? max(mx_r[qq], key) : mx_r[qq];
@@ -2278,7 +2287,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
                 if (act) {
                     const uint32_t key = which == 0 ? key_lognormal(a.now, la, m, tab, st)
                                                     : key_structural(a.now, la, m, off, tab, st);
-                    finish((int)(mb >> 16), m, key, true);
+                    finish((int)(mb >> 16), m, key, true, which == 0 ? qm_ln : qm_st);
                 }
             }
         };
@@ -2313,7 +2322,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_batched(DevCtx c, SelectArgs a,
                 const bool ev = in && meta_evictable(m) && meta_queue(m) < Q;
                 const int kind = ev ? tab.kind[meta_queue(m)] : -1;
                 const bool to0 = kind == SAE_KIND_LOGNORMAL, to1 = kind == SAE_KIND_STRUCTURAL;
-                if (in && !to0 && !to1) finish(b, m, ev ? key_cheap(kind, a.now, la, m, tab, st) : 0u, ev);
+                if (in && !to0 && !to1) finish(b, m, ev ? key_cheap(kind, a.now, la, m, tab, st) : 0u, ev, qm_rest);
                 const unsigned long long m0 = __ballot(to0), m1 = __ballot(to1);
                 if (to0 || to1) {
                     const uint32_t p = to0 ? nq0 + (uint32_t)__popcll(m0 & lt) : nq1 + (uint32_t)__popcll(m1 & lt);
