@@ -193,6 +193,26 @@ def test_nothing_evictable_and_all_evictable():
         p.close()
 
 
+@pytest.mark.parametrize("n", [1, 3, 63, 65, 1025])
+def test_very_small_pools(n):
+    """Pools of a few blocks, every queue kind present (evict-first,
+    structural with gamma != 1, two log-normal, recency): the batched
+    engine's first pass then ends with short per-wave scoring lists and
+    lanes past the pool, the scan's with a partial batch; every engine and
+    the exact path equal the oracle for k = 1, 2 and the largest k."""
+    kinds, mu, sigma = [0, 1, 2, 2, 3], [0, 0, 11.7, 9.2, 0], [1, 1, 1.25, 1.34, 1]
+    cfg = synth.pool_config("tiny", kinds=kinds, mix=[0.15, 0.3, 0.2, 0.2, 0.15], mu=mu, sigma=sigma)
+    pool = synth.make_pool(cfg, n_blocks=n, seed=4242 + n)
+    p = Pair(kinds, pool, 64, mu=mu, sigma=sigma, gamma=0.8)
+    try:
+        for flags in (api.SS_ENGINE_BATCHED, api.SS_ENGINE_SCAN, api.SS_FORCE_FALLBACK):
+            for k in (1, 2, 64):
+                p.select(pool["now"], k, flags)
+        assert p.status() in ([], ["SELECT_FALLBACK"])  # the forced exact path reports itself
+    finally:
+        p.close()
+
+
 def test_ties_and_recent_blocks():
     """Many identical scores (same dt, type, offsets) and blocks touched at
     `now` (dt = 0, score +inf): ties go to the lower block id."""
