@@ -355,6 +355,30 @@ sae_status sae_score_select(sae_ctx *ctx, int32_t now, int32_t k, const int32_t 
                             uint32_t flags, int32_t *victims, float *scores, int32_t *count,
                             int32_t *decision, int32_t *decision_count, sae_stream_t stream);
 
+/*
+ * HOT 1 + HOT 2 — a serving step's prefix match and eviction as one call
+ * (Sec. 2.1, then Sec. 3.1 and Algorithm 1 on the pool the match left).
+ * Same arguments, checks, errors and results as sae_prefix_match(ctx, n_req,
+ * max_len, hashes, lens, inst, pm_now, pm_flags, match_len, matched_ids)
+ * followed on the same stream by sae_score_select(ctx, now, k, k_per_inst,
+ * flags, victims, scores, count, decision, decision_count): every output,
+ * and every change to the pool, index and counters, is the one of those two
+ * calls in that order.  With the pool-scan engine the selection's sample of
+ * the pool and its per-queue candidate bounds are computed in the prefix
+ * match's launch, while the requests probe the index, so the step has two
+ * launches fewer on its critical path.  A sampled block may be seen before
+ * or after the match touches it; the bounds only steer the work (the exact
+ * path takes over wherever they would miss a victim, SAE_ST_SELECT_FALLBACK),
+ * so no result depends on it.  An argument error of either half fails the
+ * whole call before anything is enqueued.
+ */
+sae_status sae_match_select(sae_ctx *ctx, int32_t n_req, int32_t max_len, const uint64_t *hashes,
+                            const int32_t *lens, const int32_t *inst, int32_t pm_now, uint32_t pm_flags,
+                            int32_t *match_len, int32_t *matched_ids, int32_t now, int32_t k,
+                            const int32_t *k_per_inst, uint32_t flags, int32_t *victims, float *scores,
+                            int32_t *count, int32_t *decision, int32_t *decision_count,
+                            sae_stream_t stream);
+
 /* Flags of sae_feedback_update */
 enum { SAE_FB_FORCE = 1u << 0 };
 

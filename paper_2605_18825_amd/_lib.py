@@ -93,6 +93,8 @@ SIGNATURES = {
     "sae_ref_blocks": (_I32, [_P, _I32, _P, _P, _I32, _P]),
     "sae_prefix_match": (_I32, [_P, _I32, _I32, _P, _P, _P, _I32, _U32, _P, _P, _P]),
     "sae_score_select": (_I32, [_P, _I32, _I32, _P, _U32, _P, _P, _P, _P, _P, _P]),
+    "sae_match_select": (_I32, [_P, _I32, _I32, _P, _P, _P, _I32, _U32, _P, _P, _I32, _I32, _P, _U32, _P, _P, _P, _P,
+                                _P, _P]),
     "sae_feedback_update": (_I32, [_P, _U32, _P]),
     "sae_poll_status": (_I32, [_P, _P, ctypes.POINTER(_U32)]),
     "sae_get_intervals": (_I32, [_P, _I32, _I32, _P, _I32, ctypes.POINTER(_I32), _P]),

@@ -200,6 +200,16 @@ def sae_score_select(ctx, now, k, flags, victims, count, decision, decision_coun
                                              _stream(stream)))
 
 
+def sae_match_select(ctx, hashes, lens, pm_now, pm_flags, match_len, now, k, flags, victims, count, decision,
+                     decision_count, matched_ids=None, inst=None, scores=None, k_per_inst=None, stream=None):
+    """sae_prefix_match then sae_score_select, as one call (same results)."""
+    n_req, max_len = hashes.shape
+    _check(ctx, _lib.load().sae_match_select(ctx, n_req, max_len, _ptr(hashes), _ptr(lens), _ptr(inst), int(pm_now),
+                                             int(pm_flags), _ptr(match_len), _ptr(matched_ids), int(now), int(k),
+                                             _ptr(k_per_inst), int(flags), _ptr(victims), _ptr(scores), _ptr(count),
+                                             _ptr(decision), _ptr(decision_count), _stream(stream)))
+
+
 def sae_feedback_update(ctx, flags=0, stream=None):
     _check(ctx, _lib.load().sae_feedback_update(ctx, int(flags), _stream(stream)))
 

@@ -15,44 +15,11 @@
 // ring once stale and deleted slots reach a quarter of it, so a commit only
 // inserts.
 #include "sae_internal.h"
+#include "pm_match.h"
 
 namespace {
 
 constexpr int kThreads = 256;
-
-// Lookup by linear probing from the home slot.  The probe order is the plain
-// one (home, home + 1, ...), but slots are fetched a whole aligned group of
-// IDX_GROUP (one 128-byte line) at a time, with every load of the group in
-// flight together, so a lookup usually costs one memory round trip.  Tables
-// hold at least 64 slots, a multiple of IDX_GROUP.
-#define IDX_GROUP 8
-__device__ __forceinline__ int index_find(const IndexSlot *tab, uint32_t mask, unsigned long long h, uint32_t *tq)
-{
-    const uint4 *t4 = reinterpret_cast<const uint4 *>(tab);
-    if (SAE_HASH_RESERVED(h)) return -1;
-    const int lim = (int)(mask + 1 < (uint32_t)SAE_MAX_PROBES ? mask + 1 : (uint32_t)SAE_MAX_PROBES);
-    uint32_t s = hash_home(h, mask);
-    int seen = 0;
-    while (seen < lim) {
-        const uint32_t g = s & ~(uint32_t)(IDX_GROUP - 1);
-        uint4 v[IDX_GROUP];
-#pragma unroll
-        for (int t = 0; t < IDX_GROUP; ++t) v[t] = t4[g + t];
-#pragma unroll
-        for (int t = 0; t < IDX_GROUP; ++t) {
-            if ((uint32_t)t < s - g || seen >= lim) continue;
-            ++seen;
-            const unsigned long long vh = (unsigned long long)v[t].x | ((unsigned long long)v[t].y << 32);
-            if (vh == h) {
-                *tq = v[t].w;
-                return (int32_t)v[t].z;
-            }
-            if (vh == SAE_EMPTY_HASH) return -1;
-        }
-        s = (g + IDX_GROUP) & mask;
-    }
-    return -1;
-}
 
 __device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsigned long long h, int32_t id,
                                              uint32_t tq)
@@ -390,193 +357,13 @@ __global__ void k_ref_b(DevCtx c, int n, const int32_t *inst_a, const int32_t *i
     else meta_and(c.meta, g, (uint32_t)(~SAE_META_REF) & 0xFFFFu);
 }
 
-// Counter field of the prefix match's f-th hit count: queues, then positional
-// bins, then block types.
-__device__ __forceinline__ int pm_field(int f)
+// One wave per request, kThreads per workgroup (prefix_match_wg).
+__global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, PmArgs pa)
 {
-    if (f < SAE_MAX_QUEUES) return SAE_CF_HITS + f;
-    if (f < SAE_MAX_QUEUES + SAE_N_BINS) return SAE_CF_BHITS + (f - SAE_MAX_QUEUES);
-    return SAE_CF_THITS + (f - SAE_MAX_QUEUES - SAE_N_BINS);
+    __shared__ PmShared<kThreads> sh;
+    prefix_match_wg<kThreads>(c, blockIdx.x, pa, sh);
 }
 
-// ---------------------------------------------------------------------------
-// Strict prefix matching, one wave per request.  Lanes probe 64 consecutive
-// hashes; the lowest missing lane ends the match and no later chunk is probed.
-// queue_hits (and the positional-bin hits of structural blocks) are summed per
-// workgroup in LDS (when its requests share an instance) and added into one
-// striped counter copy.
-// With SAE_PM_INTERVALS the request also finds, per log-normal queue, its
-// deepest matched block and stores now - last_access of it (Algorithm 4's
-// reuse interval, 0 when none) in pm_rec[r]; no block is touched here, so
-// every last_access read is the one from before the call, and k_pm_place
-// touches afterwards.
-#ifndef PM_FIRST
-#define PM_FIRST 8  // hashes of a request's first probe round
-#endif
-static_assert(PM_FIRST >= 1 && PM_FIRST <= SAE_WAVE, "the first round fits a wave");
-__global__ void __launch_bounds__(kThreads) k_prefix_match(DevCtx c, int n_req, int max_len, const uint64_t *hashes,
-                                                          const int32_t *lens, const int32_t *inst_a, int32_t now,
-                                                          uint32_t flags, int32_t *match_len, int32_t *matched_ids)
-{
-    constexpr int NC = SAE_MAX_QUEUES + SAE_N_BINS + SAE_N_TYPES;  // queue, bin and type hits
-    __shared__ int32_t winst[kThreads / SAE_WAVE];
-    __shared__ uint32_t wg_hits[NC];
-    const int lane = (int)__lane_id();
-    const int wave = threadIdx.x / SAE_WAVE;
-    const int r = (blockIdx.x * blockDim.x + threadIdx.x) / SAE_WAVE;
-    const bool active = r < n_req;
-    const bool intervals = (flags & SAE_PM_INTERVALS) != 0;
-    const bool touch = (flags & SAE_PM_TOUCH) && !intervals;
-    int inst = (active && inst_a) ? inst_a[r] : 0;
-    const bool inst_ok = inst >= 0 && inst < c.n_inst;
-    // positional-bin hits are gathered only while the decay-power learner is on
-    const uint32_t ilearn = (active && inst_ok) ? c.state[inst].learn : 0u;
-    const bool bins = (flags & SAE_PM_STATS) && c.struct_mask && (ilearn & SAE_LEARN_DECAY_POWER);
-    // hits per block type are gathered only for the text-form token rule
-    const bool types = (flags & SAE_PM_STATS) && (ilearn & SAE_LEARN_TOKEN_EMA);
-    if (threadIdx.x < NC) wg_hits[threadIdx.x] = 0;
-    if (lane == 0) winst[wave] = (active && inst_ok) ? inst : -1;
-    uint32_t qcount[NC];
-#pragma unroll
-    for (int q = 0; q < NC; ++q) qcount[q] = 0;
-    int32_t deep[SAE_MAX_QUEUES];  // deepest matched block per log-normal queue (-1: none)
-#pragma unroll
-    for (int q = 0; q < SAE_MAX_QUEUES; ++q) deep[q] = -1;
-    if (active) {
-        int32_t *mid = matched_ids ? matched_ids + (long long)r * max_len : nullptr;
-        // the first two rounds' hashes are loaded with the length (indices
-        // clamped into the row, so in bounds whatever the length): one round
-        // trip before the first probe instead of two
-        const uint64_t *hr = hashes + (long long)r * max_len;
-        const unsigned long long h0 = hr[lane < max_len ? lane : max_len - 1];
-        const unsigned long long h1 = hr[PM_FIRST + lane < max_len ? PM_FIRST + lane : max_len - 1];
-        int len = lens[r];
-        if (len > max_len) len = max_len;
-        if (len < 0) len = 0;
-        if (!inst_ok) {
-            if (mid)
-                for (int j = lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
-            if (lane == 0) {
-                match_len[r] = 0;
-                set_status(c.status, SAE_ST_BAD_BLOCK);
-            }
-        } else {
-            const IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-            const long long base = (long long)inst * c.N;
-            int m = 0;
-            int j0 = 0;
-            // Rounds of hashes: the first PM_FIRST, then 64 at a time.  The
-            // index slot carries the block's queue, type and positional bin,
-            // so a round costs one round trip (its probe); the next round's
-            // hashes come with this round's probe.  A short first round spares
-            // the probes past an early miss (most requests that miss, miss
-            // early) for one more round trip on the long matches.
-            int w = PM_FIRST;  // lanes of this round
-            uint32_t tq = 0;
-            int32_t id = (lane < w && lane < len) ? index_find(tab, c.index_mask, h0, &tq) : -1;
-            unsigned long long hnext = (w + lane < len) ? h1 : 0ull;
-            while (j0 < len) {  // uniform
-                const int j = j0 + lane;
-                const bool inr = lane < w && j < len;
-                const bool miss = inr && (id < 0);
-                const unsigned long long mm = __ballot(miss);
-                const int first = mm ? (__ffsll((long long)mm) - 1) : w;
-                const int lim = min(first, len - j0);
-                const bool hit = lane < lim;
-                int q = 0, ty = 0;
-                uint32_t bin = 0;
-                if (hit) {
-                    const long long g = base + id;
-                    q = (int)((tq >> 3) & 7u);
-                    ty = (int)(tq & 7u);
-                    if (bins && ((c.struct_mask >> q) & 1u)) bin = tq >> SAE_TQ_BIN_SHIFT;
-                    if (touch) {
-                        c.la[g] = now;
-                        atomicAdd(&c.access_count[g], 1);
-                    }
-                    if (mid) mid[j] = id;
-                } else if (mid && lane < w && j < max_len) {
-                    mid[j] = -1;
-                }
-                if (flags & SAE_PM_STATS) {
-#pragma unroll
-                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
-                        qcount[qq] += (uint32_t)__popcll(__ballot(hit && q == qq));
-                    if (bins) {
-                        const bool sh = hit && ((c.struct_mask >> q) & 1u);
-#pragma unroll
-                        for (int bb = 0; bb < SAE_N_BINS; ++bb)
-                            qcount[SAE_MAX_QUEUES + bb] += (uint32_t)__popcll(__ballot(sh && bin == (uint32_t)bb));
-                    }
-                    if (types) {
-#pragma unroll
-                        for (int tt = 0; tt < SAE_N_TYPES; ++tt)
-                            qcount[SAE_MAX_QUEUES + SAE_N_BINS + tt] += (uint32_t)__popcll(__ballot(hit && ty == tt));
-                    }
-                }
-                if (intervals) {
-#pragma unroll
-                    for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
-                        if (!((c.ln_mask >> qq) & 1u)) continue;
-                        const unsigned long long bm = __ballot(hit && q == qq);
-                        if (bm) deep[qq] = __shfl(id, 63 - __clzll((long long)bm));
-                    }
-                }
-                m = j0 + lim;
-                j0 += w;
-                if (mm || j0 >= len) break;  // uniform
-                // this round matched whole: probe the next 64
-                w = SAE_WAVE;
-                const int jn = j0 + lane;
-                id = (jn < len) ? index_find(tab, c.index_mask, hnext, &tq) : -1;
-                hnext = (jn + SAE_WAVE < len) ? hr[jn + SAE_WAVE] : 0ull;
-            }
-            if (mid)
-                for (int j = j0 + lane; j < max_len; j += SAE_WAVE) mid[j] = -1;
-            if (lane == 0) match_len[r] = m;
-            if (intervals && lane < SAE_MAX_QUEUES) {
-                int32_t b = -1;
-#pragma unroll
-                for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq)
-                    if (lane == qq) b = deep[qq];
-                int32_t rec = 0;
-                if (b >= 0) {
-                    const long long dt = (long long)now - (long long)c.la[base + b];
-                    if (dt >= 1 && dt <= 0x7FFFFFFFll) rec = (int32_t)dt;
-                }
-                c.pm_rec[(long long)r * SAE_MAX_QUEUES + lane] = rec;
-            }
-        }
-        if (intervals && !inst_ok && lane < SAE_MAX_QUEUES) c.pm_rec[(long long)r * SAE_MAX_QUEUES + lane] = 0;
-    }
-    __syncthreads();
-    if (!(flags & SAE_PM_STATS)) return;
-    // one instance for the whole workgroup?  then sum in LDS
-    int i0 = -1;
-    bool uniform = true;
-    for (int w = 0; w < kThreads / SAE_WAVE; ++w) {
-        const int v = winst[w];
-        if (v < 0) continue;
-        if (i0 < 0) i0 = v;
-        else if (v != i0) uniform = false;
-    }
-    if (i0 < 0) return;
-    if (uniform) {
-        if (lane == 0 && active && inst_ok)
-#pragma unroll
-            for (int qq = 0; qq < NC; ++qq)
-                if (qcount[qq]) atomicAdd(&wg_hits[qq], qcount[qq]);
-        __syncthreads();
-        const int f = threadIdx.x;
-        if (f < NC && wg_hits[f] && (f >= SAE_MAX_QUEUES || f < c.Q))
-            atomicAdd(counter_slot(c, i0, blockIdx.x) + pm_field(f), (int)wg_hits[f]);
-    } else if (lane == 0 && active && inst_ok) {
-        int32_t *cs = counter_slot(c, inst, blockIdx.x);
-#pragma unroll
-        for (int f = 0; f < NC; ++f)
-            if (qcount[f] && (f >= SAE_MAX_QUEUES || f < c.Q)) atomicAdd(cs + pm_field(f), (int)qcount[f]);
-    }
-}
 
 // Second pass of a prefix match with SAE_PM_INTERVALS, 1024 threads per
 // workgroup.  Workgroups 0 .. n_inst-1 append instance i's intervals to its
@@ -802,22 +589,28 @@ hipError_t launch_ref(const DevCtx &c, int32_t n, const int32_t *inst, const int
     return hipGetLastError();
 }
 
+hipError_t launch_pm_place(const DevCtx &c, int32_t n_req, int32_t max_len, const int32_t *inst, int32_t now,
+                           uint32_t flags, const int32_t *matched_ids, hipStream_t s)
+{
+    long long tg = 0;
+    if (flags & SAE_PM_TOUCH) tg = ((long long)n_req * max_len + kPlaceThreads - 1) / kPlaceThreads;
+    if (tg > 1024) tg = 1024;
+    hipLaunchKernelGGL(k_pm_place, dim3((unsigned)(c.n_inst + tg)), dim3(kPlaceThreads), 0, s, c, n_req, max_len,
+                       inst, now, flags, matched_ids);
+    return hipGetLastError();
+}
+
 hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, const uint64_t *hashes,
                                const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
                                int32_t *match_len, int32_t *matched_ids, hipStream_t s)
 {
     if (n_req <= 0) return hipSuccess;
-    long long threads = (long long)n_req * SAE_WAVE;
-    hipLaunchKernelGGL(k_prefix_match, dim3(grid_for(threads)), dim3(kThreads), 0, s, c, n_req, max_len, hashes, lens,
-                       inst, now, flags, match_len, matched_ids);
+    const long long threads = (long long)n_req * SAE_WAVE;
+    const PmArgs pa = {n_req, max_len, hashes, lens, inst, now, flags, match_len, matched_ids};
+    hipLaunchKernelGGL(k_prefix_match, dim3(grid_for(threads)), dim3(kThreads), 0, s, c, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(flags & SAE_PM_INTERVALS)) return e;
-    long long tg = 0;
-    if (flags & SAE_PM_TOUCH) tg = ((long long)n_req * max_len + kPlaceThreads - 1) / kPlaceThreads;
-    if (tg > 1024) tg = 1024;
-    hipLaunchKernelGGL(k_pm_place, dim3((unsigned)(c.n_inst + tg)), dim3(kPlaceThreads), 0, s, c, n_req, max_len,
-                       inst, now, flags, (const int32_t *)matched_ids);
-    return hipGetLastError();
+    return launch_pm_place(c, n_req, max_len, inst, now, flags, matched_ids, s);
 }
 
 hipError_t launch_commit(const DevCtx &c, const SelectArgs &a, hipStream_t s)

@@ -17,6 +17,7 @@
 #include <hip/hip_ext.h>
 
 #include "sae_internal.h"
+#include "pm_match.h"
 
 #define SCAN_THREADS 256
 #define SEL_THREADS 1024
@@ -703,28 +704,40 @@ __device__ unsigned long long lds_select_rank(const unsigned long long *el, int 
 // SAMPLE_WGS * SAMPLE_CHUNK / 4 groups of four consecutive blocks spread
 // evenly over it: a sample without long runs of consecutive ids keeps the
 // buckets of an id-ordered queue (equal keys) small.
-static_assert(SCAN_THREADS == SAMPLE_CHUNK, "one sampled block per thread");
-__global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
+struct SampleShared {
+    ScoreTab tab;
+    unsigned long long tmp[SAMPLE_CHUNK];
+    uint8_t tq[SAMPLE_CHUNK];
+    uint32_t qcnt[SAE_MAX_QUEUES], qoff[SAE_MAX_QUEUES], qfill[SAE_MAX_QUEUES];
+    uint32_t pos_s, st_s;
+};
+
+// Chunk `chunk` of instance inst, one sampled block per thread t = 0 ..
+// SAMPLE_CHUNK - 1 of a part of the workgroup.  Every thread of the workgroup
+// calls (the barriers are the workgroup's), each part with its own chunk and
+// shared state; a part with active false only takes the barriers.
+__device__ void sample_chunk(const DevCtx &c, const SelectArgs &a, int inst, int chunk, int t, SampleShared &sh,
+                             bool active = true)
 {
-    __shared__ ScoreTab tab;
-    __shared__ unsigned long long tmp[SAMPLE_CHUNK];
-    __shared__ uint8_t tq[SAMPLE_CHUNK];
-    __shared__ uint32_t qcnt[SAE_MAX_QUEUES], qoff[SAE_MAX_QUEUES], qfill[SAE_MAX_QUEUES];
-    __shared__ uint32_t pos_s, st_s;
-    const int inst = blockIdx.y;
-    const int chunk = blockIdx.x;
+    ScoreTab &tab = sh.tab;
+    unsigned long long *tmp = sh.tmp;
+    uint8_t *tq = sh.tq;
+    uint32_t *qcnt = sh.qcnt, *qoff = sh.qoff, *qfill = sh.qfill;
+    uint32_t &pos_s = sh.pos_s, &st_s = sh.st_s;
     const int Q = c.Q;
     const long long N = c.N;
     const long long base = (long long)inst * N;
     long long b = -1;
-    if (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) {
+    if (!active) {
+        // no block
+    } else if (N <= (long long)SAMPLE_WGS * SAMPLE_CHUNK) {
         const long long start = ((long long)chunk * N) / SAMPLE_WGS;
         const long long end = (((long long)chunk + 1) * N) / SAMPLE_WGS;  // end - start <= SAMPLE_CHUNK
-        if (start + threadIdx.x < end) b = start + threadIdx.x;
+        if (start + t < end) b = start + t;
     } else {
         const long long G = (long long)SAMPLE_WGS * SAMPLE_CHUNK / 4;
-        const long long g = (long long)chunk * (SAMPLE_CHUNK / 4) + (threadIdx.x >> 2);
-        b = (g * N) / G + (threadIdx.x & 3);  // N / G > 4, so b < N
+        const long long g = (long long)chunk * (SAMPLE_CHUNK / 4) + (t >> 2);
+        b = (g * N) / G + (t & 3);  // N / G > 4, so b < N
     }
     uint32_t m = 0, off = 0;
     int32_t la = 0;
@@ -733,12 +746,12 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
         la = c.la[base + b];
         off = c.off[base + b];
     }
-    load_score_tab(tab, c.state[inst], c);
-    if (threadIdx.x < SAE_MAX_QUEUES) {
-        qcnt[threadIdx.x] = 0;
-        qfill[threadIdx.x] = 0;
+    load_score_tab(tab, c.state[inst], c, t);
+    if (t < SAE_MAX_QUEUES) {
+        qcnt[t] = 0;
+        qfill[t] = 0;
     }
-    if (threadIdx.x == 0) {
+    if (t == 0) {
         pos_s = 0;
         st_s = 0;
     }
@@ -754,25 +767,32 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
     }
     if (st) atomicOr(&st_s, st);
     lds_barrier();
-    if (threadIdx.x == 0) {
+    if (t == 0) {
         uint32_t o = 0;
         for (int qq = 0; qq < SAE_MAX_QUEUES; ++qq) {
             qoff[qq] = o;
             o += qcnt[qq];
         }
     }
-    if (threadIdx.x < SAE_MAX_QUEUES)
-        c.samp_qn[((long long)inst * SAMPLE_WGS + chunk) * SAE_MAX_QUEUES + threadIdx.x] = qcnt[threadIdx.x];
+    if (active && t < SAE_MAX_QUEUES)
+        c.samp_qn[((long long)inst * SAMPLE_WGS + chunk) * SAE_MAX_QUEUES + t] = qcnt[t];
     lds_barrier();
     // the chunk's region holds queue 0's elements, then queue 1's, ...
     const long long reg = ((long long)inst * SAMPLE_WGS + chunk) * SAMPLE_CHUNK;
     const uint32_t n = pos_s;
-    for (uint32_t p = threadIdx.x; p < n; p += blockDim.x) {
+    for (uint32_t p = t; p < n; p += SAMPLE_CHUNK) {
         const int qq = tq[p];
         const uint32_t pos = qoff[qq] + atomicAdd(&qfill[qq], 1u);
         c.samp[reg + pos] = tmp[p];
     }
-    if (threadIdx.x == 0) set_status(c.status, st_s);
+    if (t == 0) set_status(c.status, st_s);
+}
+
+static_assert(SCAN_THREADS == SAMPLE_CHUNK, "one sampled block per thread");
+__global__ void __launch_bounds__(SCAN_THREADS) k_sample(DevCtx c, SelectArgs a)
+{
+    __shared__ SampleShared sh;
+    sample_chunk(c, a, blockIdx.y, blockIdx.x, threadIdx.x, sh);
 }
 
 __device__ __forceinline__ int pow2_ge(int x)
@@ -891,16 +911,27 @@ __device__ uint32_t lognormal_dt_floor(const ScoreTab &t, int q, int ty, uint32_
 #define ALL_EST 2048.0
 static_assert(SAMPLE_WGS <= SAE_WAVE, "the chunks' counts fit one wave");
 static_assert(SAMPLE_WGS * SAMPLE_CHUNK <= LCAP, "a queue's sampled elements fit the LDS staging area");
-__global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
+struct SplitShared {
+    BoundScratch bs;
+    uint32_t cbase[SAMPLE_WGS], cpre[SAMPLE_WGS + 1], nsp_s;
+    int32_t nb_s;
+    unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s;
+    ScoreTab tab;
+};
+
+// Queue q of instance inst; el: LCAP elements of LDS.  With ready false (the
+// sample could not be waited for) the queue gets no candidates, so that the
+// exact path computes its list.  All SEL_THREADS threads call.
+__device__ void split_queue(const DevCtx &c, const SelectArgs &a, int q, int inst, unsigned long long *el,
+                            SplitShared &sh, bool ready)
 {
-    extern __shared__ unsigned long long el[];  // [LCAP]
-    __shared__ BoundScratch bs;
-    __shared__ uint32_t cbase[SAMPLE_WGS], cpre[SAMPLE_WGS + 1], nsp_s;
-    __shared__ int32_t nb_s;
-    __shared__ unsigned long long spl[SAE_NBUCKET], spl_raw[SAE_NBUCKET], bound_s;
-    __shared__ ScoreTab tab;
-    const int q = blockIdx.x;
-    const int inst = blockIdx.y;
+    BoundScratch &bs = sh.bs;
+    uint32_t *cbase = sh.cbase, *cpre = sh.cpre;
+    uint32_t &nsp_s = sh.nsp_s;
+    int32_t &nb_s = sh.nb_s;
+    unsigned long long *spl = sh.spl, *spl_raw = sh.spl_raw;
+    unsigned long long &bound_s = sh.bound_s;
+    ScoreTab &tab = sh.tab;
     const int Q = c.Q;
     const int tid = threadIdx.x;
     const int wave = tid / SAE_WAVE;
@@ -936,7 +967,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
     }
     lds_barrier();
     const uint32_t tot = cpre[SAMPLE_WGS];  // sampled elements of this queue
-    const int kq = inst_k(a, inst, c.max_k);
+    const int kq = ready ? inst_k(a, inst, c.max_k) : 0;
     const double f = sample_fraction(c.N);
     const double est = (double)tot / f;
     const uint32_t r = bound_rank(fmin((double)kq, est), f);
@@ -1066,6 +1097,88 @@ __global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
             lim = (kb < tk) ? 0x7FFFFFFF : ((kb == tk) ? (int32_t)(ti > 0x7FFFFFFFu ? 0x7FFFFFFFu : ti) : -1);
         }
         c.eflim[(long long)inst * 16 + tid] = lim;
+    }
+}
+
+__global__ void __launch_bounds__(SEL_THREADS) k_split(DevCtx c, SelectArgs a)
+{
+    extern __shared__ unsigned long long el[];  // [LCAP]
+    __shared__ SplitShared sh;
+    split_queue(c, a, blockIdx.x, blockIdx.y, el, sh, true);
+}
+
+// A prefix match and the next selection's steps 1 and 2 in one launch of
+// SEL_THREADS-thread workgroups (one per compute unit, for their LDS), so
+// that the sampling and the bounds run while the requests probe the index.
+// Workgroups, in this order:
+//  * n_inst * PREP_SAMPLE_WGS sampling workgroups, PREP_PARTS chunks each
+//    (the rest of their threads idle: fewer chunks per compute unit keep its
+//    scattered loads few, and these workgroups end first); each adds 1 to
+//    its instance's prep_done counter once its chunks are stored;
+//  * the prefix match, per_wg >= SEL_THREADS / 64 requests per workgroup
+//    (prefix_match_wg), as many as make the whole grid fit the device at
+//    once where that takes at most 64;
+//  * n_inst * Q bound workgroups (split_queue), last, as they need the sample:
+//    each first waits until its instance's counter reaches `target` (this
+//    call's sampling done).
+// The wait ends: workgroups start in index order, so every sampling
+// workgroup has started before any bound workgroup, and none of them waits
+// on anything; a bounded spin still gives up (that queue then takes the
+// exact path) rather than wait forever.
+// The sample may see last_access from before or after a touch of the
+// concurrent prefix match.  That only moves the candidate bound, which
+// shapes the work, not the result: the final kernel checks that the
+// candidates cover every list and otherwise computes it exactly.
+#define PREP_PARTS 2                               // chunks per sampling workgroup
+#define PREP_SAMPLE_WGS (SAMPLE_WGS / PREP_PARTS)  // sampling workgroups per instance
+#define PREP_SPIN_LIMIT (1u << 18)
+static_assert(SAMPLE_WGS % PREP_PARTS == 0 && PREP_PARTS * SAMPLE_CHUNK <= SEL_THREADS, "whole sampling workgroups");
+union PrepShared {
+    SampleShared s[SEL_THREADS / SAMPLE_CHUNK];
+    SplitShared p;
+    PmShared<SEL_THREADS> m;
+};
+__global__ void __launch_bounds__(SEL_THREADS) k_match_prep(DevCtx c, SelectArgs a, PmArgs pa, uint32_t target,
+                                                            int n_pm, int per_wg)
+{
+    extern __shared__ unsigned long long el[];  // [LCAP]
+    __shared__ PrepShared sh;
+    __shared__ int32_t ready_s;
+    const int b = blockIdx.x;
+    const int ns = c.n_inst * PREP_SAMPLE_WGS;
+    if (b < ns) {
+        const int inst = b / PREP_SAMPLE_WGS, part = threadIdx.x / SAMPLE_CHUNK;
+        sample_chunk(c, a, inst, (b % PREP_SAMPLE_WGS) * PREP_PARTS + part, threadIdx.x % SAMPLE_CHUNK, sh.s[part],
+                     part < PREP_PARTS);
+        // every wave's stores reach the L2 before the barrier; thread 0's
+        // release then writes the L2 back for the other dies' caches
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __hip_atomic_fetch_add(&c.prep_done[inst], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else if (b < ns + n_pm) {
+        prefix_match_wg<SEL_THREADS, true>(c, b - ns, pa, sh.m, per_wg);
+    } else {
+        const int inst = (b - ns - n_pm) / c.Q, q = (b - ns - n_pm) % c.Q;
+        if (threadIdx.x == 0) {
+            int32_t ok = 1;
+            uint32_t spins = 0;
+            while ((int32_t)(__hip_atomic_load(&c.prep_done[inst], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
+                             target) < 0) {
+                if (++spins > PREP_SPIN_LIMIT) {
+                    ok = 0;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            ready_s = ok;
+        }
+        __syncthreads();
+        split_queue(c, a, q, inst, el, sh.p, ready_s != 0);
     }
 }
 
@@ -2851,17 +2964,40 @@ bool batched_engine_fits(const DevCtx &c)
     return lds <= 128 * 1024;
 }
 
-hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
+hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                              const PmArgs *pm, uint32_t *prep_calls)
 {
     hipError_t e;
-    // step 1: sample
-    hipLaunchKernelGGL(k_sample, dim3(SAMPLE_WGS, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    // step 2: candidate bounds, bucket upper ends, the scan's filter entries
     const size_t lds_el = (size_t)LCAP * sizeof(unsigned long long);
-    if ((e = allow_lds((const void *)k_split, lds_el)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_split, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (pm) {
+        // steps 1 and 2 in the prefix match's launch, then its second pass
+        if ((e = allow_lds((const void *)k_match_prep, lds_el)) != hipSuccess) return e;
+        // one workgroup per compute unit (LDS): the prefix-match workgroups that fit beside the others take
+        // the requests, up to 64 each
+        const long long other = (long long)c.n_inst * (PREP_SAMPLE_WGS + c.Q);
+        const long long avail = (long long)c.n_cu > other ? (long long)c.n_cu - other : 1;
+        long long per = ((long long)pm->n_req + avail - 1) / avail;
+        per = per < SEL_THREADS / SAE_WAVE ? SEL_THREADS / SAE_WAVE : (per > 64 ? 64 : per);
+        const int n_pm = (int)(((long long)pm->n_req + per - 1) / per);
+        const long long wgs = other + n_pm;
+        const uint32_t calls = *prep_calls;
+        hipLaunchKernelGGL(k_match_prep, dim3((unsigned)wgs), dim3(SEL_THREADS), lds_el, s, c, a, *pm,
+                           (calls + 1u) * (uint32_t)PREP_SAMPLE_WGS, n_pm, (int)per);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        *prep_calls = calls + 1u;  // the sampling counters have moved on
+        if (pm->flags & SAE_PM_INTERVALS) {
+            e = launch_pm_place(c, pm->n_req, pm->max_len, pm->inst, pm->now, pm->flags, pm->matched_ids, s);
+            if (e != hipSuccess) return e;
+        }
+    } else {
+        // step 1: sample
+        hipLaunchKernelGGL(k_sample, dim3(SAMPLE_WGS, c.n_inst), dim3(SCAN_THREADS), 0, s, c, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        // step 2: candidate bounds, bucket upper ends, the scan's filter entries
+        if ((e = allow_lds((const void *)k_split, lds_el)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_split, dim3(c.Q, c.n_inst), dim3(SEL_THREADS), lds_el, s, c, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     // step 3: streaming pass (with profiling, the events carry the dispatch's own start and end)
     if (ev0 && ev1)
         hipExtLaunchKernelGGL(k_scan, dim3(c.scan_gx, c.n_inst), dim3(SCAN_THREADS), 0, s, ev0, ev1, 0, c, a);

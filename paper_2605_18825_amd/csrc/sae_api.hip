@@ -23,6 +23,7 @@ struct sae_ctx {
     std::vector<void *> allocs;
     bool prof = false;
     int casc_set = 0;  // the counter set the next cascading decision uses
+    uint32_t prep_calls = 0;  // pool-scan sae_match_select calls so far (wraps)
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_used;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_free;
 };
@@ -143,6 +144,8 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
     d.n_inst = k.n_instances;
     d.N = k.blocks_per_instance;
     d.Q = k.n_queues;
+    if (hipDeviceGetAttribute(&d.n_cu, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess || d.n_cu < 1)
+        d.n_cu = 1;
     d.max_k = k.max_k;
     d.ef_queue = -1;
     for (int q = 0; q < SAE_MAX_QUEUES; ++q) d.kind[q] = (q < k.n_queues) ? k.queue_kind[q] : SAE_KIND_RECENCY;
@@ -178,6 +181,7 @@ sae_status sae_create(const sae_config *cfg, sae_ctx **out)
               dev_alloc(c, &d.cpart, I * SAE_CSLOTS * SAE_CF_STRIDE) &&
               dev_alloc(c, &d.samp, I * SAE_SAMPLE_WGS * SAE_SAMPLE_CHUNK) &&
               dev_alloc(c, &d.samp_qn, I * SAE_SAMPLE_WGS * SAE_MAX_QUEUES) &&
+              dev_alloc(c, &d.prep_done, I) &&
               dev_alloc(c, &d.sel, I * Q * d.max_k) && dev_alloc(c, &d.sel_count, I * Q) &&
               dev_alloc(c, &d.sel_stats, I * Q * 4) && dev_alloc(c, &c->skip, I * d.N) &&
               dev_alloc(c, &d.ivl, d.ln_mask ? I * Q * SAE_IVL_CAP : 0) &&
@@ -598,9 +602,10 @@ sae_status sae_ref_blocks(sae_ctx *c, int32_t n, const int32_t *inst, const int3
     return SAE_OK;
 }
 
-sae_status sae_prefix_match(sae_ctx *c, int32_t n_req, int32_t max_len, const uint64_t *hashes, const int32_t *lens,
-                            const int32_t *inst, int32_t now, uint32_t flags, int32_t *match_len,
-                            int32_t *matched_ids, sae_stream_t stream)
+namespace {
+
+sae_status pm_check(sae_ctx *c, int32_t n_req, int32_t max_len, const uint64_t *hashes, const int32_t *lens,
+                    uint32_t flags, int32_t *match_len, int32_t *matched_ids)
 {
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
     if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
@@ -615,15 +620,28 @@ sae_status sae_prefix_match(sae_ctx *c, int32_t n_req, int32_t max_len, const ui
         if (n_req > c->dc.max_req) return fail(c, SAE_ERR_ARG, "SAE_PM_INTERVALS: n_req exceeds max_requests");
     }
     if ((long long)n_req * SAE_WAVE > 0x7FFFFFFFll) return fail(c, SAE_ERR_ARG, "n_req too large");
+    return SAE_OK;
+}
+
+}  // namespace
+
+sae_status sae_prefix_match(sae_ctx *c, int32_t n_req, int32_t max_len, const uint64_t *hashes, const int32_t *lens,
+                            const int32_t *inst, int32_t now, uint32_t flags, int32_t *match_len,
+                            int32_t *matched_ids, sae_stream_t stream)
+{
+    const sae_status st = pm_check(c, n_req, max_len, hashes, lens, flags, match_len, matched_ids);
+    if (st != SAE_OK || n_req == 0) return st;
     hipError_t e = launch_prefix_match(c->dc, n_req, max_len, hashes, lens, inst, now, flags, match_len,
                                        matched_ids, S(stream));
     if (e != hipSuccess) return hip_fail(c, e, "sae_prefix_match");
     return SAE_OK;
 }
 
-sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k_per_inst, uint32_t flags,
-                            int32_t *victims, float *scores, int32_t *count, int32_t *decision,
-                            int32_t *decision_count, sae_stream_t stream)
+namespace {
+
+sae_status ss_check(sae_ctx *c, int32_t now, int32_t k, const int32_t *k_per_inst, uint32_t flags, int32_t *victims,
+                    float *scores, int32_t *count, int32_t *decision, int32_t *decision_count, SelectArgs &a,
+                    bool &batched)
 {
     if (!c) return fail(c, SAE_ERR_ARG, "ctx must be non-NULL");
     if (!c->pool_bound) return fail(c, SAE_ERR_STATE, "no pool bound");
@@ -637,7 +655,6 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
     if (!k_per_inst && (k < 0 || k > c->dc.max_k)) return fail(c, SAE_ERR_ARG, "k must be in 0..max_k");
     if (!victims || !count || !decision || !decision_count)
         return fail(c, SAE_ERR_ARG, "victims, count, decision, decision_count must be non-NULL");
-    bool batched;
     if (flags & SAE_SS_ENGINE_BATCHED) {
         if (!batched_engine_fits(c->dc))
             return fail(c, SAE_ERR_ARG, "batched engine needs <= 65536 blocks per instance and Q*max_k to fit LDS");
@@ -647,7 +664,6 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
     } else {
         batched = batched_engine_fits(c->dc) && (c->dc.n_inst >= 32 || c->dc.N <= 16384);
     }
-    SelectArgs a;
     a.now = now;
     a.k = k;
     a.k_per_inst = k_per_inst;
@@ -657,7 +673,14 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
     a.count = count;
     a.decision = decision;
     a.decision_count = decision_count;
-    hipStream_t s = S(stream);
+    return SAE_OK;
+}
+
+// The selection's launches; with pm (pool-scan engine only), the prefix match
+// pm shares the launch of the selection's sampling and bounds.
+sae_status ss_run(sae_ctx *c, const SelectArgs &a, bool batched, hipStream_t s, const PmArgs *pm)
+{
+    const uint32_t flags = a.flags;
     hipError_t e;
     if (batched) {
         e = launch_select_batched(c->dc, a, s);
@@ -676,13 +699,13 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
             e0 = pr.first;
             e1 = pr.second;
         }
-        e = launch_select_scan(c->dc, a, s, e0, e1);
+        e = launch_select_scan(c->dc, a, s, e0, e1, pm, &c->prep_calls);
     }
     if (e == hipSuccess && (flags & SAE_SS_CASCADE)) {
         e = launch_cascade(c->dc, a, s, c->casc_set);
         c->casc_set ^= 1;
     }
-    if (e != hipSuccess) return hip_fail(c, e, "sae_score_select");
+    if (e != hipSuccess) return hip_fail(c, e, pm ? "sae_match_select" : "sae_score_select");
     if (flags & SAE_SS_COMMIT) {
         e = launch_commit(c->dc, a, s);
         if (e != hipSuccess) return hip_fail(c, e, "commit");
@@ -701,6 +724,46 @@ sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k
         }
     }
     return SAE_OK;
+}
+
+}  // namespace
+
+sae_status sae_score_select(sae_ctx *c, int32_t now, int32_t k, const int32_t *k_per_inst, uint32_t flags,
+                            int32_t *victims, float *scores, int32_t *count, int32_t *decision,
+                            int32_t *decision_count, sae_stream_t stream)
+{
+    SelectArgs a;
+    bool batched = false;
+    const sae_status st =
+        ss_check(c, now, k, k_per_inst, flags, victims, scores, count, decision, decision_count, a, batched);
+    if (st != SAE_OK) return st;
+    return ss_run(c, a, batched, S(stream), nullptr);
+}
+
+sae_status sae_match_select(sae_ctx *c, int32_t n_req, int32_t max_len, const uint64_t *hashes, const int32_t *lens,
+                            const int32_t *inst, int32_t pm_now, uint32_t pm_flags, int32_t *match_len,
+                            int32_t *matched_ids, int32_t now, int32_t k, const int32_t *k_per_inst,
+                            uint32_t flags, int32_t *victims, float *scores, int32_t *count, int32_t *decision,
+                            int32_t *decision_count, sae_stream_t stream)
+{
+    sae_status st = pm_check(c, n_req, max_len, hashes, lens, pm_flags, match_len, matched_ids);
+    if (st != SAE_OK) return st;
+    SelectArgs a;
+    bool batched = false;
+    st = ss_check(c, now, k, k_per_inst, flags, victims, scores, count, decision, decision_count, a, batched);
+    if (st != SAE_OK) return st;
+    hipStream_t s = S(stream);
+    if (batched || n_req == 0) {
+        // the batched engine has no separate sampling step: the two calls in turn
+        if (n_req > 0) {
+            hipError_t e = launch_prefix_match(c->dc, n_req, max_len, hashes, lens, inst, pm_now, pm_flags, match_len,
+                                               matched_ids, s);
+            if (e != hipSuccess) return hip_fail(c, e, "sae_match_select");
+        }
+        return ss_run(c, a, batched, s, nullptr);
+    }
+    const PmArgs pm = {n_req, max_len, hashes, lens, inst, pm_now, pm_flags, match_len, matched_ids};
+    return ss_run(c, a, false, s, &pm);
 }
 
 sae_status sae_feedback_update(sae_ctx *c, uint32_t flags, sae_stream_t stream)

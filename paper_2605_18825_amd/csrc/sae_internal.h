@@ -134,6 +134,7 @@ struct DevCtx {
     int32_t *eflim;            // [n_inst][16] evict-first queue: largest candidate id per num_tokens - 1 (-1: none)
     unsigned long long *samp;  // [n_inst][SAE_SAMPLE_WGS][SAE_SAMPLE_CHUNK] sampled (key << 32 | id)
     uint32_t *samp_qn;         // [n_inst][SAE_SAMPLE_WGS][SAE_MAX_QUEUES] sampled elements per chunk and queue
+    uint32_t *prep_done;       // [n_inst] sampling workgroups of sae_match_select finished, ever (wraps)
     uint32_t *sel_stats;       // [n_inst][Q][4] last pool scan: evictable, candidates, beyond a stripe, slow path
     unsigned long long *split; // [n_inst][Q][SAE_NBUCKET] bucket upper ends, ascending; the last is thr
     int32_t *nsplit;           // [n_inst][Q] buckets (0: no candidates)
@@ -142,6 +143,7 @@ struct DevCtx {
     uint32_t *stripe_n;        // [n_inst][Q][SAE_STRIPES + 1] slots taken in each stripe (may exceed its
                                // capacity: the rest went to the overflow list), then in the overflow list
     int32_t scan_gx;           // scan workgroups per instance
+    int32_t n_cu;              // compute units of the device
     int32_t *cpart;            // [n_inst][SAE_CSLOTS][SAE_CF_STRIDE] feedback counters, striped
     unsigned long long *sel;   // [n_inst][Q][max_k]   sorted selection
     int32_t *sel_count;        // [n_inst][Q]
@@ -448,9 +450,9 @@ struct ScoreTab {
     float gamma;
 };
 
-__device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, const DevCtx &c)
+// Threads tid = 0 .. 39 of the caller's group fill the table.
+__device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, const DevCtx &c, int tid)
 {
-    int tid = threadIdx.x;
     if (tid < SAE_MAX_QUEUES * 8) {
         int q = tid >> 3, ty = tid & 7;
         t.aw[q][ty] = (ty < SAE_N_TYPES) ? s.alpha[q] * s.w[ty] : 0.0f;
@@ -461,6 +463,11 @@ __device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, 
         t.kind[tid] = c.kind[tid];
     }
     if (tid == 0) t.gamma = s.gamma;
+}
+
+__device__ __forceinline__ void load_score_tab(ScoreTab &t, const InstState &s, const DevCtx &c)
+{
+    load_score_tab(t, s, c, (int)threadIdx.x);
 }
 
 // Selection key of one block: IEEE bits of P(b) (Eq. 3), or of (float)
@@ -549,6 +556,16 @@ struct SelectArgs {
     int32_t *decision_count;
 };
 
+// Arguments of one prefix-match call (sae_prefix_match).
+struct PmArgs {
+    int n_req, max_len;
+    const uint64_t *hashes;
+    const int32_t *lens, *inst;
+    int32_t now;
+    uint32_t flags;
+    int32_t *match_len, *matched_ids;
+};
+
 hipError_t launch_block_type(const uint8_t *counts, int64_t n, uint8_t *tau, hipStream_t s);
 hipError_t launch_recipe_eval(int fn, int64_t n, const float *x, float *y, hipStream_t s);
 hipError_t launch_classify(int n, const uint8_t *hint, uint16_t *meta, const int32_t *roles, hipStream_t s);
@@ -561,10 +578,18 @@ hipError_t launch_ref(const DevCtx &c, int32_t n, const int32_t *inst, const int
 hipError_t launch_prefix_match(const DevCtx &c, int32_t n_req, int32_t max_len, const uint64_t *hashes,
                                const int32_t *lens, const int32_t *inst, int32_t now, uint32_t flags,
                                int32_t *match_len, int32_t *matched_ids, hipStream_t s);
+// Algorithm 4's placement and the touches of a prefix match with SAE_PM_INTERVALS.
+hipError_t launch_pm_place(const DevCtx &c, int32_t n_req, int32_t max_len, const int32_t *inst, int32_t now,
+                           uint32_t flags, const int32_t *matched_ids, hipStream_t s);
 hipError_t launch_ghost_rebuild(const DevCtx &c, hipStream_t s);
 hipError_t launch_index_rebuild(const DevCtx &c, hipStream_t s);
-hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s,
-                              hipEvent_t ev0, hipEvent_t ev1);
+// The pool-scan engine's launches.  With pm, the prefix match pm runs first,
+// in one launch with the selection's sampling and bounds (the selection then
+// sees the pool after the prefix match, as if called after it); *prep_calls
+// counts the context's launches of that kind (the device counters they
+// advance follow it) and is incremented when one is enqueued.
+hipError_t launch_select_scan(const DevCtx &c, const SelectArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                              const PmArgs *pm = nullptr, uint32_t *prep_calls = nullptr);
 hipError_t launch_select_batched(const DevCtx &c, const SelectArgs &a, hipStream_t s);
 hipError_t launch_cascade(const DevCtx &c, const SelectArgs &a, hipStream_t s, int set);
 // Device address of the no-allocation predictor's buffer on the current device.

@@ -69,3 +69,10 @@ class SelectBuffers:
     def run(self, ctx, now, k, flags=0, k_per_inst=None, stream=None):
         api.sae_score_select(ctx, now, k, flags, self.victims, self.count, self.decision, self.decision_count,
                              scores=self.scores, k_per_inst=k_per_inst, stream=stream)
+
+    def run_after_match(self, ctx, hashes, lens, pm_now, pm_flags, match_len, now, k, flags=0, matched_ids=None,
+                        inst=None, k_per_inst=None, stream=None):
+        """A prefix match, then this selection, in one sae_match_select call."""
+        api.sae_match_select(ctx, hashes, lens, pm_now, pm_flags, match_len, now, k, flags, self.victims, self.count,
+                             self.decision, self.decision_count, matched_ids=matched_ids, inst=inst,
+                             scores=self.scores, k_per_inst=k_per_inst, stream=stream)

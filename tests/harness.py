@@ -98,48 +98,79 @@ class Pair:
         if commit:
             flags |= api.SS_COMMIT
         self.out.run(self.ctx, now, k, flags)
+        lists, key, dec = self._oracle_select(now, k, flags)
+        if check:
+            self._check_select(lists, key, dec)
+        return lists, key, dec
+
+    def _oracle_select(self, now, k, flags):
+        commit = bool(flags & api.SS_COMMIT)
         if flags & api.SS_CASCADE:
             lists, key, _ = self.oc.select_per_queue(now, k)
             dec = self.oc.decide_cascade(now, k)
             if commit:
                 self.oc.commit(dec)
-        else:
-            lists, key, dec = self.oc.score_select(now, k, commit=commit)
-        if check:
-            torch.cuda.synchronize()
-            cnt = self.out.count[0].cpu().numpy()
-            vic = self.out.victims[0].cpu().numpy()
-            sc = self.out.scores[0].cpu().numpy().view(np.uint32)
-            for q in range(self.Q):
-                c = int(cnt[q])
-                want = lists[q]
-                assert c == len(want), "queue %d: count %d vs oracle %d" % (q, c, len(want))
-                got = vic[q, :c]
-                if not np.array_equal(got, want):
-                    bad = np.nonzero(got != want)[0][0]
-                    raise AssertionError("queue %d: first difference at position %d: gpu %d (key %08x) vs oracle %d "
-                                         "(key %08x)" % (q, bad, got[bad], sc[q, bad], want[bad], key[want[bad]]))
-                assert np.array_equal(sc[q, :c], key[want]), "queue %d: score bits differ" % q
-            d = int(self.out.decision_count[0])
-            assert d == len(dec), "decision size %d vs %d" % (d, len(dec))
-            assert np.array_equal(self.out.decision[0, :d].cpu().numpy(), dec), "decision differs"
-        return lists, key, dec
+            return lists, key, dec
+        return self.oc.score_select(now, k, commit=commit)
 
-    def prefix_match(self, hashes, lens, now, flags, check=True):
+    def _check_select(self, lists, key, dec):
+        torch.cuda.synchronize()
+        cnt = self.out.count[0].cpu().numpy()
+        vic = self.out.victims[0].cpu().numpy()
+        sc = self.out.scores[0].cpu().numpy().view(np.uint32)
+        for q in range(self.Q):
+            c = int(cnt[q])
+            want = lists[q]
+            assert c == len(want), "queue %d: count %d vs oracle %d" % (q, c, len(want))
+            got = vic[q, :c]
+            if not np.array_equal(got, want):
+                bad = np.nonzero(got != want)[0][0]
+                raise AssertionError("queue %d: first difference at position %d: gpu %d (key %08x) vs oracle %d "
+                                     "(key %08x)" % (q, bad, got[bad], sc[q, bad], want[bad], key[want[bad]]))
+            assert np.array_equal(sc[q, :c], key[want]), "queue %d: score bits differ" % q
+        d = int(self.out.decision_count[0])
+        assert d == len(dec), "decision size %d vs %d" % (d, len(dec))
+        assert np.array_equal(self.out.decision[0, :d].cpu().numpy(), dec), "decision differs"
+
+    def _pm_buffers(self, hashes, lens):
         R = torch.as_tensor(u64(hashes).view(np.int64)).cuda()
         L = torch.as_tensor(np.asarray(lens, np.int32)).cuda()
         ml = torch.zeros(len(lens), dtype=torch.int32, device="cuda")
         mid = torch.zeros(R.shape, dtype=torch.int32, device="cuda")
+        return R, L, ml, mid
+
+    def _oracle_pm(self, hashes, lens, now, flags):
+        return self.oc.prefix_match(hashes, lens, now, touch=bool(flags & api.PM_TOUCH),
+                                    stats=bool(flags & api.PM_STATS), intervals=bool(flags & api.PM_INTERVALS))
+
+    @staticmethod
+    def _check_pm(ml, mid, om, omid):
+        torch.cuda.synchronize()
+        g = ml.cpu().numpy()
+        assert np.array_equal(g, om), "match_len differs at %s" % np.nonzero(g != om)[0][:10]
+        assert np.array_equal(mid.cpu().numpy(), omid), "matched ids differ"
+
+    def prefix_match(self, hashes, lens, now, flags, check=True):
+        R, L, ml, mid = self._pm_buffers(hashes, lens)
         api.sae_prefix_match(self.ctx, R, L, now, flags, ml, matched_ids=mid)
-        om, omid = self.oc.prefix_match(hashes, lens, now, touch=bool(flags & api.PM_TOUCH),
-                                        stats=bool(flags & api.PM_STATS), intervals=bool(flags & api.PM_INTERVALS))
+        om, omid = self._oracle_pm(hashes, lens, now, flags)
         if check:
-            torch.cuda.synchronize()
-            g = ml.cpu().numpy()
-            assert np.array_equal(g, om), "match_len differs at %s" % np.nonzero(g != om)[0][:10]
-            gm = mid.cpu().numpy()
-            assert np.array_equal(gm, omid), "matched ids differ"
+            self._check_pm(ml, mid, om, omid)
         return om
+
+    def match_select(self, hashes, lens, pm_now, pm_flags, now, k, flags=0, commit=False):
+        """sae_match_select on the GPU; on the oracle its prefix match and then
+        its selection.  Both halves are compared as prefix_match() and
+        select() compare them."""
+        if commit:
+            flags |= api.SS_COMMIT
+        R, L, ml, mid = self._pm_buffers(hashes, lens)
+        self.out.run_after_match(self.ctx, R, L, pm_now, pm_flags, ml, now, k, flags, matched_ids=mid)
+        om, omid = self._oracle_pm(hashes, lens, pm_now, pm_flags)
+        lists, key, dec = self._oracle_select(now, k, flags)
+        self._check_pm(ml, mid, om, omid)
+        self._check_select(lists, key, dec)
+        return om, dec
 
     def insert(self, ids, hashes, parent, la, queue, counts_or_tau, ntok, ob, omax, tau_given=None):
         """Add() on both sides.  Block types: the oracle computes its own from

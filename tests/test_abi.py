@@ -76,6 +76,8 @@ def test_hot_calls_reject_null_context(lib):
     L = load()
     assert L.sae_score_select(None, 0, 1, None, 0, None, None, None, None, None, None) == -1
     assert L.sae_prefix_match(None, 1, 1, None, None, None, 0, 0, None, None, None) == -1
+    assert L.sae_match_select(None, 1, 1, None, None, None, 0, 0, None, None, 0, 1, None, 0, None, None, None, None,
+                              None, None) == -1
     assert L.sae_feedback_update(None, 0, None) == -1
     n = ctypes.c_int32()
     assert L.sae_get_intervals(None, 0, 0, None, 0, ctypes.byref(n), None) == -1

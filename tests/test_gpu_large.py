@@ -1,7 +1,8 @@
 """GPU parity at full size: 4,194,304 blocks, 5 queues, k = 4,096, and 4,096
 prefix-match requests of 128 hashes, in the launch configuration the
 benchmark times.  Every victim, score bit, decision entry, match length,
-counter and pool bit is compared with the oracle."""
+counter and pool bit is compared with the oracle, also for the prefix match
+and decision issued as one sae_match_select call."""
 import numpy as np
 import pytest
 
@@ -85,6 +86,24 @@ def test_large_match_commit_feedback(large):
     say("large: second decision")
     p.select(pool["now"] + 30, cfg["k"], commit=True)
     p.check_counters()
+
+
+def test_large_match_select(large):
+    """sae_match_select at full size, as the benchmark's step calls it: 4,096
+    requests x 128 hashes with touch and statistics, then the committed
+    decision of k = 4,096, the selection's sampling and bounds in the prefix
+    match's launch; equal to the oracle's prefix match followed by its
+    selection, twice in a row."""
+    p, pool, cfg = large
+    for j, t in enumerate((40, 50)):
+        R, L = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], 60 + j)
+        say("large: match+select %d" % j)
+        om, dec = p.match_select(R, L, pool["now"] + t, api.PM_TOUCH | api.PM_STATS, pool["now"] + t, cfg["k"],
+                                 commit=True)
+        assert om.sum() > 0 and len(dec) == cfg["k"]
+        p.check_counters()
+        p.check_pool()
+    assert set(p.status()) <= {"SELECT_FALLBACK"}
 
 
 def test_large_equal_key_clusters():
