@@ -44,7 +44,8 @@ sys.path.insert(0, ROOT)
 METRIC = "cached blocks scored+selected per sec (G blk/s) at 4M blocks; % HBM peak"
 HBM_PEAK_GBS = 8000.0
 BYTES_PER_BLOCK = 10  # last_access 4 + meta 2 + off 4: what the scoring pass must read
-PASS_KERNEL_SOURCES = ["paper_2605_18825_amd/csrc/k_select.hip", "paper_2605_18825_amd/csrc/sae_internal.h"]
+PASS_KERNEL_SOURCES = ["paper_2605_18825_amd/csrc/k_select.hip", "paper_2605_18825_amd/csrc/sae_internal.h",
+                       "paper_2605_18825_amd/csrc/pm_match.h"]
 
 
 def kernel_source_hash():
