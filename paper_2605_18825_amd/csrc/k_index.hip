@@ -40,20 +40,6 @@ __device__ __forceinline__ bool index_insert(IndexSlot *tab, uint32_t mask, unsi
     return false;
 }
 
-__device__ __forceinline__ void index_erase(IndexSlot *tab, uint32_t mask, unsigned long long h)
-{
-    uint32_t s = hash_home(h, mask);
-    for (int p = 0; p <= (int)mask && p < SAE_MAX_PROBES; ++p) {
-        unsigned long long v = tab[s].hash;
-        if (v == h) {
-            tab[s].hash = SAE_TOMB_HASH;
-            return;
-        }
-        if (v == SAE_EMPTY_HASH) return;
-        s = (s + 1) & mask;
-    }
-}
-
 // index_insert with the home slot's hash already loaded, and the lookup of a
 // live, unconsumed recently_evicted entry of hash h (its table slot index, or
 // -1; *ring_pos its ring position) likewise.
@@ -264,19 +250,29 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     if (i >= n) return;
     int inst = inst_a ? inst_a[i] : 0;
     int32_t b = ids[i];
-    if (inst < 0 || inst >= c.n_inst || b < 0 || b >= c.N) {
+    const unsigned long long h = hash[i];
+    const bool ok = inst >= 0 && inst < c.n_inst && b >= 0 && b < c.N;
+    // the slot's meta and the first probes of the index and of recently_evicted
+    // go out together (addresses clamped into the instance's tables)
+    const int ic = ok ? inst : 0;
+    const long long g = (long long)ic * c.N + (ok ? b : 0);
+    IndexSlot *tab = c.index + (long long)ic * ((long long)c.index_mask + 1);
+    GhostSlot *gt = c.gtab + (long long)ic * ((long long)c.ghost_mask + 1);
+    GhostEntry *ring = c.ring + (long long)ic * c.ring_cap;
+    const uint32_t si = hash_home(h, c.index_mask), sg = hash_home(h, c.ghost_mask);
+    const uint32_t mg = c.meta[g];
+    const unsigned long long vi = tab[si].hash, vg = gt[sg].hash;
+    if (!ok) {
         skip[i] = 1;
         set_status(c.status, SAE_ST_BAD_BLOCK);
         return;
     }
-    long long g = (long long)inst * c.N + b;
-    unsigned long long h = hash[i];
     if (SAE_HASH_RESERVED(h)) {
         skip[i] = 1;
         set_status(c.status, SAE_ST_BAD_HASH);
         return;
     }
-    if (c.meta[g] & SAE_META_VALID) {
+    if (mg & SAE_META_VALID) {
         skip[i] = 1;
         set_status(c.status, SAE_ST_SLOT_BUSY);
         return;
@@ -291,12 +287,6 @@ __global__ void k_insert_a(DevCtx c, int n, const int32_t *inst_a, const int32_t
     c.child_count[g] = 0;
     c.ref_count[g] = 0;
     c.access_count[g] = 0;
-    IndexSlot *tab = c.index + (long long)inst * ((long long)c.index_mask + 1);
-    GhostSlot *gt = c.gtab + (long long)inst * ((long long)c.ghost_mask + 1);
-    GhostEntry *ring = c.ring + (long long)inst * c.ring_cap;
-    // the first probes of the index and of recently_evicted go out together
-    const uint32_t si = hash_home(h, c.index_mask), sg = hash_home(h, c.ghost_mask);
-    const unsigned long long vi = tab[si].hash, vg = gt[sg].hash;
     if (!index_insert_from(tab, c.index_mask, h, b, slot_tq(m, off[i]), si, vi))
         set_status(c.status, SAE_ST_INDEX_FULL);
     int32_t *cs = counter_slot(c, inst, i);
@@ -571,11 +561,14 @@ hipError_t launch_insert(const DevCtx &c, int32_t n, const int32_t *inst, const 
                          uint8_t *skip, hipStream_t s)
 {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_insert_a, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, ids, hash, parent, la, meta,
+    // one wave per workgroup: an insert is a chain of scattered accesses, so
+    // the inserts are spread over as many compute units as possible
+    const unsigned grid = (unsigned)(((long long)n + kCommitThreads - 1) / kCommitThreads);
+    hipLaunchKernelGGL(k_insert_a, dim3(grid), dim3(kCommitThreads), 0, s, c, n, inst, ids, hash, parent, la, meta,
                        off, skip);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_insert_b, dim3(grid_for(n)), dim3(kThreads), 0, s, c, n, inst, parent, (const uint8_t *)skip);
+    hipLaunchKernelGGL(k_insert_b, dim3(grid), dim3(kCommitThreads), 0, s, c, n, inst, parent, (const uint8_t *)skip);
     return hipGetLastError();
 }
 
