@@ -20,8 +20,8 @@
  *    sae_score_select without SAE_SS_COMMIT runs, since neither writes what
  *    the other reads (the pool, the index, the parameters).
  *  - The context allocates all of its internal device memory in sae_create();
- *    the hot calls (sae_prefix_match, sae_score_select, sae_feedback_update)
- *    never allocate.
+ *    the hot calls (sae_prefix_match, sae_score_select, sae_match_select,
+ *    sae_feedback_update) never allocate.
  *  - Conditions found on the device (index full, o_b > o_max, a slot reused
  *    while still valid, last_access in the future, ...) set bits of a device
  *    status word, read by sae_poll_status().
