@@ -10,7 +10,8 @@ the selection's sampling and bounds sharing the prefix match's launch.
  * The same with every learner on and Algorithm 4's intervals recorded.
  * Edge cases on the pool-scan engine: no requests, request counts that fill
    no whole workgroup, lengths 0 / 1 / 65 / 130, the cascading decision, the
-   forced exact path, k = 1.
+   forced exact path, k = 1, the match at an earlier time than the
+   selection.
  * Four instances (k per instance, one of them 0), 3,500 requests (more
    workgroups than the device holds at once, so that prefix-match and bound
    workgroups start late) against a second context driven by
@@ -133,6 +134,11 @@ def test_edge_cases_on_the_scan_engine():
             now += 100
         say("edge: k = 1")
         p.match_select(R0[:8], L0[:8], now, PM, now, 1, flags=api.SS_ENGINE_SCAN | api.SS_COMMIT)
+        p.check_counters()
+        p.check_pool()
+        now += 100
+        say("edge: the match 40 ticks before the selection")
+        p.match_select(R0[20:], L0[20:], now - 40, PM, now, k, flags=api.SS_ENGINE_SCAN | api.SS_COMMIT)
         p.check_counters()
         p.check_pool()
         assert set(p.status()) <= {"SELECT_FALLBACK"}
