@@ -106,6 +106,33 @@ def test_large_match_select(large):
     assert set(p.status()) <= {"SELECT_FALLBACK"}
 
 
+def test_large_stage_two_decision():
+    """Full size with an evict-first queue of about 2,000 blocks, fewer than
+    k = 4,096: every decision takes all of that queue's evictable blocks and
+    fills the rest from the other queues merged by (P, id) (Algorithm 1's
+    second stage, the final kernel's union workgroups), with the pass alone
+    and with the combined call, twice in a row with commits."""
+    cfg = synth.pool_config("large", mix=[0.0005, 0.35, 0.3, 0.2, 0.1495])
+    say("stage two: generating pool")
+    pool = synth.make_pool(cfg, seed=4321)
+    p = Pair(cfg["kinds"], pool, cfg["k"], mu=cfg["mu"], sigma=cfg["sigma"], K=cfg["k"])
+    try:
+        say("stage two: score_select")
+        _, _, dec = p.select(pool["now"], cfg["k"])
+        n_ef = int(np.count_nonzero(pool["queue"] == 0))
+        assert n_ef < cfg["k"] and len(dec) == cfg["k"]
+        for j, t in enumerate((10, 20)):
+            R, L = synth.make_requests(pool["chains"], cfg["n_req"], cfg["req_len"], cfg["hit_frac"], 70 + j)
+            say("stage two: match+select %d" % j)
+            p.match_select(R, L, pool["now"] + t, api.PM_TOUCH | api.PM_STATS, pool["now"] + t, cfg["k"],
+                           commit=True)
+            p.check_counters()
+            p.check_pool()
+        assert set(p.status()) <= {"SELECT_FALLBACK"}
+    finally:
+        p.close()
+
+
 def test_large_equal_key_clusters():
     """Blocks added together share last_access, so their keys repeat: here
     last_access takes 400 values, which makes clusters of about 2,000 equal
