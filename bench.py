@@ -23,7 +23,9 @@ The JSON line also carries:
   * step_two_calls: the same step with sae_prefix_match and sae_score_select
     as two calls;
   * steady_state: the step over enough steps that the index and
-    recently-evicted tables are rebuilt as in a long run;
+    recently-evicted tables are rebuilt as in a long run; step_steady_pools:
+    the step alone on the pools that leg left (decisions mostly from
+    Algorithm 1's second stage);
   * configs: the other configurations' per-operation GPU times beside the
     oracle's host time (tiny pool, mid pool, trace replay, batched sweep),
     and the batched sweep's fixed-against-learned comparison over its full
@@ -474,6 +476,13 @@ def extra_legs(v):
                     "per cache, so each cache's index is rebuilt from its deleted slots %d times and its "
                     "recently-evicted table as often as its size calls for" % (ss_per, ss_per // 256),
         },
+        "step_steady_pools": {
+            "value": N / (v["ms_st2"] * 1e-3) / 1e9, "unit": "G blk/s", "ms_per_step": v["ms_st2"],
+            "evict_first_share_of_decision": v["ef_share"],
+            "step": "the headline step on the pools the steady-state leg left (clusters of equal keys); the "
+                    "evict-first queue then supplies only this share of each decision, the rest is Algorithm "
+                    "1's second stage",
+        },
         "predictor": {
             "value": PN / (ms_pred * 1e-3), "unit": "predictions/s", "ms_per_call": ms_pred,
             "batch": PN, "d": PD,
@@ -670,6 +679,10 @@ def main():
 
             ms_ss = timed_loop(step_insert, ss_steps, 0)
             dc_min = min(int(c["out"].decision_count[0]) for c in caches)
+            # --- the headline step on the steady-state pools (no Add()): most of each decision now comes
+            # from Algorithm 1's second stage, and the pools hold clusters of equal keys
+            ms_st2 = timed_loop(step, args.steps, args.warmup)
+            ef_share = sum(int(c["out"].count[0, 0]) for c in caches) / float(k * len(caches))
     if extra:
         note("steady state: %.3f ms/step over %d steps" % (ms_ss, ss_steps))
         ms_pred, pred_bytes, pred_flops, PN, PD = predictor_leg(api, args, R, stream)
