@@ -14,8 +14,9 @@ the selection's sampling and bounds sharing the prefix match's launch.
    selection.
  * Four instances (k per instance, one of them 0), 3,500 requests (more
    workgroups than the device holds at once, so that prefix-match and bound
-   workgroups start late) against a second context driven by
-   sae_prefix_match and sae_score_select: identical bit for bit.
+   workgroups start late), with and without Algorithm 4's interval
+   recording, against a second context driven by sae_prefix_match and
+   sae_score_select: identical bit for bit, interval buffers included.
  * A context on the batched engine (the call runs the two halves in turn).
 """
 import numpy as np
@@ -151,6 +152,7 @@ class Ctx:
 
     def __init__(self, pools, cfg, k, max_req):
         self.n_inst, self.Q = len(pools), len(cfg["kinds"])
+        self.kinds = cfg["kinds"]
         self.ctx = api.sae_create(self.n_inst, pools[0]["n_blocks"], cfg["kinds"], max_k=k, max_requests=max_req)
         self.dp = DevicePool(self.n_inst, pools[0]["n_blocks"])
         for i, pl in enumerate(pools):
@@ -172,14 +174,18 @@ class Ctx:
             c = api.sae_get_counters(self.ctx, i)
             snap["c%d" % i] = np.array(list(c.evicted) + list(c.missed) + list(c.hits) + list(c.evictions) +
                                        [c.eviction_count], np.int64)
+            for q in range(self.Q):
+                if self.kinds[q] == api.KIND_LOGNORMAL:
+                    snap["ivl%d.%d" % (i, q)] = np.array(api.sae_get_intervals(self.ctx, i, q), np.int32)
         return snap
 
 
-def test_four_instances_equal_the_two_calls():
+@pytest.mark.parametrize("pm_flags", [PM, PM | api.PM_INTERVALS], ids=["touch-stats", "with-intervals"])
+def test_four_instances_equal_the_two_calls(pm_flags):
     cfg = synth.pool_config("tiny")
     N, k, n_inst = 40000, 64, 4
     pools = [synth.make_pool(cfg, n_blocks=N, seed=900 + i) for i in range(n_inst)]
-    a, b = Ctx(pools, cfg, k, 0), Ctx(pools, cfg, k, 0)
+    a, b = Ctx(pools, cfg, k, 3500), Ctx(pools, cfg, k, 3500)
     rng = np.random.default_rng(11)
     now = max(pl["now"] for pl in pools)
     kpi = torch.tensor([k, 17, 0, 1], dtype=torch.int32, device="cuda")
@@ -201,9 +207,9 @@ def test_four_instances_equal_the_two_calls():
                 bufs.append((torch.full((len(L),), -7, dtype=torch.int32, device="cuda"),
                              torch.full(hd.shape, -7, dtype=torch.int32, device="cuda")))
             (ml_a, mid_a), (ml_b, mid_b) = bufs
-            api.sae_prefix_match(a.ctx, hd, ld, now, PM, ml_a, matched_ids=mid_a, inst=idev)
+            api.sae_prefix_match(a.ctx, hd, ld, now, pm_flags, ml_a, matched_ids=mid_a, inst=idev)
             a.out.run(a.ctx, now, k, api.SS_COMMIT | api.SS_ENGINE_SCAN, k_per_inst=kpi)
-            b.out.run_after_match(b.ctx, hd, ld, now, PM, ml_b, now, k, api.SS_COMMIT | api.SS_ENGINE_SCAN,
+            b.out.run_after_match(b.ctx, hd, ld, now, pm_flags, ml_b, now, k, api.SS_COMMIT | api.SS_ENGINE_SCAN,
                                   matched_ids=mid_b, inst=idev, k_per_inst=kpi)
             sa, sb = a.snapshot(ml_a, mid_a), b.snapshot(ml_b, mid_b)
             for key in sa:
