@@ -12,11 +12,14 @@ the selection's sampling and bounds sharing the prefix match's launch.
    no whole workgroup, lengths 0 / 1 / 65 / 130, the cascading decision, the
    forced exact path, k = 1, the match at an earlier time than the
    selection.
- * Four instances (k per instance, one of them 0), 3,500 requests (more
-   workgroups than the device holds at once, so that prefix-match and bound
-   workgroups start late), with and without Algorithm 4's interval
-   recording, against a second context driven by sae_prefix_match and
-   sae_score_select: identical bit for bit, interval buffers included.
+ * Four instances (k per instance, one of them 0), 3,500 requests, with and
+   without Algorithm 4's interval recording, against a second context
+   driven by sae_prefix_match and sae_score_select: identical bit for bit,
+   interval buffers included.
+ * 20,000 requests on one instance: 64 per prefix-match workgroup (the
+   most), more workgroups than the device holds at once, so that
+   prefix-match and bound workgroups start late; identical to the two
+   calls.
  * A context on the batched engine (the call runs the two halves in turn).
 """
 import numpy as np
@@ -191,8 +194,7 @@ def test_four_instances_equal_the_two_calls(pm_flags):
     kpi = torch.tensor([k, 17, 0, 1], dtype=torch.int32, device="cuda")
     try:
         for cyc in range(6):
-            # 3,500 requests: with the sampling and bound workgroups of four instances, more workgroups
-            # than the device holds at once
+            # 3,500 requests over four instances: prefix-match workgroups of about 33 requests each
             R, L = synth.make_requests(pools[0]["chains"], 3500, cfg["req_len"], cfg["hit_frac"], rng)
             inst = rng.integers(0, n_inst, len(L)).astype(np.int32)
             for j in range(len(L)):  # a hit request follows a chain of its own instance
@@ -220,6 +222,40 @@ def test_four_instances_equal_the_two_calls(pm_flags):
             say("four instances: cycle %d identical (%d victims)" % (cyc, int(sa["decision_count"].sum())))
             for c in (a, b):
                 api.sae_feedback_update(c.ctx, 0)
+            now += 1000
+    finally:
+        api.sae_destroy(a.ctx)
+        api.sae_destroy(b.ctx)
+
+
+def test_more_workgroups_than_the_device_holds():
+    cfg = synth.pool_config("mid")
+    pool = synth.make_pool(cfg, n_blocks=65536, seed=31)
+    k = 256
+    a, b = Ctx([pool], cfg, k, 0), Ctx([pool], cfg, k, 0)
+    rng = np.random.default_rng(12)
+    now = pool["now"]
+    try:
+        for cyc in range(3):
+            R, L = synth.make_requests(pool["chains"], 20000, 24, cfg["hit_frac"], rng)
+            hd = torch.as_tensor(u64(R).view(np.int64)).cuda()
+            ld = torch.as_tensor(L).cuda()
+            out = []
+            for c in (a, b):
+                out.append((torch.full((len(L),), -7, dtype=torch.int32, device="cuda"),
+                            torch.full(hd.shape, -7, dtype=torch.int32, device="cuda")))
+            (ml_a, mid_a), (ml_b, mid_b) = out
+            api.sae_prefix_match(a.ctx, hd, ld, now, PM, ml_a, matched_ids=mid_a)
+            a.out.run(a.ctx, now, k, api.SS_COMMIT | api.SS_ENGINE_SCAN)
+            b.out.run_after_match(b.ctx, hd, ld, now, PM, ml_b, now, k, api.SS_COMMIT | api.SS_ENGINE_SCAN,
+                                  matched_ids=mid_b)
+            sa, sb = a.snapshot(ml_a, mid_a), b.snapshot(ml_b, mid_b)
+            for key in sa:
+                if not np.array_equal(sa[key], sb[key]):
+                    bad = np.argwhere(sa[key] != sb[key])[:5].tolist()
+                    raise AssertionError("cycle %d: %s differs at %s" % (cyc, key, bad))
+            assert int(sa["ml"].sum()) > 0 and int(sa["decision_count"][0]) == k
+            say("20,000 requests: cycle %d identical (%d blocks matched)" % (cyc, int(sa["ml"].sum())))
             now += 1000
     finally:
         api.sae_destroy(a.ctx)
